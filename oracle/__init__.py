@@ -1,0 +1,205 @@
+"""Reference oracle for the NEURON-Fabric bucket reducer (ctypes over libnfo.so).
+
+TEST INFRASTRUCTURE ONLY: the test suite, the smoke entry point and the
+benchmark's CPU-baseline leg may import this package; the GPU library and its
+binding never do.  Every function takes and returns plain numpy arrays on the
+host and calls the single-threaded C++ code in nfo.cpp.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+from . import build as _build
+
+ROUTE_L, ROUTE_F, ROUTE_P = 0, 1, 2
+R_NOT_ADMITTED, R_NO_ELIGIBLE, R_VETO, R_GUARD = 1, 2, 4, 8
+R_NONFINITE, R_ZERO_WORKER, R_NORM_SPIKE, R_FORCED = 16, 32, 64, 128
+DECODE_SOFT, DECODE_MAJORITY = 0, 1
+OP_SUM, OP_MEAN = 0, 1
+
+
+class Stats(ctypes.Structure):
+    _fields_ = [("nonfinite", ctypes.c_uint64), ("sum_abs_elig", ctypes.c_double),
+                ("sum_sq", ctypes.c_double)]
+
+
+class Policy(ctypes.Structure):
+    _fields_ = [("admitted", ctypes.c_int), ("veto", ctypes.c_int),
+                ("guard_ok", ctypes.c_int), ("force_lowbit", ctypes.c_int),
+                ("decode_mode", ctypes.c_int), ("fp32_op", ctypes.c_int),
+                ("kappa", ctypes.c_double)]
+
+
+class Decision(ctypes.Structure):
+    _fields_ = [("route", ctypes.c_int32), ("reasons", ctypes.c_uint32),
+                ("scale", ctypes.c_float), ("n_eligible", ctypes.c_int64),
+                ("bytes_route", ctypes.c_double), ("bytes_fp32", ctypes.c_double)]
+
+
+STATS_DTYPE = np.dtype([("nonfinite", "<u8"), ("sum_abs_elig", "<f8"), ("sum_sq", "<f8")])
+
+_lib = None
+_P = ctypes.c_void_p
+_I64 = ctypes.c_int64
+_I32 = ctypes.c_int32
+
+
+def load(path=None):
+    """Load (building first if absent) the oracle library; returns the CDLL."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    path = path or _build.LIB
+    if not os.path.exists(path):
+        _build.build(path)
+    lib = ctypes.CDLL(path)
+    sig = {
+        "nfo_mask_from_segments": (ctypes.c_int, [_P, _P, _P, _I64, _I64, _P]),
+        "nfo_count_eligible": (_I64, [_P, _I64]),
+        "nfo_health": (None, [_P, _I64, _I32, _I64, _P, _P]),
+        "nfo_health_acc": (None, [_P, _I64, _I32, _I64, _P, _P]),
+        "nfo_scale": (ctypes.c_float, [_P, _I32, _I64]),
+        "nfo_decide": (None, [_P, _I32, _I64, _I64, _P, _P]),
+        "nfo_pack": (None, [_P, _I64, _I32, _I64, _P, _P, _I64]),
+        "nfo_counts": (None, [_P, _I64, _I32, _I64, _P]),
+        "nfo_fp32_path": (None, [_P, _I64, _I32, _I64, _I32, _P]),
+        "nfo_decode_table": (None, [_I32, _I32, _P]),
+        "nfo_output": (None, [_P, _I64, _P, _P, _P, ctypes.c_float, _I32, _P]),
+        "nfo_reduce_bucket": (ctypes.c_int, [_P, _I64, _I32, _I64, _P, _P, _P, _I64,
+                                             _P, _P, _P, _P]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+    if path == _build.LIB:
+        _lib = lib
+    return lib
+
+
+def _ptr(a):
+    return ctypes.c_void_p(a.ctypes.data) if a is not None and a.size else ctypes.c_void_p(0)
+
+
+def _grads(g):
+    g = np.asarray(g)
+    assert g.dtype == np.float32 and g.ndim == 2 and g.strides[1] == 4
+    return g, g.strides[0] // 4
+
+
+def policy(admitted=1, veto=0, guard_ok=1, force_lowbit=0, decode_mode=DECODE_SOFT,
+           fp32_op=OP_SUM, kappa=4.0):
+    return Policy(admitted, veto, guard_ok, force_lowbit, decode_mode, fp32_op, kappa)
+
+
+def mask_from_segments(off, length, eligible, n, lib=None):
+    lib = lib or load()
+    off = np.ascontiguousarray(off, dtype=np.int64)
+    length = np.ascontiguousarray(length, dtype=np.int64)
+    eligible = np.ascontiguousarray(eligible, dtype=np.uint8)
+    mask = np.zeros(max((n + 63) // 64, 1), dtype=np.uint64)
+    rc = lib.nfo_mask_from_segments(_ptr(off), _ptr(length), _ptr(eligible),
+                                    len(off), n, _ptr(mask))
+    if rc != 0:
+        raise ValueError("segment outside the bucket")
+    return mask[: (n + 63) // 64]
+
+
+def count_eligible(mask, n, lib=None):
+    lib = lib or load()
+    mask = np.ascontiguousarray(mask, dtype=np.uint64)
+    return int(lib.nfo_count_eligible(_ptr(mask), n))
+
+
+def health(g, mask, lib=None):
+    lib = lib or load()
+    g, stride = _grads(g)
+    W, n = g.shape
+    st = np.zeros(W, dtype=STATS_DTYPE)
+    lib.nfo_health(_ptr(g), stride, W, n, _ptr(np.ascontiguousarray(mask, np.uint64)), _ptr(st))
+    return st
+
+
+def health_acc(g, mask, stats, lib=None):
+    """Continue `stats` (STATS_DTYPE, length W) over the chunk g (start % 64 == 0)."""
+    lib = lib or load()
+    g, stride = _grads(g)
+    W, n = g.shape
+    lib.nfo_health_acc(_ptr(g), stride, W, n, _ptr(np.ascontiguousarray(mask, np.uint64)),
+                       _ptr(stats))
+    return stats
+
+
+def scale(stats, n_eligible, lib=None):
+    lib = lib or load()
+    st = np.ascontiguousarray(stats, dtype=STATS_DTYPE)
+    return np.float32(lib.nfo_scale(_ptr(st), len(st), n_eligible))
+
+
+def decide(stats, n, n_eligible, pol=None, lib=None):
+    lib = lib or load()
+    st = np.ascontiguousarray(stats, dtype=STATS_DTYPE)
+    d = Decision()
+    pol = pol or policy()
+    lib.nfo_decide(_ptr(st), len(st), n, n_eligible, ctypes.byref(pol), ctypes.byref(d))
+    return d
+
+
+def pack(g, mask, lib=None):
+    lib = lib or load()
+    g, stride = _grads(g)
+    W, n = g.shape
+    nw = (n + 63) // 64
+    bits = np.zeros((W, max(nw, 1)), dtype=np.uint64)
+    lib.nfo_pack(_ptr(g), stride, W, n, _ptr(np.ascontiguousarray(mask, np.uint64)),
+                 _ptr(bits), bits.shape[1])
+    return bits[:, :nw]
+
+
+def counts(bits, n, lib=None):
+    lib = lib or load()
+    bits = np.ascontiguousarray(bits, dtype=np.uint64)
+    W = bits.shape[0]
+    c = np.zeros(n, dtype=np.uint8)
+    lib.nfo_counts(_ptr(bits), bits.shape[1], W, n, _ptr(c))
+    return c
+
+
+def fp32_path(g, op=OP_SUM, lib=None):
+    lib = lib or load()
+    g, stride = _grads(g)
+    W, n = g.shape
+    y = np.zeros(n, dtype=np.float32)
+    lib.nfo_fp32_path(_ptr(g), stride, W, n, op, _ptr(y))
+    return y
+
+
+def decode_table(W, mode=DECODE_SOFT, lib=None):
+    lib = lib or load()
+    q = np.zeros(W + 1, dtype=np.float32)
+    lib.nfo_decode_table(W, mode, _ptr(q))
+    return q
+
+
+def reduce_bucket(g, mask, pol=None, lib=None):
+    """Whole bucket.  Returns dict(bits, counts, out, stats, decision)."""
+    lib = lib or load()
+    g, stride = _grads(g)
+    W, n = g.shape
+    nw = (n + 63) // 64
+    bits = np.zeros((W, max(nw, 1)), dtype=np.uint64)
+    c = np.zeros(max(n, 1), dtype=np.uint8)
+    out = np.zeros(max(n, 1), dtype=np.float32)
+    st = np.zeros(W, dtype=STATS_DTYPE)
+    d = Decision()
+    pol = pol or policy()
+    m = np.ascontiguousarray(mask, np.uint64)
+    if m.size == 0:
+        m = np.zeros(1, np.uint64)
+    rc = lib.nfo_reduce_bucket(_ptr(g), stride, W, n, _ptr(m), ctypes.byref(pol),
+                               _ptr(bits), bits.shape[1], _ptr(c), _ptr(out), _ptr(st),
+                               ctypes.byref(d))
+    if rc != 0:
+        raise ValueError("invalid arguments")
+    return dict(bits=bits[:, :nw], counts=c[:n], out=out[:n], stats=st, decision=d)

@@ -1,0 +1,264 @@
+/*
+ * nfo.cpp - reference oracle for the NEURON-Fabric bucket reducer.
+ *
+ * TEST INFRASTRUCTURE ONLY (see nfo.h).  Plain single-threaded C++: every
+ * loop visits elements in ascending order and workers in ascending order,
+ * and nothing is blocked, fused or reordered.  Build with -ffp-contract=off
+ * so that no multiply-add is contracted.
+ *
+ * Readings fixed here where the paper is silent or ambiguous:
+ *   R1  One eligibility mask per bucket, shared by all W workers: the binding
+ *       is per model and identical on every replica (§5.1, §5.3).  A
+ *       parameter absent from the binding is FP32-only (§5.1).
+ *   R2  Sign payloads are positional bitmaps, LSB-first uint64: bit j of word
+ *       k is element 64k+j; elements that are not eligible, and padding past
+ *       n, hold 0.  §6.1 speaks of bit-packed updates without a layout.
+ *   R3  The sign indicator is (g > 0): +0, -0 and NaN give 0.  §5.2 names
+ *       positive-sign indicators.
+ *   R4  Counts are uint8, so 1 <= W <= 255.
+ *   R5  One scale per bucket: the mean over workers of each worker's mean
+ *       |g| over eligible elements (§5.2 records a mean-absolute scale).
+ *       Per-worker sums in FP64 with i ascending; the combination divides
+ *       each worker sum by n_E, adds in worker order, divides by W, and
+ *       rounds to FP32 once.
+ *   R6  Decode: SOFT q_c = (2c - W) / W, the vote margin (default); MAJORITY
+ *       q_c = sign(2c - W) with a tie giving 0 (§5.2's majority voting).
+ *       Both are FP32 correctly-rounded quotients of exact integers.  The
+ *       decoded value is fl32(scale * q_c).
+ *   R7  FP32 path (§2.1 sums or averages): s = g_0, then s = fl32(s + g_w)
+ *       for w = 1..W-1 (worker order, no contraction).  SUM returns s, MEAN
+ *       returns fl32(s / W) by IEEE division.
+ *   R8  Health per worker: nonfinite count over all n; sum |g| over eligible
+ *       elements; sum g*g over all n (the FP64 product of two FP32 values is
+ *       exact).  FP64 accumulators start at +0.0.
+ *   R9  Reason bits are all evaluated every time (nfo.h lists them).
+ *   R10 Any non-finite input value in any worker sends the bucket to FP32.
+ *   R11 A worker whose eligible |g| sum is exactly 0 (n_E > 0) sends the
+ *       bucket to FP32: under R3 it would vote -1 everywhere.
+ *   R12 Norm spike: over the workers whose sum g*g is finite (at least two),
+ *       m = the lower median (sorted ascending, index floor((k-1)/2)); the
+ *       bucket spikes if some such worker has sum g*g > (kappa*kappa) * m.
+ *   R13 Route precedence: P (not admitted, or no eligible element) before
+ *       forced L, before F (veto, guard, non-finite, zero worker, spike),
+ *       before L.
+ *   R14 Modeled bytes per worker (§3.2 MGTR): FP32 = 4n; the selected route
+ *       is n_E/8 + 4 (one FP32 scale) + 4 n_F for L and 4n for F and P.
+ */
+#include "nfo.h"
+
+#include <math.h>
+#include <string.h>
+
+/* element i of the mask: R1, R2 */
+static int mask_bit(const uint64_t* mask, int64_t i) {
+  return (int)((mask[i / 64] >> (i % 64)) & 1u);
+}
+
+/* An FP32 value is non-finite when its exponent field is all ones. */
+static int is_nonfinite(float x) {
+  uint32_t u;
+  memcpy(&u, &x, sizeof u);
+  return ((u >> 23) & 0xffu) == 0xffu;
+}
+
+/* ---- a1: mask from the binding's segments (§5.1, R1, R2) ---------------- */
+int nfo_mask_from_segments(const int64_t* off, const int64_t* len,
+                           const uint8_t* eligible, int64_t nseg, int64_t n,
+                           uint64_t* mask) {
+  int64_t nwords = (n + 63) / 64;
+  for (int64_t k = 0; k < nwords; ++k) mask[k] = 0;
+  for (int64_t s = 0; s < nseg; ++s) {
+    if (off[s] < 0 || len[s] < 0 || off[s] + len[s] > n) return -1;
+    if (!eligible[s]) continue;  /* FP32-only segment: bits stay 0 */
+    for (int64_t i = off[s]; i < off[s] + len[s]; ++i)
+      mask[i / 64] |= (uint64_t)1 << (i % 64);
+  }
+  return 0;
+}
+
+int64_t nfo_count_eligible(const uint64_t* mask, int64_t n) {
+  int64_t c = 0;
+  for (int64_t i = 0; i < n; ++i) c += mask_bit(mask, i);
+  return c;
+}
+
+/* ---- a2: per-worker health (R8) ----------------------------------------- */
+void nfo_health_acc(const float* g, int64_t stride, int32_t W, int64_t n,
+                    const uint64_t* mask, nfo_stats* stats) {
+  for (int32_t w = 0; w < W; ++w) {
+    const float* row = g + (int64_t)w * stride;
+    for (int64_t i = 0; i < n; ++i) {
+      double x = (double)row[i];
+      if (is_nonfinite(row[i])) stats[w].nonfinite += 1;
+      stats[w].sum_sq += x * x;
+      if (mask_bit(mask, i)) stats[w].sum_abs_elig += fabs(x);
+    }
+  }
+}
+
+void nfo_health(const float* g, int64_t stride, int32_t W, int64_t n,
+                const uint64_t* mask, nfo_stats* stats) {
+  for (int32_t w = 0; w < W; ++w) {
+    stats[w].nonfinite = 0;
+    stats[w].sum_abs_elig = 0.0;
+    stats[w].sum_sq = 0.0;
+  }
+  nfo_health_acc(g, stride, W, n, mask, stats);
+}
+
+/* ---- a5 part 1: bucket scale (§5.2, R5) --------------------------------- */
+float nfo_scale(const nfo_stats* stats, int32_t W, int64_t n_eligible) {
+  if (n_eligible <= 0) return 0.0f;
+  double acc = 0.0;
+  for (int32_t w = 0; w < W; ++w)
+    acc += stats[w].sum_abs_elig / (double)n_eligible;
+  return (float)(acc / (double)W);
+}
+
+/* ---- a5 part 2: reasons, route and modeled bytes (§3.2, §6.4, R9-R14) --- */
+void nfo_decide(const nfo_stats* stats, int32_t W, int64_t n,
+                int64_t n_eligible, const nfo_policy* p, nfo_decision* d) {
+  uint32_t r = 0;
+  if (!p->admitted) r |= NFO_R_NOT_ADMITTED;
+  if (n_eligible == 0) r |= NFO_R_NO_ELIGIBLE;
+  if (p->veto) r |= NFO_R_VETO;
+  if (!p->guard_ok) r |= NFO_R_GUARD;
+
+  uint64_t nonfinite = 0;
+  for (int32_t w = 0; w < W; ++w) nonfinite += stats[w].nonfinite;
+  if (nonfinite > 0) r |= NFO_R_NONFINITE;
+
+  if (n_eligible > 0)
+    for (int32_t w = 0; w < W; ++w)
+      if (stats[w].sum_abs_elig == 0.0) r |= NFO_R_ZERO_WORKER;
+
+  /* R12: lower median of the finite sums of squares, by insertion sort. */
+  double fin[256];
+  int k = 0;
+  for (int32_t w = 0; w < W; ++w) {
+    double v = stats[w].sum_sq;
+    if (!isfinite(v)) continue;
+    int j = k++;
+    while (j > 0 && fin[j - 1] > v) {
+      fin[j] = fin[j - 1];
+      --j;
+    }
+    fin[j] = v;
+  }
+  if (k >= 2) {
+    double m = fin[(k - 1) / 2];
+    double thr = (p->kappa * p->kappa) * m;
+    for (int i = 0; i < k; ++i)
+      if (fin[i] > thr) r |= NFO_R_NORM_SPIKE;
+  }
+
+  int32_t route;
+  if (r & (NFO_R_NOT_ADMITTED | NFO_R_NO_ELIGIBLE)) {
+    route = NFO_ROUTE_P;
+  } else if (p->force_lowbit) {
+    route = NFO_ROUTE_L;
+    r |= NFO_R_FORCED;
+  } else if (r & (NFO_R_VETO | NFO_R_GUARD | NFO_R_NONFINITE |
+                  NFO_R_ZERO_WORKER | NFO_R_NORM_SPIKE)) {
+    route = NFO_ROUTE_F;
+  } else {
+    route = NFO_ROUTE_L;
+  }
+
+  d->route = route;
+  d->reasons = r;
+  d->scale = nfo_scale(stats, W, n_eligible);
+  d->n_eligible = n_eligible;
+  d->bytes_fp32 = 4.0 * (double)n;
+  if (route == NFO_ROUTE_L)
+    d->bytes_route = (double)n_eligible / 8.0 + 4.0 +
+                     4.0 * (double)(n - n_eligible);
+  else
+    d->bytes_route = 4.0 * (double)n;
+}
+
+/* ---- a3: write-side sign payload (§5.2, §6.1, R2, R3) ------------------- */
+void nfo_pack(const float* g, int64_t stride, int32_t W, int64_t n,
+              const uint64_t* mask, uint64_t* bits, int64_t bits_stride) {
+  int64_t nwords = (n + 63) / 64;
+  for (int32_t w = 0; w < W; ++w) {
+    const float* row = g + (int64_t)w * stride;
+    uint64_t* brow = bits + (int64_t)w * bits_stride;
+    for (int64_t k = 0; k < nwords; ++k) brow[k] = 0;
+    for (int64_t i = 0; i < n; ++i)
+      if (mask_bit(mask, i) && row[i] > 0.0f)
+        brow[i / 64] |= (uint64_t)1 << (i % 64);
+  }
+}
+
+/* ---- a6 part 1: per-coordinate sign counts (§6.1, R4) ------------------- */
+void nfo_counts(const uint64_t* bits, int64_t bits_stride, int32_t W,
+                int64_t n, uint8_t* counts) {
+  for (int64_t i = 0; i < n; ++i) {
+    int c = 0;
+    for (int32_t w = 0; w < W; ++w)
+      c += (int)((bits[(int64_t)w * bits_stride + i / 64] >> (i % 64)) & 1u);
+    counts[i] = (uint8_t)c;
+  }
+}
+
+/* ---- a4 / a7: full-precision path (§2.1, §6.1 FP32 reference, R7) ------- */
+void nfo_fp32_path(const float* g, int64_t stride, int32_t W, int64_t n,
+                   int32_t op, float* y) {
+  for (int64_t i = 0; i < n; ++i) {
+    float s = g[i];
+    for (int32_t w = 1; w < W; ++w) s = s + g[(int64_t)w * stride + i];
+    if (op == NFO_OP_MEAN) s = s / (float)W;
+    y[i] = s;
+  }
+}
+
+/* ---- a6 part 2: decode table (§5.2, R6) --------------------------------- */
+void nfo_decode_table(int32_t W, int32_t mode, float* q) {
+  for (int32_t c = 0; c <= W; ++c) {
+    int32_t margin = 2 * c - W;
+    if (mode == NFO_DECODE_MAJORITY)
+      q[c] = margin > 0 ? 1.0f : (margin < 0 ? -1.0f : 0.0f);
+    else
+      q[c] = (float)margin / (float)W;
+  }
+}
+
+/* ---- output assembly (§3.3 step 7, §5.2 write-back, R6) ----------------- */
+void nfo_output(const uint64_t* mask, int64_t n, const uint8_t* counts,
+                const float* y, const float* q, float scale, int32_t route,
+                float* out) {
+  for (int64_t i = 0; i < n; ++i) {
+    if (route == NFO_ROUTE_L && mask_bit(mask, i))
+      out[i] = scale * q[counts[i]];
+    else
+      out[i] = y[i];
+  }
+}
+
+/* ---- the whole bucket (§3.3 steps 3-7) ---------------------------------- */
+int nfo_reduce_bucket(const float* g, int64_t stride, int32_t W, int64_t n,
+                      const uint64_t* mask, const nfo_policy* p,
+                      uint64_t* bits, int64_t bits_stride, uint8_t* counts,
+                      float* out, nfo_stats* stats, nfo_decision* d) {
+  if (W < 1 || W > 255 || n < 0 || stride < n || bits_stride < (n + 63) / 64)
+    return -1;
+  int64_t n_eligible = nfo_count_eligible(mask, n);          /* step 3 */
+  nfo_health(g, stride, W, n, mask, stats);
+  nfo_decide(stats, W, n, n_eligible, p, d);                 /* steps 4, 6 */
+  nfo_pack(g, stride, W, n, mask, bits, bits_stride);        /* step 5 */
+  nfo_counts(bits, bits_stride, W, n, counts);               /* step 7 */
+  float q[256];
+  nfo_decode_table(W, p->decode_mode, q);
+  /* The FP32 path is needed at every position: at routed positions for any
+   * route, and at eligible positions when the route is F or P.  It is taken
+   * in ascending chunks whose starts are multiples of 64. */
+  for (int64_t i0 = 0; i0 < n; i0 += 4096) {
+    int64_t m = n - i0 < 4096 ? n - i0 : 4096;
+    float y[4096];
+    nfo_fp32_path(g + i0, stride, W, m, p->fp32_op, y);
+    nfo_output(mask + i0 / 64, m, counts + i0, y, q, d->scale, d->route,
+               out + i0);
+  }
+  return 0;
+}

@@ -1,0 +1,106 @@
+"""Planted mistakes in copies of the oracle must each fail at least one pin.
+
+Each mutant is a plausible slip (a dropped term, a wrong sign, index, bound or
+operand, an accumulator of the wrong width, a reordered rule).  The test
+applies it to a temporary copy of oracle/nfo.cpp, builds that copy, and runs
+the pins of oracle_pins.py against it.  The real oracle is never modified.
+"""
+import os
+import shutil
+import tempfile
+
+import pytest
+
+import oracle as nfo
+from oracle import build as obuild
+from tests import oracle_pins
+
+SRC = os.path.join(os.path.dirname(obuild.__file__), "nfo.cpp")
+HDR = os.path.join(os.path.dirname(obuild.__file__), "nfo.h")
+
+# (name, original text, replacement) - the original must occur exactly once
+MUTANTS = [
+    ("pack_sign_of_zero", "mask_bit(mask, i) && row[i] > 0.0f", "mask_bit(mask, i) && row[i] >= 0.0f"),
+    ("pack_ignores_mask", "mask_bit(mask, i) && row[i] > 0.0f", "row[i] > 0.0f"),
+    ("pack_msb_first", "        brow[i / 64] |= (uint64_t)1 << (i % 64);",
+     "        brow[i / 64] |= (uint64_t)1 << (63 - i % 64);"),
+    ("counts_wrong_stride", "bits[(int64_t)w * bits_stride + i / 64]",
+     "bits[(int64_t)w * ((n + 63) / 64) + i / 64]"),
+    ("counts_drop_last_worker", "    for (int32_t w = 0; w < W; ++w)\n      c += ",
+     "    for (int32_t w = 0; w + 1 < W; ++w)\n      c += "),
+    ("fp32_drops_first_term", "    float s = g[i];", "    float s = 0.0f;"),
+    ("fp32_mean_by_reciprocal", "s = s / (float)W;", "s = s * (1.0f / (float)W);"),
+    ("fp32_reversed_order", "    for (int32_t w = 1; w < W; ++w) s = s + g[(int64_t)w * stride + i];",
+     "    s = g[(int64_t)(W - 1) * stride + i];\n"
+     "    for (int32_t w = W - 2; w >= 0; --w) s = s + g[(int64_t)w * stride + i];"),
+    ("ssq_eligible_only", "      stats[w].sum_sq += x * x;", "      if (mask_bit(mask, i)) stats[w].sum_sq += x * x;"),
+    ("ssq_fp32_accumulate", "      stats[w].sum_sq += x * x;", "      stats[w].sum_sq = (float)(stats[w].sum_sq + x * x);"),
+    ("sabs_all_elements", "      if (mask_bit(mask, i)) stats[w].sum_abs_elig += fabs(x);",
+     "      stats[w].sum_abs_elig += fabs(x);"),
+    ("sabs_signed", "stats[w].sum_abs_elig += fabs(x);", "stats[w].sum_abs_elig += x;"),
+    ("nonfinite_nan_only", "return ((u >> 23) & 0xffu) == 0xffu;", "return isnan(x);"),
+    ("scale_over_n", "d->scale = nfo_scale(stats, W, n_eligible);", "d->scale = nfo_scale(stats, W, n);"),
+    ("scale_missing_mean_over_workers", "return (float)(acc / (double)W);", "return (float)acc;"),
+    ("scale_fp32_accumulator", "  double acc = 0.0;\n  for (int32_t w = 0; w < W; ++w)\n    acc +=",
+     "  float acc = 0.0f;\n  for (int32_t w = 0; w < W; ++w)\n    acc +="),
+    ("decode_by_reciprocal", "q[c] = (float)margin / (float)W;", "q[c] = (float)margin * (1.0f / (float)W);"),
+    ("decode_sign_flipped", "int32_t margin = 2 * c - W;", "int32_t margin = W - 2 * c;"),
+    ("decode_margin_halved", "int32_t margin = 2 * c - W;", "int32_t margin = c - W / 2;"),
+    ("majority_tie_positive", "q[c] = margin > 0 ? 1.0f", "q[c] = margin >= 0 ? 1.0f"),
+    ("median_upper", "double m = fin[(k - 1) / 2];", "double m = fin[k / 2];"),
+    ("spike_ge", "if (fin[i] > thr) r |= NFO_R_NORM_SPIKE;", "if (fin[i] >= thr) r |= NFO_R_NORM_SPIKE;"),
+    ("spike_kappa_not_squared", "double thr = (p->kappa * p->kappa) * m;", "double thr = p->kappa * m;"),
+    ("spike_needs_three", "  if (k >= 2) {", "  if (k >= 3) {"),
+    ("spike_counts_nonfinite", "    if (!isfinite(v)) continue;\n", ""),
+    ("zero_worker_without_eligible", "  if (n_eligible > 0)\n    for (int32_t w = 0; w < W; ++w)\n      if",
+     "  if (n_eligible >= 0)\n    for (int32_t w = 0; w < W; ++w)\n      if"),
+    ("route_forced_before_plain", "  if (r & (NFO_R_NOT_ADMITTED | NFO_R_NO_ELIGIBLE)) {",
+     "  if (!p->force_lowbit && (r & (NFO_R_NOT_ADMITTED | NFO_R_NO_ELIGIBLE))) {"),
+    ("route_ignores_no_eligible", "  if (r & (NFO_R_NOT_ADMITTED | NFO_R_NO_ELIGIBLE)) {",
+     "  if (r & NFO_R_NOT_ADMITTED) {"),
+    ("route_ignores_veto", "  } else if (r & (NFO_R_VETO | NFO_R_GUARD |", "  } else if (r & (NFO_R_GUARD |"),
+    ("route_ignores_guard", "  } else if (r & (NFO_R_VETO | NFO_R_GUARD |", "  } else if (r & (NFO_R_VETO |"),
+    ("forced_reason_missing", "    r |= NFO_R_FORCED;\n", ""),
+    ("bytes_without_scale", "(double)n_eligible / 8.0 + 4.0 +", "(double)n_eligible / 8.0 +"),
+    ("bytes_bits_not_bytes", "(double)n_eligible / 8.0 + 4.0 +", "(double)n_eligible + 4.0 +"),
+    ("output_decodes_routed", "    if (route == NFO_ROUTE_L && mask_bit(mask, i))", "    if (route == NFO_ROUTE_L)"),
+    ("output_count_off_by_one", "out[i] = scale * q[counts[i]];", "out[i] = scale * q[counts[i] ? counts[i] - 1 : 0];"),
+    ("output_ignores_route", "    if (route == NFO_ROUTE_L && mask_bit(mask, i))", "    if (mask_bit(mask, i))"),
+    ("mask_ignores_eligibility", "    if (!eligible[s]) continue;  /* FP32-only segment: bits stay 0 */\n", ""),
+    ("mask_short_segment", "for (int64_t i = off[s]; i < off[s] + len[s]; ++i)",
+     "for (int64_t i = off[s]; i + 1 < off[s] + len[s]; ++i)"),
+    ("mask_no_bounds_check", "    if (off[s] < 0 || len[s] < 0 || off[s] + len[s] > n) return -1;\n", ""),
+    ("count_eligible_all", "  for (int64_t i = 0; i < n; ++i) c += mask_bit(mask, i);",
+     "  for (int64_t i = 0; i < n; ++i) c += 1;"),
+    ("health_skips_last_element", "    for (int64_t i = 0; i < n; ++i) {\n      double x",
+     "    for (int64_t i = 0; i + 1 < n; ++i) {\n      double x"),
+]
+
+
+def test_mutant_table_applies():
+    src = open(SRC).read()
+    for name, old, new in MUTANTS:
+        assert src.count(old) == 1, f"{name}: target occurs {src.count(old)} times"
+        assert old != new, name
+
+
+@pytest.fixture(scope="module")
+def tmpdir_mut():
+    d = tempfile.mkdtemp(prefix="nfo_mut_")
+    yield d
+    shutil.rmtree(d, ignore_errors=True)
+
+
+@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_mutant_is_caught(tmpdir_mut, name, old, new):
+    src = open(SRC).read()
+    d = os.path.join(tmpdir_mut, name)
+    os.makedirs(d, exist_ok=True)
+    shutil.copy(HDR, d)
+    with open(os.path.join(d, "nfo.cpp"), "w") as f:
+        f.write(src.replace(old, new))
+    lib_path = obuild.build(out=os.path.join(d, "libnfo_mut.so"),
+                            src=os.path.join(d, "nfo.cpp"), extra=("-w",))
+    lib = nfo.load(lib_path)
+    failures = oracle_pins.run_all(lib)
+    assert failures, f"mutant {name} passed every pin"
