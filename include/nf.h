@@ -1,0 +1,233 @@
+/*
+ * nf.h - C ABI of the NEURON-Fabric bucket reducer for AMD MI355X (gfx950).
+ *
+ * The reducer is the data-parallel hot path of controlled low-bit gradient
+ * aggregation (NEURON-Fabric, arXiv 2606.25759).  It takes the FP32 gradient
+ * buckets of W data-parallel workers and the bucket's per-element
+ * eligibility mask, and
+ *   - packs the signs of the low-bit-eligible elements (write side, §3.3
+ *     step 5, §5.2),
+ *   - sums the FP32-routed elements in full precision (§2.1, §3.3 step 5),
+ *   - computes per-worker health statistics and the bucket's route
+ *     decision L / F / P with its modeled traffic (§3.2, §6.4),
+ *   - counts the packed signs per coordinate and decodes the scaled aggregate
+ *     direction (read side, §3.3 step 7, §5.2, §6.1), or, on fallback, sums
+ *     the eligible elements in FP32 as well.
+ *
+ * The W workers are W rows of one device buffer: row w of a bucket starts at
+ * grads + w * worker_stride.
+ *
+ * Conventions shared by every function:
+ *   - Every function returns nf_status.  On an error nothing is launched and
+ *     nf_last_error() (thread-local) describes the failing argument.
+ *   - Pointers named *_host are host memory.  Every other pointer is device
+ *     memory owned by the caller; the library never allocates.  Scratch
+ *     space comes from a caller-provided workspace `ws` of at least the size
+ *     the matching nf_*workspace_bytes function returns.
+ *   - Device work is enqueued asynchronously on `stream` (a hipStream_t passed
+ *     as void*; NULL is the null stream).  Results are valid after the stream
+ *     is synchronised.  A launch failure returns NF_ERR_HIP.
+ *   - Requirements checked before any launch (NF_ERR_INVALID_ARG unless
+ *     stated): 1 <= W <= 255 (counts are uint8); n >= 0;
+ *     worker_stride >= n; grads 16-byte aligned and worker_stride a multiple
+ *     of 4 (NF_ERR_ALIGNMENT); mask and bits 8-byte aligned, out 4-byte
+ *     aligned (NF_ERR_ALIGNMENT); bits_stride_words >= ceil(n / 64).  Inputs
+ *     and outputs must not overlap (not checked).
+ *   - Layouts: masks and sign bitmaps are little-endian uint64 words,
+ *     LSB-first: bit j of word k is element 64k + j.  Mask bits at or past n
+ *     are ignored.  One mask is shared by all W workers (the binding is per
+ *     model, §5.1).  Bitmap row w starts at bits + w * bits_stride_words.
+ *   - Floating point: FP32 sums add workers in order w = 0..W-1 in FP32
+ *     without contraction, so they are bit-reproducible; per-worker health
+ *     sums are FP64 in a fixed order (deterministic, within 1e-12 relative
+ *     of a sequential FP64 sum); no floating-point atomics are used, so two
+ *     calls on the same inputs give bitwise identical results.
+ *   - Calls on different streams with different workspaces may run
+ *     concurrently.  The library keeps no mutable state besides the
+ *     thread-local error string.
+ */
+#ifndef NF_H
+#define NF_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define NF_ABI_VERSION 1
+
+typedef enum {
+  NF_OK = 0,
+  NF_ERR_INVALID_ARG = 1,
+  NF_ERR_ALIGNMENT = 2,
+  NF_ERR_UNSUPPORTED = 3,
+  NF_ERR_HIP = 4,
+  NF_ERR_WORKSPACE = 5
+} nf_status;
+
+/* Route states (§3.2): low-bit; FP32 fallback of an admitted route; plain FP32. */
+enum { NF_ROUTE_LOWBIT = 0, NF_ROUTE_FALLBACK = 1, NF_ROUTE_PLAIN = 2 };
+
+/* Reason bits of a route decision; every bit is evaluated on every call. */
+enum {
+  NF_REASON_NOT_ADMITTED = 1,  /* policy.admitted == 0 (Commander, §4.2)      */
+  NF_REASON_NO_ELIGIBLE = 2,   /* no mask bit set in [0, n) (§5.1)            */
+  NF_REASON_VETO = 4,          /* policy.veto != 0 (Supervisor, §4.3)         */
+  NF_REASON_GUARD = 8,         /* policy.guard_ok == 0 (endpoint guard, §6.4) */
+  NF_REASON_NONFINITE = 16,    /* some worker holds a NaN or an infinity      */
+  NF_REASON_ZERO_WORKER = 32,  /* n_E > 0 and a worker's eligible |g| sum is 0 */
+  NF_REASON_NORM_SPIKE = 64,   /* a finite sum g^2 > kappa^2 * lower median    */
+  NF_REASON_FORCED = 128       /* low-bit taken because force_lowbit was set  */
+};
+
+enum { NF_DECODE_SOFT = 0, NF_DECODE_MAJORITY = 1 };
+enum { NF_FP32_SUM = 0, NF_FP32_MEAN = 1 };
+enum { NF_SEL_ROUTED = 0, NF_SEL_ELIGIBLE = 1, NF_SEL_ALL = 2 };
+
+/* Per-worker health of one bucket. */
+typedef struct {
+  uint64_t nonfinite;   /* count of NaN / +-Inf values over all n elements    */
+  double sum_abs_elig;  /* sum of |g| over eligible elements (FP64)           */
+  double sum_sq;        /* sum of g*g over all n elements (FP64)              */
+} nf_worker_stats;
+
+/* Controller and guard inputs of a route decision. */
+typedef struct {
+  int32_t admitted;      /* Commander has admitted the low-bit mode (§4.2)     */
+  int32_t veto;          /* Supervisor veto is active (§4.3)                   */
+  int32_t guard_ok;      /* endpoint-capacity guard admits low-bit (§6.4)      */
+  int32_t force_lowbit;  /* guard disabled: take low-bit despite F reasons     */
+  int32_t decode_mode;   /* NF_DECODE_SOFT (default) or NF_DECODE_MAJORITY     */
+  int32_t fp32_op;       /* NF_FP32_SUM (default) or NF_FP32_MEAN              */
+  double kappa;          /* norm-spike ratio on L2 norms, > 0 (default 4.0)    */
+} nf_route_policy;
+
+/* Route decision of one bucket (40 bytes). */
+typedef struct {
+  int32_t route;        /* NF_ROUTE_*                                          */
+  uint32_t reasons;     /* NF_REASON_* bitmask                                 */
+  float scale;          /* mean over workers of the mean |g| over eligible
+                           elements, rounded once to FP32; 0 if n_E == 0      */
+  uint32_t reserved;    /* 0                                                   */
+  int64_t n_eligible;   /* n_E: mask bits set in [0, n)                        */
+  double bytes_route;   /* modeled payload bytes per worker of this route:
+                           n_E/8 + 4 + 4(n - n_E) for L, 4n for F and P        */
+  double bytes_fp32;    /* matched FP32 payload bytes per worker: 4n (§3.2)    */
+} nf_route_decision;
+
+int nf_abi_version(void);
+const char* nf_last_error(void);
+
+/*
+ * Binding -> eligibility mask (§5.1: per-parameter eligibility; an element
+ * not covered by an eligible segment is FP32).  Host helper: segment s covers
+ * [off_host[s], off_host[s] + len_host[s]) and is eligible when
+ * eligible_host[s] != 0.  Writes ceil(n/64) words to mask_host (padding bits
+ * zero).  NF_ERR_INVALID_ARG if a segment leaves [0, n).
+ */
+nf_status nf_mask_from_segments(const int64_t* off_host, const int64_t* len_host,
+                                const uint8_t* eligible_host, int64_t nseg, int64_t n,
+                                uint64_t* mask_host);
+
+/* Workspace bytes for one bucket of n elements (nf_bucket_health,
+ * nf_pack_signs, nf_route_bucket). */
+size_t nf_workspace_bytes(int32_t W, int64_t n);
+
+/*
+ * Per-worker health of one bucket (write-side statistics behind the fallback
+ * decision; the paper's Supervisor and guard act on health, §4.3, §6.4).
+ * Writes stats[0..W) (device).  Reads 4*W*n bytes once.
+ */
+nf_status nf_bucket_health(const float* grads, int64_t worker_stride, int32_t W, int64_t n,
+                           const uint64_t* mask, nf_worker_stats* stats, void* ws,
+                           size_t ws_bytes, void* stream);
+
+/*
+ * Write-side sign payload (§3.3 step 5, §5.2 positive-sign indicators, §6.1
+ * bit-packed updates): bit j of bits[w][k] = mask(64k+j) && g_w[64k+j] > 0
+ * (+0, -0 and NaN give 0).  Writes all ceil(n/64) words of each of the W rows,
+ * with zero padding.  When stats is not NULL the same single read also
+ * produces the per-worker health of nf_bucket_health.
+ */
+nf_status nf_pack_signs(const float* grads, int64_t worker_stride, int32_t W, int64_t n,
+                        const uint64_t* mask, uint64_t* bits, int64_t bits_stride_words,
+                        nf_worker_stats* stats, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Full-precision path (§2.1 sum or average; §6.1 FP32 reference path):
+ * out[i] = g_0[i] + g_1[i] + ... + g_{W-1}[i] in FP32, workers in order;
+ * NF_FP32_MEAN divides the sum by W (IEEE division).  Written only at the
+ * selected positions: NF_SEL_ROUTED mask = 0, NF_SEL_ELIGIBLE mask = 1,
+ * NF_SEL_ALL every position (mask may then be NULL).  No workspace.
+ */
+nf_status nf_fp32_reduce(const float* grads, int64_t worker_stride, int32_t W, int64_t n,
+                         const uint64_t* mask, int32_t select, int32_t fp32_op, float* out,
+                         void* stream);
+
+/*
+ * Read side of the sign-count route (§3.3 step 7, §5.2 vote and scaled
+ * write-back, §6.1 per-coordinate counts): c_i = sum_w bit_w(i) in [0, W];
+ * when counts is not NULL it receives all n counts.  When out is not NULL,
+ * out[i] = fl32(scale * q[c_i]) at positions with mask = 1 (others untouched),
+ * with scale = *scale_dev (device, one float) and
+ * q[c] = fl32((2c - W) / W) (NF_DECODE_SOFT) or sign(2c - W) with a tie giving
+ * 0 (NF_DECODE_MAJORITY).  No workspace.
+ */
+nf_status nf_signcount_reduce(const uint64_t* bits, int64_t bits_stride_words, int32_t W,
+                              int64_t n, const uint64_t* mask, const float* scale_dev,
+                              int32_t decode_mode, uint8_t* counts, float* out, void* stream);
+
+/*
+ * Route decision from statistics (host, pure function; the rules the device
+ * path applies).  Reasons as listed above; route by precedence P (not
+ * admitted, or no eligible element) > forced L > F (veto, guard, non-finite,
+ * zero worker, norm spike) > L.  The norm-spike rule takes the workers whose
+ * sum_sq is finite (at least two), their lower median m (index
+ * floor((k-1)/2) in ascending order), and flags sum_sq > (kappa*kappa)*m.
+ */
+nf_status nf_route_decide(const nf_worker_stats* stats_host, int32_t W, int64_t n,
+                          int64_t n_eligible, const nf_route_policy* policy_host,
+                          nf_route_decision* decision_host);
+
+/*
+ * One bucket end to end (§3.3 steps 3-7), with no host synchronisation:
+ * pass 1 reads the gradients once and produces the sign payload, the health
+ * statistics and the FP32 sums at mask = 0; a one-block decision kernel
+ * writes *decision (device); pass 2 then counts and decodes at mask = 1
+ * (route L), sums the eligible elements in FP32 (route F), or does nothing
+ * (route P).  When the policy fixes the route before any data is read (not
+ * admitted, veto or guard without force_lowbit), pass 1 writes FP32 sums at
+ * every position instead and bits are not written.
+ * Always written: out[0..n), stats[0..W), *decision.  bits: written unless
+ * the policy fixed the route before reading.  counts (nullable): written
+ * when the route is L.
+ */
+nf_status nf_route_bucket(const float* grads, int64_t worker_stride, int32_t W, int64_t n,
+                          const uint64_t* mask, const nf_route_policy* policy_host,
+                          uint64_t* bits, int64_t bits_stride_words, uint8_t* counts,
+                          float* out, nf_worker_stats* stats, nf_route_decision* decision,
+                          void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Many buckets of one flat gradient buffer in three launches (DDP cuts a
+ * model's flat gradient into fixed-capacity buckets, §2.1).  Bucket b covers
+ * elements [b*bucket_n, min((b+1)*bucket_n, n_total)) of every worker row,
+ * of the mask, of the bitmap rows (from word b*bucket_n/64), of counts and of
+ * out; nb = ceil(n_total / bucket_n).  bucket_n must be a multiple of 64
+ * unless bucket_n >= n_total.  stats is [nb][W], decisions is [nb] (device).
+ * Per bucket, the results equal those of nf_route_bucket on that bucket.
+ */
+size_t nf_workspace_bytes_buckets(int32_t W, int64_t n_total, int64_t bucket_n);
+nf_status nf_route_buckets(const float* grads, int64_t worker_stride, int32_t W,
+                           int64_t n_total, int64_t bucket_n, const uint64_t* mask,
+                           const nf_route_policy* policy_host, uint64_t* bits,
+                           int64_t bits_stride_words, uint8_t* counts, float* out,
+                           nf_worker_stats* stats, nf_route_decision* decisions, void* ws,
+                           size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* NF_H */

@@ -1,0 +1,270 @@
+"""ctypes binding of libnf.so (the C ABI of include/nf.h), same function names.
+
+Argument marshalling only: every wrapper checks dtypes and devices, turns
+torch tensors into device pointers and the current torch stream into a
+hipStream_t, calls the library, and raises NFError on a non-zero status.  No
+step of the reducer runs here, and there is no fallback: if libnf.so is
+missing, loading fails loudly.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+try:  # torch first: its HIP runtime is the one the library then binds to
+    import torch
+except ImportError:  # pragma: no cover - the library itself needs no torch
+    torch = None
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libnf.so")
+
+NF_OK, NF_ERR_INVALID_ARG, NF_ERR_ALIGNMENT, NF_ERR_UNSUPPORTED, NF_ERR_HIP, NF_ERR_WORKSPACE = range(6)
+NF_ROUTE_LOWBIT, NF_ROUTE_FALLBACK, NF_ROUTE_PLAIN = 0, 1, 2
+NF_REASON_NOT_ADMITTED, NF_REASON_NO_ELIGIBLE, NF_REASON_VETO, NF_REASON_GUARD = 1, 2, 4, 8
+NF_REASON_NONFINITE, NF_REASON_ZERO_WORKER, NF_REASON_NORM_SPIKE, NF_REASON_FORCED = 16, 32, 64, 128
+NF_DECODE_SOFT, NF_DECODE_MAJORITY = 0, 1
+NF_FP32_SUM, NF_FP32_MEAN = 0, 1
+NF_SEL_ROUTED, NF_SEL_ELIGIBLE, NF_SEL_ALL = 0, 1, 2
+
+# Exported names, in the order include/nf.h declares them.
+EXPORTS = ["nf_abi_version", "nf_last_error", "nf_mask_from_segments", "nf_workspace_bytes",
+           "nf_bucket_health", "nf_pack_signs", "nf_fp32_reduce", "nf_signcount_reduce",
+           "nf_route_decide", "nf_route_bucket", "nf_workspace_bytes_buckets", "nf_route_buckets"]
+
+
+class nf_worker_stats(ctypes.Structure):
+    _fields_ = [("nonfinite", ctypes.c_uint64), ("sum_abs_elig", ctypes.c_double),
+                ("sum_sq", ctypes.c_double)]
+
+
+class nf_route_policy(ctypes.Structure):
+    _fields_ = [("admitted", ctypes.c_int32), ("veto", ctypes.c_int32),
+                ("guard_ok", ctypes.c_int32), ("force_lowbit", ctypes.c_int32),
+                ("decode_mode", ctypes.c_int32), ("fp32_op", ctypes.c_int32),
+                ("kappa", ctypes.c_double)]
+
+
+class nf_route_decision(ctypes.Structure):
+    _fields_ = [("route", ctypes.c_int32), ("reasons", ctypes.c_uint32),
+                ("scale", ctypes.c_float), ("reserved", ctypes.c_uint32),
+                ("n_eligible", ctypes.c_int64), ("bytes_route", ctypes.c_double),
+                ("bytes_fp32", ctypes.c_double)]
+
+
+STATS_DTYPE = np.dtype([("nonfinite", "<u8"), ("sum_abs_elig", "<f8"), ("sum_sq", "<f8")])
+DECISION_DTYPE = np.dtype([("route", "<i4"), ("reasons", "<u4"), ("scale", "<f4"),
+                           ("reserved", "<u4"), ("n_eligible", "<i8"),
+                           ("bytes_route", "<f8"), ("bytes_fp32", "<f8")])
+STATS_BYTES = ctypes.sizeof(nf_worker_stats)        # 24
+DECISION_BYTES = ctypes.sizeof(nf_route_decision)   # 40
+
+
+class NFError(RuntimeError):
+    def __init__(self, status, message):
+        super().__init__(f"nf status {status}: {message}")
+        self.status = status
+
+
+_lib = None
+_P = ctypes.c_void_p
+_I64 = ctypes.c_int64
+_I32 = ctypes.c_int32
+_SZ = ctypes.c_size_t
+
+
+def load(path=None):
+    """Load libnf.so (built by paper_2606_25759_amd/build.py); raises if absent."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    path = path or LIB_PATH
+    if not os.path.exists(path):
+        raise OSError(f"{path} is missing: build it with python -c "
+                      "'import __graft_entry__; __graft_entry__.build()'")
+    lib = ctypes.CDLL(path)
+    sigs = {
+        "nf_abi_version": (ctypes.c_int, []),
+        "nf_last_error": (ctypes.c_char_p, []),
+        "nf_mask_from_segments": (ctypes.c_int, [_P, _P, _P, _I64, _I64, _P]),
+        "nf_workspace_bytes": (_SZ, [_I32, _I64]),
+        "nf_workspace_bytes_buckets": (_SZ, [_I32, _I64, _I64]),
+        "nf_bucket_health": (ctypes.c_int, [_P, _I64, _I32, _I64, _P, _P, _P, _SZ, _P]),
+        "nf_pack_signs": (ctypes.c_int, [_P, _I64, _I32, _I64, _P, _P, _I64, _P, _P, _SZ, _P]),
+        "nf_fp32_reduce": (ctypes.c_int, [_P, _I64, _I32, _I64, _P, _I32, _I32, _P, _P]),
+        "nf_signcount_reduce": (ctypes.c_int, [_P, _I64, _I32, _I64, _P, _P, _I32, _P, _P, _P]),
+        "nf_route_decide": (ctypes.c_int, [_P, _I32, _I64, _I64, _P, _P]),
+        "nf_route_bucket": (ctypes.c_int, [_P, _I64, _I32, _I64, _P, _P, _P, _I64, _P, _P, _P, _P,
+                                           _P, _SZ, _P]),
+        "nf_route_buckets": (ctypes.c_int, [_P, _I64, _I32, _I64, _I64, _P, _P, _P, _I64, _P, _P,
+                                            _P, _P, _P, _SZ, _P]),
+    }
+    for name, (res, args) in sigs.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    if path == LIB_PATH:
+        _lib = lib
+    return lib
+
+
+def _check(status):
+    if status != NF_OK:
+        raise NFError(status, load().nf_last_error().decode())
+
+
+def _dev_ptr(t, dtype=None, name="tensor"):
+    """Device pointer of a CUDA/HIP tensor (None -> NULL)."""
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return getattr(stream, "cuda_stream", stream)
+
+
+def _rows(grads):
+    """(pointer, worker_stride, W) of a [W, >= n] float32 device tensor."""
+    if grads.dim() != 2 or grads.stride(1) != 1:
+        raise ValueError("grads must be a [W, stride] tensor with unit element stride")
+    return _dev_ptr(grads, torch.float32, "grads"), grads.stride(0), grads.shape[0]
+
+
+def _bits_rows(bits):
+    if bits is None:
+        return None, 0
+    if bits.dim() != 2 or bits.stride(1) != 1:
+        raise ValueError("bits must be a [W, words] int64/uint64 tensor")
+    if bits.dtype not in (torch.int64, torch.uint64):
+        raise ValueError("bits must be 64-bit")
+    return _dev_ptr(bits, None, "bits"), bits.stride(0)
+
+
+def _words(mask):
+    if mask is None:
+        return None
+    if mask.dtype not in (torch.int64, torch.uint64):
+        raise ValueError("mask must be 64-bit words")
+    return _dev_ptr(mask, None, "mask")
+
+
+# --------------------------------------------------------------- host calls
+
+def nf_abi_version():
+    return load().nf_abi_version()
+
+
+def nf_last_error():
+    return load().nf_last_error().decode()
+
+
+def nf_mask_from_segments(off, length, eligible, n):
+    """Host segments -> host uint64 mask words (numpy)."""
+    off = np.ascontiguousarray(off, dtype=np.int64)
+    length = np.ascontiguousarray(length, dtype=np.int64)
+    eligible = np.ascontiguousarray(eligible, dtype=np.uint8)
+    mask = np.zeros(max((n + 63) // 64, 1), dtype=np.uint64)
+    _check(load().nf_mask_from_segments(off.ctypes.data, length.ctypes.data, eligible.ctypes.data,
+                                        len(off), n, mask.ctypes.data))
+    return mask[: (n + 63) // 64]
+
+
+def nf_workspace_bytes(W, n):
+    return int(load().nf_workspace_bytes(W, n))
+
+
+def nf_workspace_bytes_buckets(W, n_total, bucket_n):
+    return int(load().nf_workspace_bytes_buckets(W, n_total, bucket_n))
+
+
+def policy(admitted=1, veto=0, guard_ok=1, force_lowbit=0, decode_mode=NF_DECODE_SOFT,
+           fp32_op=NF_FP32_SUM, kappa=4.0):
+    return nf_route_policy(admitted, veto, guard_ok, force_lowbit, decode_mode, fp32_op, kappa)
+
+
+def nf_route_decide(stats, n, n_eligible, pol=None):
+    """Host decision from a numpy STATS_DTYPE array; returns nf_route_decision."""
+    st = np.ascontiguousarray(stats, dtype=STATS_DTYPE)
+    d = nf_route_decision()
+    pol = pol or policy()
+    _check(load().nf_route_decide(st.ctypes.data, len(st), n, n_eligible, ctypes.byref(pol),
+                                  ctypes.byref(d)))
+    return d
+
+
+# ------------------------------------------------------------- device calls
+
+def empty_workspace(nbytes, device="cuda"):
+    """Caller-owned workspace (the torch allocator aligns to 512 bytes)."""
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+
+
+def nf_bucket_health(grads, n, mask, stats, ws, stream=None):
+    g, stride, W = _rows(grads)
+    _check(load().nf_bucket_health(g, stride, W, n, _words(mask), _dev_ptr(stats, torch.uint8, "stats"),
+                                   _dev_ptr(ws, torch.uint8, "ws"), ws.numel(), _stream(stream)))
+
+
+def nf_pack_signs(grads, n, mask, bits, stats, ws, stream=None):
+    g, stride, W = _rows(grads)
+    b, bstride = _bits_rows(bits)
+    _check(load().nf_pack_signs(g, stride, W, n, _words(mask), b, bstride,
+                                _dev_ptr(stats, torch.uint8, "stats"), _dev_ptr(ws, torch.uint8, "ws"),
+                                ws.numel(), _stream(stream)))
+
+
+def nf_fp32_reduce(grads, n, mask, select, fp32_op, out, stream=None):
+    g, stride, W = _rows(grads)
+    _check(load().nf_fp32_reduce(g, stride, W, n, _words(mask), select, fp32_op,
+                                 _dev_ptr(out, torch.float32, "out"), _stream(stream)))
+
+
+def nf_signcount_reduce(bits, W, n, mask, scale, decode_mode, counts, out, stream=None):
+    b, bstride = _bits_rows(bits)
+    _check(load().nf_signcount_reduce(b, bstride, W, n, _words(mask),
+                                      _dev_ptr(scale, torch.float32, "scale"), decode_mode,
+                                      _dev_ptr(counts, torch.uint8, "counts"),
+                                      _dev_ptr(out, torch.float32, "out"), _stream(stream)))
+
+
+def nf_route_bucket(grads, n, mask, pol, bits, counts, out, stats, decision, ws, stream=None):
+    g, stride, W = _rows(grads)
+    b, bstride = _bits_rows(bits)
+    _check(load().nf_route_bucket(g, stride, W, n, _words(mask), ctypes.byref(pol), b, bstride,
+                                  _dev_ptr(counts, torch.uint8, "counts"),
+                                  _dev_ptr(out, torch.float32, "out"),
+                                  _dev_ptr(stats, torch.uint8, "stats"),
+                                  _dev_ptr(decision, torch.uint8, "decision"),
+                                  _dev_ptr(ws, torch.uint8, "ws"), ws.numel(), _stream(stream)))
+
+
+def nf_route_buckets(grads, n_total, bucket_n, mask, pol, bits, counts, out, stats, decisions, ws,
+                     stream=None):
+    g, stride, W = _rows(grads)
+    b, bstride = _bits_rows(bits)
+    _check(load().nf_route_buckets(g, stride, W, n_total, bucket_n, _words(mask), ctypes.byref(pol),
+                                   b, bstride, _dev_ptr(counts, torch.uint8, "counts"),
+                                   _dev_ptr(out, torch.float32, "out"),
+                                   _dev_ptr(stats, torch.uint8, "stats"),
+                                   _dev_ptr(decisions, torch.uint8, "decisions"),
+                                   _dev_ptr(ws, torch.uint8, "ws"), ws.numel(), _stream(stream)))
+
+
+# ------------------------------------------------------- result decoding
+
+def stats_host(stats_dev, W, nb=1):
+    """Device stats buffer (uint8) -> numpy STATS_DTYPE array [nb, W]."""
+    raw = stats_dev[: nb * W * STATS_BYTES].cpu().numpy()
+    return raw.view(STATS_DTYPE).reshape(nb, W)
+
+
+def decisions_host(dec_dev, nb=1):
+    raw = dec_dev[: nb * DECISION_BYTES].cpu().numpy()
+    return raw.view(DECISION_DTYPE).reshape(nb)

@@ -1,0 +1,379 @@
+// nf_api.hip - the C ABI of include/nf.h: argument checks, workspace
+// layout, and the launch sequence on the caller's stream.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+
+#include "nf_internal.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+nf_status fail(nf_status st, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+nf_status fail(nf_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+nf_status ok() {
+  g_err.clear();
+  return NF_OK;
+}
+
+nf_status hip_fail(hipError_t e, const char* what) {
+  return fail(NF_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+// Checks shared by every entry point that reads gradient rows.
+nf_status check_grads(const float* g, int64_t stride, int32_t W, int64_t n) {
+  if (W < 1 || W > 255) return fail(NF_ERR_INVALID_ARG, "W=%d outside [1, 255]", W);
+  if (n < 0) return fail(NF_ERR_INVALID_ARG, "n=%lld < 0", (long long)n);
+  if (stride < n) return fail(NF_ERR_INVALID_ARG, "worker_stride=%lld < n=%lld", (long long)stride, (long long)n);
+  if (n > 0 && !g) return fail(NF_ERR_INVALID_ARG, "grads is NULL");
+  if (!aligned(g, 16)) return fail(NF_ERR_ALIGNMENT, "grads not 16-byte aligned");
+  if (stride % 4) return fail(NF_ERR_ALIGNMENT, "worker_stride=%lld not a multiple of 4", (long long)stride);
+  return NF_OK;
+}
+
+nf_status check_mask(const uint64_t* mask, int64_t n) {
+  if (n > 0 && !mask) return fail(NF_ERR_INVALID_ARG, "mask is NULL");
+  if (!aligned(mask, 8)) return fail(NF_ERR_ALIGNMENT, "mask not 8-byte aligned");
+  return NF_OK;
+}
+
+nf_status check_bits(const uint64_t* bits, int64_t bstride, int64_t n, int32_t W) {
+  (void)W;
+  if (n > 0 && !bits) return fail(NF_ERR_INVALID_ARG, "bits is NULL");
+  if (!aligned(bits, 8)) return fail(NF_ERR_ALIGNMENT, "bits not 8-byte aligned");
+  if (bstride < (n + 63) / 64)
+    return fail(NF_ERR_INVALID_ARG, "bits_stride_words=%lld < ceil(n/64)=%lld", (long long)bstride,
+                (long long)((n + 63) / 64));
+  return NF_OK;
+}
+
+nf_status check_policy(const nf_route_policy* p) {
+  if (!p) return fail(NF_ERR_INVALID_ARG, "policy is NULL");
+  if (!(p->kappa > 0.0) || p->kappa != p->kappa || p->kappa - p->kappa != 0.0)
+    return fail(NF_ERR_INVALID_ARG, "kappa must be finite and > 0");
+  if (p->decode_mode != NF_DECODE_SOFT && p->decode_mode != NF_DECODE_MAJORITY)
+    return fail(NF_ERR_INVALID_ARG, "decode_mode=%d", p->decode_mode);
+  if (p->fp32_op != NF_FP32_SUM && p->fp32_op != NF_FP32_MEAN)
+    return fail(NF_ERR_INVALID_ARG, "fp32_op=%d", p->fp32_op);
+  return NF_OK;
+}
+
+nf_status check_ws(void* ws, size_t ws_bytes, size_t need) {
+  if (ws_bytes < need)
+    return fail(NF_ERR_WORKSPACE, "workspace of %zu bytes < %zu required", ws_bytes, need);
+  if (need && !ws) return fail(NF_ERR_WORKSPACE, "workspace is NULL");
+  if (!aligned(ws, 256)) return fail(NF_ERR_ALIGNMENT, "workspace not 256-byte aligned");
+  return NF_OK;
+}
+
+#define NF_TRY(x)                    \
+  do {                               \
+    nf_status st__ = (x);            \
+    if (st__ != NF_OK) return st__;  \
+  } while (0)
+
+// Pass 1 + statistics (and optionally the decision) for buckets of one flat
+// buffer.  Shared by the health, pack and route entry points.
+nf_status run_pass1_decide(const nf::Geometry& geo, const float* g, int64_t stride,
+                           const uint64_t* mask, uint64_t* bits, int64_t bstride, float* out,
+                           int sums, int mean, nf_worker_stats* stats, nf_route_decision* dec,
+                           const nf_route_policy* pol, void* ws, hipStream_t s) {
+  const nf::WorkspaceLayout lay = nf::workspace_layout(geo);
+  char* w = static_cast<char*>(ws);
+  nf::Pass1Args a;
+  a.g = g;
+  a.wstride = stride;
+  a.mask = mask;
+  a.bits = bits;
+  a.bstride = bstride;
+  a.out = out;
+  a.part = reinterpret_cast<nf::Partial*>(w + lay.partials);
+  a.part_ne = reinterpret_cast<uint64_t*>(w + lay.ne);
+  a.n_total = geo.n_total;
+  a.bucket_n = geo.bucket_n;
+  a.W = geo.W;
+  a.wg = geo.wg;
+  a.eg = geo.eg;
+  a.T = geo.T;
+  a.bpb = geo.bpb;
+  a.sums = sums;
+  a.mean = mean;
+  hipError_t e = nf::launch_pass1(geo, a, s);
+  if (e != hipSuccess) return hip_fail(e, "pass-1 launch");
+  nf::DecideArgs d;
+  d.part = a.part;
+  d.part_ne = a.part_ne;
+  d.stats = stats;
+  d.dec = dec;
+  if (pol) {
+    d.pol = *pol;
+  } else {
+    memset(&d.pol, 0, sizeof d.pol);
+    d.pol.kappa = 4.0;
+  }
+  d.n_total = geo.n_total;
+  d.bucket_n = geo.bucket_n;
+  d.W = geo.W;
+  d.bpb = geo.bpb;
+  e = nf::launch_decide(geo, d, s);
+  if (e != hipSuccess) return hip_fail(e, "decide launch");
+  return NF_OK;
+}
+
+// Pass-2 arguments for the buckets of a flat buffer.
+nf::Pass2Args pass2_args(const nf::Geometry& geo) {
+  nf::Pass2Args p;
+  memset(&p, 0, sizeof p);
+  p.n_total = geo.n_total;
+  p.bucket_n = geo.bucket_n;
+  p.W = geo.W;
+  p.bpb2 = geo.bpb2;
+  return p;
+}
+
+nf_status route_flat(const float* g, int64_t stride, int32_t W, int64_t n_total, int64_t bucket_n,
+                     const uint64_t* mask, const nf_route_policy* pol, uint64_t* bits,
+                     int64_t bstride, uint8_t* counts, float* out, nf_worker_stats* stats,
+                     nf_route_decision* dec, void* ws, size_t ws_bytes, void* stream) {
+  NF_TRY(check_grads(g, stride, W, n_total));
+  NF_TRY(check_mask(mask, n_total));
+  NF_TRY(check_policy(pol));
+  if (n_total > 0 && !out) return fail(NF_ERR_INVALID_ARG, "out is NULL");
+  if (!aligned(out, 4)) return fail(NF_ERR_ALIGNMENT, "out not 4-byte aligned");
+  if (!stats || !dec) return fail(NF_ERR_INVALID_ARG, "stats and decision are required");
+  if (!aligned(stats, 8) || !aligned(dec, 8)) return fail(NF_ERR_ALIGNMENT, "stats/decision not 8-byte aligned");
+  const nf::Geometry geo = nf::make_geometry(W, n_total, bucket_n);
+  NF_TRY(check_ws(ws, ws_bytes, nf::workspace_layout(geo).total));
+  // The policy alone fixes the route when low-bit is not admitted, vetoed
+  // or guard-rejected (and not forced): then no sign payload is built and
+  // pass 1 writes the FP32 sums at every position.
+  const bool predecided = !pol->admitted || (!pol->force_lowbit && (pol->veto || !pol->guard_ok));
+  if (!predecided) NF_TRY(check_bits(bits, bstride, n_total, W));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  NF_TRY(run_pass1_decide(geo, g, stride, mask, predecided ? nullptr : bits, bstride, out,
+                          predecided ? nf::kSumsAll : nf::kSumsRouted, pol->fp32_op == NF_FP32_MEAN,
+                          stats, dec, pol, ws, s));
+  if (predecided || n_total == 0) return ok();
+  nf::Pass2Args p = pass2_args(geo);
+  p.bits = bits;
+  p.bstride = bstride;
+  p.g = g;
+  p.wstride = stride;
+  p.mask = mask;
+  p.dec = dec;
+  p.counts = counts;
+  p.out = out;
+  p.op = nf::kOpFromDecision;
+  p.decode_mode = pol->decode_mode;
+  p.mean = pol->fp32_op == NF_FP32_MEAN;
+  hipError_t e = nf::launch_pass2(geo, p, s);
+  if (e != hipSuccess) return hip_fail(e, "pass-2 launch");
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+int nf_abi_version(void) { return NF_ABI_VERSION; }
+
+const char* nf_last_error(void) { return g_err.c_str(); }
+
+nf_status nf_mask_from_segments(const int64_t* off_host, const int64_t* len_host,
+                                const uint8_t* eligible_host, int64_t nseg, int64_t n,
+                                uint64_t* mask_host) {
+  if (n < 0 || nseg < 0) return fail(NF_ERR_INVALID_ARG, "negative n or nseg");
+  if (nseg > 0 && (!off_host || !len_host || !eligible_host))
+    return fail(NF_ERR_INVALID_ARG, "segment arrays are NULL");
+  const int64_t nw = (n + 63) / 64;
+  if (nw > 0 && !mask_host) return fail(NF_ERR_INVALID_ARG, "mask_host is NULL");
+  for (int64_t s = 0; s < nseg; ++s)
+    if (off_host[s] < 0 || len_host[s] < 0 || off_host[s] > n - len_host[s])
+      return fail(NF_ERR_INVALID_ARG, "segment %lld [%lld, +%lld) outside [0, %lld)", (long long)s,
+                  (long long)off_host[s], (long long)len_host[s], (long long)n);
+  memset(mask_host, 0, (size_t)nw * sizeof(uint64_t));
+  for (int64_t s = 0; s < nseg; ++s) {
+    if (!eligible_host[s] || len_host[s] == 0) continue;
+    int64_t lo = off_host[s], hi = off_host[s] + len_host[s];  // [lo, hi)
+    int64_t wlo = lo >> 6, whi = (hi - 1) >> 6;
+    for (int64_t k = wlo; k <= whi; ++k) {
+      int64_t a = k == wlo ? (lo & 63) : 0;
+      int64_t b = k == whi ? ((hi - 1) & 63) : 63;  // inclusive
+      uint64_t m = (b == 63 ? ~0ull : ((1ull << (b + 1)) - 1ull)) & ~((1ull << a) - 1ull);
+      mask_host[k] |= m;
+    }
+  }
+  return ok();
+}
+
+size_t nf_workspace_bytes(int32_t W, int64_t n) {
+  if (W < 1 || W > 255 || n < 0) return 0;
+  return nf::workspace_layout(nf::make_geometry(W, n, n > 0 ? n : 1)).total;
+}
+
+size_t nf_workspace_bytes_buckets(int32_t W, int64_t n_total, int64_t bucket_n) {
+  if (W < 1 || W > 255 || n_total < 0 || bucket_n <= 0) return 0;
+  return nf::workspace_layout(nf::make_geometry(W, n_total, bucket_n)).total;
+}
+
+nf_status nf_bucket_health(const float* grads, int64_t worker_stride, int32_t W, int64_t n,
+                           const uint64_t* mask, nf_worker_stats* stats, void* ws,
+                           size_t ws_bytes, void* stream) {
+  NF_TRY(check_grads(grads, worker_stride, W, n));
+  NF_TRY(check_mask(mask, n));
+  if (!stats) return fail(NF_ERR_INVALID_ARG, "stats is NULL");
+  if (!aligned(stats, 8)) return fail(NF_ERR_ALIGNMENT, "stats not 8-byte aligned");
+  const nf::Geometry geo = nf::make_geometry(W, n, n > 0 ? n : 1);
+  NF_TRY(check_ws(ws, ws_bytes, nf::workspace_layout(geo).total));
+  NF_TRY(run_pass1_decide(geo, grads, worker_stride, mask, nullptr, 0, nullptr, nf::kSumsNone, 0,
+                          stats, nullptr, nullptr, ws, static_cast<hipStream_t>(stream)));
+  return ok();
+}
+
+nf_status nf_pack_signs(const float* grads, int64_t worker_stride, int32_t W, int64_t n,
+                        const uint64_t* mask, uint64_t* bits, int64_t bits_stride_words,
+                        nf_worker_stats* stats, void* ws, size_t ws_bytes, void* stream) {
+  NF_TRY(check_grads(grads, worker_stride, W, n));
+  NF_TRY(check_mask(mask, n));
+  NF_TRY(check_bits(bits, bits_stride_words, n, W));
+  if (!aligned(stats, 8)) return fail(NF_ERR_ALIGNMENT, "stats not 8-byte aligned");
+  const nf::Geometry geo = nf::make_geometry(W, n, n > 0 ? n : 1);
+  NF_TRY(check_ws(ws, ws_bytes, nf::workspace_layout(geo).total));
+  if (n == 0 && !stats) return ok();
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (stats) {
+    NF_TRY(run_pass1_decide(geo, grads, worker_stride, mask, bits, bits_stride_words, nullptr,
+                            nf::kSumsNone, 0, stats, nullptr, nullptr, ws, s));
+  } else {
+    const nf::WorkspaceLayout lay = nf::workspace_layout(geo);
+    char* w = static_cast<char*>(ws);
+    nf::Pass1Args a;
+    a.g = grads;
+    a.wstride = worker_stride;
+    a.mask = mask;
+    a.bits = bits;
+    a.bstride = bits_stride_words;
+    a.out = nullptr;
+    a.part = reinterpret_cast<nf::Partial*>(w + lay.partials);
+    a.part_ne = reinterpret_cast<uint64_t*>(w + lay.ne);
+    a.n_total = geo.n_total;
+    a.bucket_n = geo.bucket_n;
+    a.W = geo.W;
+    a.wg = geo.wg;
+    a.eg = geo.eg;
+    a.T = geo.T;
+    a.bpb = geo.bpb;
+    a.sums = nf::kSumsNone;
+    a.mean = 0;
+    hipError_t e = nf::launch_pass1(geo, a, s);
+    if (e != hipSuccess) return hip_fail(e, "pass-1 launch");
+  }
+  return ok();
+}
+
+nf_status nf_fp32_reduce(const float* grads, int64_t worker_stride, int32_t W, int64_t n,
+                         const uint64_t* mask, int32_t select, int32_t fp32_op, float* out,
+                         void* stream) {
+  NF_TRY(check_grads(grads, worker_stride, W, n));
+  if (select != NF_SEL_ROUTED && select != NF_SEL_ELIGIBLE && select != NF_SEL_ALL)
+    return fail(NF_ERR_INVALID_ARG, "select=%d", select);
+  if (fp32_op != NF_FP32_SUM && fp32_op != NF_FP32_MEAN) return fail(NF_ERR_INVALID_ARG, "fp32_op=%d", fp32_op);
+  if (select != NF_SEL_ALL) NF_TRY(check_mask(mask, n));
+  if (n > 0 && !out) return fail(NF_ERR_INVALID_ARG, "out is NULL");
+  if (!aligned(out, 4)) return fail(NF_ERR_ALIGNMENT, "out not 4-byte aligned");
+  if (n == 0) return ok();
+  const nf::Geometry geo = nf::make_geometry(W, n, n);
+  nf::Pass2Args p = pass2_args(geo);
+  p.g = grads;
+  p.wstride = worker_stride;
+  p.mask = select == NF_SEL_ALL ? nullptr : mask;
+  p.out = out;
+  p.op = nf::kOpFp32;
+  p.select = select;
+  p.mean = fp32_op == NF_FP32_MEAN;
+  hipError_t e = nf::launch_pass2(geo, p, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "fp32 launch");
+  return ok();
+}
+
+nf_status nf_signcount_reduce(const uint64_t* bits, int64_t bits_stride_words, int32_t W, int64_t n,
+                              const uint64_t* mask, const float* scale_dev, int32_t decode_mode,
+                              uint8_t* counts, float* out, void* stream) {
+  if (W < 1 || W > 255) return fail(NF_ERR_INVALID_ARG, "W=%d outside [1, 255]", W);
+  if (n < 0) return fail(NF_ERR_INVALID_ARG, "n < 0");
+  NF_TRY(check_bits(bits, bits_stride_words, n, W));
+  if (decode_mode != NF_DECODE_SOFT && decode_mode != NF_DECODE_MAJORITY)
+    return fail(NF_ERR_INVALID_ARG, "decode_mode=%d", decode_mode);
+  if (out) {
+    NF_TRY(check_mask(mask, n));
+    if (!scale_dev) return fail(NF_ERR_INVALID_ARG, "scale_dev is NULL");
+    if (!aligned(out, 4) || !aligned(scale_dev, 4)) return fail(NF_ERR_ALIGNMENT, "out/scale not 4-byte aligned");
+  }
+  if (n == 0 || (!out && !counts)) return ok();
+  const nf::Geometry geo = nf::make_geometry(W, n, n);
+  nf::Pass2Args p = pass2_args(geo);
+  p.bits = bits;
+  p.bstride = bits_stride_words;
+  p.mask = mask;
+  p.scale = scale_dev;
+  p.counts = counts;
+  p.out = out;
+  p.op = nf::kOpCountDecode;
+  p.decode_mode = decode_mode;
+  hipError_t e = nf::launch_pass2(geo, p, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "signcount launch");
+  return ok();
+}
+
+nf_status nf_route_decide(const nf_worker_stats* stats_host, int32_t W, int64_t n, int64_t n_eligible,
+                          const nf_route_policy* policy_host, nf_route_decision* decision_host) {
+  if (W < 1 || W > 255) return fail(NF_ERR_INVALID_ARG, "W=%d outside [1, 255]", W);
+  if (n < 0 || n_eligible < 0 || n_eligible > n) return fail(NF_ERR_INVALID_ARG, "need 0 <= n_eligible <= n");
+  if (!stats_host || !decision_host) return fail(NF_ERR_INVALID_ARG, "NULL stats or decision");
+  NF_TRY(check_policy(policy_host));
+  int k = 0;
+  for (int w = 0; w < W; ++w) k += nf::finite64(stats_host[w].sum_sq) ? 1 : 0;
+  double med = 0.0;
+  for (int w = 0; w < W; ++w)
+    if (nf::finite64(stats_host[w].sum_sq) && nf::ssq_rank(stats_host, W, w) == (k - 1) / 2)
+      med = stats_host[w].sum_sq;
+  nf::decide_from(stats_host, W, n, n_eligible, *policy_host, k, med, decision_host);
+  return ok();
+}
+
+nf_status nf_route_bucket(const float* grads, int64_t worker_stride, int32_t W, int64_t n,
+                          const uint64_t* mask, const nf_route_policy* policy_host, uint64_t* bits,
+                          int64_t bits_stride_words, uint8_t* counts, float* out,
+                          nf_worker_stats* stats, nf_route_decision* decision, void* ws,
+                          size_t ws_bytes, void* stream) {
+  return route_flat(grads, worker_stride, W, n, n > 0 ? n : 1, mask, policy_host, bits,
+                    bits_stride_words, counts, out, stats, decision, ws, ws_bytes, stream);
+}
+
+nf_status nf_route_buckets(const float* grads, int64_t worker_stride, int32_t W, int64_t n_total,
+                           int64_t bucket_n, const uint64_t* mask, const nf_route_policy* policy_host,
+                           uint64_t* bits, int64_t bits_stride_words, uint8_t* counts, float* out,
+                           nf_worker_stats* stats, nf_route_decision* decisions, void* ws,
+                           size_t ws_bytes, void* stream) {
+  if (bucket_n <= 0) return fail(NF_ERR_INVALID_ARG, "bucket_n must be > 0");
+  if (bucket_n < n_total && bucket_n % 64)
+    return fail(NF_ERR_INVALID_ARG, "bucket_n=%lld must be a multiple of 64", (long long)bucket_n);
+  return route_flat(grads, worker_stride, W, n_total, bucket_n, mask, policy_host, bits,
+                    bits_stride_words, counts, out, stats, decisions, ws, ws_bytes, stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,218 @@
+// nf_internal.h - launch geometry, kernel argument blocks and the route rules
+// shared by the host decision function and the device decision kernel.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "nf.h"
+
+#define NF_HD __host__ __device__
+
+namespace nf {
+
+// ---------------------------------------------------------------- geometry
+//
+// Pass 1 is worker-major: a block is 16 wavefronts; wavefront v serves
+// worker group wg = v % WG and element group eg = v / WG.  With W <= 16 each
+// wavefront owns one worker (WG = W) and the spare wavefronts take further
+// element groups (EG = 16 / W); with W > 16 each wavefront owns
+// ceil(W / 16) workers.  A tile is EG * T consecutive elements of all W
+// rows; T is sized so that staging one tile of all workers in LDS (needed to
+// add the workers in order at FP32-routed positions) takes at most 64 KiB.
+constexpr int kWaves = 16;
+constexpr int kThreads1 = kWaves * 64;
+constexpr int kStageFloats = 16384;      // 64 KiB of LDS
+constexpr int kMaxBlocksPerBucket = 512; // partial-statistics slots per bucket
+
+// Pass 2 is element-major: lane l of a wavefront owns element 64k + l of a
+// word k; a wavefront takes 16 consecutive words per step.
+constexpr int kThreads2 = 256;
+constexpr int kWordsPerWave2 = 16;
+constexpr int kMaxBlocks2 = 1024;
+
+// Words per worker and wavefront tile for WPW workers per wavefront: eight
+// words keep pass 1 within 64 VGPRs (eight wavefronts per SIMD) for up to
+// two workers per wavefront; more workers share 16 words.
+constexpr NF_HD int pass1_words(int wpw) { return wpw <= 2 ? 8 : 16 / wpw; }
+
+struct Geometry {
+  int W, wg, eg, wpw, T, tile;
+  int64_t n_total, bucket_n, nb;
+  int bpb;   // pass-1 blocks per bucket (= partial slots per bucket)
+  int bpb2;  // pass-2 blocks per bucket
+};
+
+inline Geometry make_geometry(int W, int64_t n_total, int64_t bucket_n) {
+  Geometry g;
+  g.W = W;
+  g.wg = W < kWaves ? W : kWaves;
+  g.eg = kWaves / g.wg;
+  // Workers per wavefront, rounded up to a power of two (a template
+  // parameter of pass 1); a wavefront's tile then holds 16 / wpw words.
+  int need = (W + g.wg - 1) / g.wg;
+  g.wpw = 1;
+  while (g.wpw < need) g.wpw *= 2;
+  g.T = 64 * pass1_words(g.wpw);  // W * EG * T <= kStageFloats for every W <= 255
+  g.tile = g.eg * g.T;
+  g.n_total = n_total;
+  g.bucket_n = bucket_n;
+  g.nb = n_total <= 0 ? 1 : (n_total + bucket_n - 1) / bucket_n;
+  int64_t full = n_total < bucket_n ? n_total : bucket_n;
+  int64_t tiles = (full + g.tile - 1) / g.tile;
+  if (tiles < 1) tiles = 1;
+  g.bpb = (int)(tiles < kMaxBlocksPerBucket ? tiles : kMaxBlocksPerBucket);
+  int64_t words = (full + 63) / 64;
+  int64_t chunks = (words + kWordsPerWave2 * 4 - 1) / (kWordsPerWave2 * 4);
+  if (chunks < 1) chunks = 1;
+  g.bpb2 = (int)(chunks < kMaxBlocks2 ? chunks : kMaxBlocks2);
+  return g;
+}
+
+// Per (bucket, block, worker) partial statistics written by pass 1.
+struct Partial {
+  double sabs;
+  double ssq;
+  uint64_t nonfinite;
+};
+
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct WorkspaceLayout {
+  size_t partials, ne, total;
+};
+
+inline WorkspaceLayout workspace_layout(const Geometry& g) {
+  WorkspaceLayout l;
+  size_t slots = (size_t)g.nb * (size_t)g.bpb;
+  l.partials = 0;
+  l.ne = align256(slots * (size_t)g.W * sizeof(Partial));
+  l.total = l.ne + align256(slots * sizeof(uint64_t));
+  return l;
+}
+
+// ------------------------------------------------------- kernel arguments
+
+enum SumMode { kSumsNone = 0, kSumsRouted = 1, kSumsAll = 2 };
+
+struct Pass1Args {
+  const float* g;
+  int64_t wstride;
+  const uint64_t* mask;
+  uint64_t* bits;  // NULL: no sign payload
+  int64_t bstride;
+  float* out;      // FP32 sums (sum mode != none)
+  Partial* part;
+  uint64_t* part_ne;
+  int64_t n_total, bucket_n;
+  int32_t W, wg, eg, T, bpb, sums, mean;
+};
+
+struct DecideArgs {
+  const Partial* part;
+  const uint64_t* part_ne;
+  nf_worker_stats* stats;
+  nf_route_decision* dec;  // NULL: statistics only
+  nf_route_policy pol;
+  int64_t n_total, bucket_n;
+  int32_t W, bpb;
+};
+
+enum Pass2Op { kOpCountDecode = 0, kOpFp32 = 1, kOpFromDecision = 2 };
+
+struct Pass2Args {
+  const uint64_t* bits;
+  int64_t bstride;
+  const float* g;
+  int64_t wstride;
+  const uint64_t* mask;
+  const nf_route_decision* dec;  // kOpFromDecision: route and scale per bucket
+  const float* scale;            // kOpCountDecode standalone
+  uint8_t* counts;
+  float* out;
+  int64_t n_total, bucket_n;
+  int32_t W, op, select, decode_mode, mean, bpb2;
+};
+
+// ------------------------------------------------------------ route rules
+//
+// Reasons and route of one bucket (§3.2 route states, §6.4 guard).  The
+// caller supplies the lower median of the finite sums of squares (k finite
+// values, median valid when k >= 2); host and device compute it by rank.
+
+NF_HD inline float bucket_scale(const nf_worker_stats* st, int W, int64_t ne) {
+  if (ne <= 0) return 0.0f;
+  double acc = 0.0;
+  for (int w = 0; w < W; ++w) acc += st[w].sum_abs_elig / (double)ne;
+  return (float)(acc / (double)W);
+}
+
+NF_HD inline bool finite64(double x) { return x - x == 0.0; }
+
+NF_HD inline void decide_from(const nf_worker_stats* st, int W, int64_t n, int64_t ne,
+                              const nf_route_policy& p, int kfinite, double median,
+                              nf_route_decision* d) {
+  uint32_t r = 0;
+  if (!p.admitted) r |= NF_REASON_NOT_ADMITTED;
+  if (ne == 0) r |= NF_REASON_NO_ELIGIBLE;
+  if (p.veto) r |= NF_REASON_VETO;
+  if (!p.guard_ok) r |= NF_REASON_GUARD;
+  uint64_t nonf = 0;
+  bool zero = false, spike = false;
+  double thr = (p.kappa * p.kappa) * median;
+  for (int w = 0; w < W; ++w) {
+    nonf += st[w].nonfinite;
+    if (st[w].sum_abs_elig == 0.0) zero = true;
+    if (kfinite >= 2 && finite64(st[w].sum_sq) && st[w].sum_sq > thr) spike = true;
+  }
+  if (nonf) r |= NF_REASON_NONFINITE;
+  if (zero && ne > 0) r |= NF_REASON_ZERO_WORKER;
+  if (spike) r |= NF_REASON_NORM_SPIKE;
+  int32_t route;
+  if (r & (NF_REASON_NOT_ADMITTED | NF_REASON_NO_ELIGIBLE)) {
+    route = NF_ROUTE_PLAIN;
+  } else if (p.force_lowbit) {
+    route = NF_ROUTE_LOWBIT;
+    r |= NF_REASON_FORCED;
+  } else if (r & (NF_REASON_VETO | NF_REASON_GUARD | NF_REASON_NONFINITE |
+                  NF_REASON_ZERO_WORKER | NF_REASON_NORM_SPIKE)) {
+    route = NF_ROUTE_FALLBACK;
+  } else {
+    route = NF_ROUTE_LOWBIT;
+  }
+  d->route = route;
+  d->reasons = r;
+  d->scale = bucket_scale(st, W, ne);
+  d->reserved = 0;
+  d->n_eligible = ne;
+  d->bytes_fp32 = 4.0 * (double)n;
+  d->bytes_route = route == NF_ROUTE_LOWBIT
+                       ? (double)ne / 8.0 + 4.0 + 4.0 * (double)(n - ne)
+                       : 4.0 * (double)n;
+}
+
+// Rank of worker w among the finite sums of squares (ties by index).
+NF_HD inline int ssq_rank(const nf_worker_stats* st, int W, int w) {
+  double v = st[w].sum_sq;
+  int rank = 0;
+  for (int u = 0; u < W; ++u) {
+    double x = st[u].sum_sq;
+    if (!finite64(x)) continue;
+    if (x < v || (x == v && u < w)) ++rank;
+  }
+  return rank;
+}
+
+// Decode value for count c: SOFT fl32((2c - W) / W), MAJORITY sign with tie 0.
+NF_HD inline float decode_q(int c, int W, int mode) {
+  int margin = 2 * c - W;
+  if (mode == NF_DECODE_MAJORITY) return margin > 0 ? 1.0f : (margin < 0 ? -1.0f : 0.0f);
+  return (float)margin / (float)W;
+}
+
+// Launchers (nf_kernels.hip).
+hipError_t launch_pass1(const Geometry& geo, const Pass1Args& a, hipStream_t s);
+hipError_t launch_decide(const Geometry& geo, const DecideArgs& a, hipStream_t s);
+hipError_t launch_pass2(const Geometry& geo, const Pass2Args& a, hipStream_t s);
+
+}  // namespace nf

@@ -1,0 +1,139 @@
+"""The C-ABI library on the host (no GPU): it loads, exports every function
+include/nf.h declares, its host functions agree with the oracle, and invalid
+arguments return error codes before anything is launched."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle as nfo
+import paper_2606_25759_amd as nf
+import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    src = open(os.path.join(ROOT, "include", "nf.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(nf_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_exports_every_declared_function():
+    lib = nf.load()
+    decl = declared_functions()
+    assert len(decl) >= 12
+    for name in decl:
+        assert hasattr(lib, name), f"{name} not exported"
+    assert sorted(nf.EXPORTS) == decl
+
+
+def test_abi_version_and_struct_sizes():
+    assert nf.nf_abi_version() == 1
+    assert ctypes.sizeof(nf.nf_worker_stats) == 24 == nf.STATS_DTYPE.itemsize
+    assert ctypes.sizeof(nf.nf_route_decision) == 40 == nf.DECISION_DTYPE.itemsize
+    assert ctypes.sizeof(nf.nf_route_policy) == 32
+
+
+@pytest.mark.parametrize("n", [0, 1, 63, 64, 65, 1000, 100_003])
+def test_mask_from_segments_matches_oracle(n):
+    lay = synth.small(1, n, 31 + n, elig_frac=0.6, nruns=17)
+    off, ln, el = synth.mask_segments(lay)
+    a = nf.nf_mask_from_segments(off, ln, el, n)
+    b = nfo.mask_from_segments(off, ln, el, n)
+    assert np.array_equal(a, b)
+
+
+def test_mask_from_segments_rejects_out_of_range():
+    with pytest.raises(nf.NFError) as e:
+        nf.nf_mask_from_segments([5], [10], [1], 12)
+    assert e.value.status == nf.NF_ERR_INVALID_ARG
+    with pytest.raises(nf.NFError):
+        nf.nf_mask_from_segments([-1], [1], [1], 12)
+
+
+def test_route_decide_host_matches_oracle():
+    rng = np.random.default_rng(5)
+    for trial in range(3000):
+        W = int(rng.integers(1, 20))
+        st = np.zeros(W, dtype=nf.STATS_DTYPE)
+        st["sum_abs_elig"] = rng.choice([0.0, 1.0, 2.5, 1e-7], size=W)
+        st["sum_sq"] = rng.choice([0.0, 1.0, 2.0, 16.0, 17.0, 40.0, np.inf, np.nan], size=W)
+        st["nonfinite"] = rng.choice([0, 0, 0, 3], size=W)
+        n = int(rng.integers(0, 1000))
+        ne = int(rng.integers(0, n + 1))
+        kw = dict(admitted=int(rng.integers(0, 2)), veto=int(rng.integers(0, 2)),
+                  guard_ok=int(rng.integers(0, 2)), force_lowbit=int(rng.integers(0, 2)),
+                  kappa=float(rng.choice([1.0, 2.0, 4.0, 3.5])))
+        d = nf.nf_route_decide(st, n, ne, nf.policy(**kw))
+        rd = nfo.decide(st, n, ne, nfo.policy(**kw))
+        assert (d.route, d.reasons, d.n_eligible) == (rd.route, rd.reasons, rd.n_eligible), trial
+        assert d.bytes_route == rd.bytes_route and d.bytes_fp32 == rd.bytes_fp32
+        assert np.float32(d.scale) == np.float32(rd.scale)
+
+
+def test_route_decide_worked_example():
+    """The W=3 worked bucket's statistics give route L, reasons 0."""
+    st = np.zeros(3, dtype=nf.STATS_DTYPE)
+    st["sum_abs_elig"] = [1.5, 4.0, 4.25]
+    st["sum_sq"] = [5.25, 22.5, 74.0625]
+    d = nf.nf_route_decide(st, 4, 3)
+    assert (d.route, d.reasons) == (nf.NF_ROUTE_LOWBIT, 0)
+    assert np.float32(d.scale).view(np.uint32) == 0x3F8AAAAB
+    assert d.bytes_route == 8.375 and d.bytes_fp32 == 16.0
+
+
+def _lib():
+    return nf.load()
+
+
+def test_invalid_arguments_return_codes_without_launch():
+    lib = _lib()
+    P = ctypes.c_void_p
+    fake = P(0x1000)          # never dereferenced: validation fails first
+    ws = P(0x100000)
+    # W out of range
+    assert lib.nf_bucket_health(fake, 64, 0, 64, fake, fake, ws, 1 << 20, None) == nf.NF_ERR_INVALID_ARG
+    assert lib.nf_bucket_health(fake, 64, 256, 64, fake, fake, ws, 1 << 20, None) == nf.NF_ERR_INVALID_ARG
+    assert "W=256" in nf.nf_last_error()
+    # stride < n
+    assert lib.nf_fp32_reduce(fake, 10, 2, 64, fake, 0, 0, fake, None) == nf.NF_ERR_INVALID_ARG
+    # misaligned gradients / stride
+    assert lib.nf_fp32_reduce(P(0x1004), 64, 2, 64, fake, 0, 0, fake, None) == nf.NF_ERR_ALIGNMENT
+    assert lib.nf_fp32_reduce(fake, 66, 2, 64, fake, 0, 0, fake, None) == nf.NF_ERR_ALIGNMENT
+    # bad select / op
+    assert lib.nf_fp32_reduce(fake, 64, 2, 64, fake, 9, 0, fake, None) == nf.NF_ERR_INVALID_ARG
+    assert lib.nf_fp32_reduce(fake, 64, 2, 64, fake, 0, 9, fake, None) == nf.NF_ERR_INVALID_ARG
+    # bits stride too small
+    assert lib.nf_pack_signs(fake, 640, 2, 640, fake, fake, 9, None, ws, 1 << 20, None) == nf.NF_ERR_INVALID_ARG
+    # workspace too small
+    need = nf.nf_workspace_bytes(2, 640)
+    assert need > 0
+    assert lib.nf_pack_signs(fake, 640, 2, 640, fake, fake, 10, None, ws, need - 1, None) == nf.NF_ERR_WORKSPACE
+    # policy checks
+    pol = nf.policy(kappa=0.0)
+    assert lib.nf_route_bucket(fake, 640, 2, 640, fake, ctypes.byref(pol), fake, 10, None, fake, fake, fake,
+                               ws, 1 << 24, None) == nf.NF_ERR_INVALID_ARG
+    pol = nf.policy(decode_mode=5)
+    assert lib.nf_route_bucket(fake, 640, 2, 640, fake, ctypes.byref(pol), fake, 10, None, fake, fake, fake,
+                               ws, 1 << 24, None) == nf.NF_ERR_INVALID_ARG
+    # bucket size not a multiple of 64
+    pol = nf.policy()
+    assert lib.nf_route_buckets(fake, 6400, 2, 6400, 100, fake, ctypes.byref(pol), fake, 100, None, fake,
+                                fake, fake, ws, 1 << 24, None) == nf.NF_ERR_INVALID_ARG
+    # decode counts: W out of range
+    assert lib.nf_signcount_reduce(fake, 10, 0, 640, fake, fake, 0, fake, fake, None) == nf.NF_ERR_INVALID_ARG
+    # decision: n_eligible > n
+    st = (nf.nf_worker_stats * 2)()
+    d = nf.nf_route_decision()
+    assert lib.nf_route_decide(st, 2, 10, 11, ctypes.byref(pol), ctypes.byref(d)) == nf.NF_ERR_INVALID_ARG
+
+
+def test_workspace_sizes():
+    assert nf.nf_workspace_bytes(0, 10) == 0
+    a = nf.nf_workspace_bytes(16, 6_553_600)
+    b = nf.nf_workspace_bytes_buckets(16, 6_553_600 * 201, 6_553_600)
+    assert 0 < a and b >= 201 * a // 2
+    assert nf.nf_workspace_bytes_buckets(16, 100, 0) == 0
