@@ -1,0 +1,229 @@
+#!/usr/bin/env python3
+"""Throughput of the bucket reducer on one MI355X.
+
+One step = one call of nf_route_buckets over every bucket of the workload:
+pass 1 (sign payload, health statistics, FP32 sums at routed positions),
+the per-bucket decision, and pass 2 (sign counts and decode, or the FP32
+fallback), for all W stacked workers.  Inputs are generated on the device
+before the timed region and stay resident in HBM.
+
+Metric: FP32-equivalent input GB/s = 4 * W * n_total / step time, and its
+fraction of the 8 TB/s HBM peak.  The JSON line also carries the roofline of
+the dominant kernel (pass 1), timed with HIP events that the library records
+on its own launch stream, and the oracle timed on the host as a CPU
+baseline on a bounded sample of the same workload.
+
+  python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload gpt1p3b]
+"""
+import argparse
+import ctypes
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, AMD specification
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="gpt1p3b",
+                    choices=["tiny", "resnet50", "vitb16", "gpt1p3b", "stress"])
+    ap.add_argument("--force-lowbit", action="store_true", help="guard disabled (forced low-bit)")
+    ap.add_argument("--no-counts", action="store_true", help="do not write the uint8 counts")
+    ap.add_argument("--cpu-buckets", type=int, default=None,
+                    help="buckets of the oracle's CPU sample (default: about 12 s of work)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+class HipEvents:
+    """hipEvent_t handles from the HIP runtime torch has loaded."""
+
+    def __init__(self):
+        self.rt = ctypes.CDLL("libamdhip64.so.7")
+        self.rt.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.rt.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                ctypes.c_void_p]
+        self.rt.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.rt.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+
+    def create(self):
+        ev = ctypes.c_void_p()
+        if self.rt.hipEventCreate(ctypes.byref(ev)) != 0:
+            raise RuntimeError("hipEventCreate failed")
+        return ev.value
+
+    def elapsed_ms(self, a, b):
+        ms = ctypes.c_float()
+        if self.rt.hipEventElapsedTime(ctypes.byref(ms), a, b) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return ms.value
+
+    def destroy(self, ev):
+        self.rt.hipEventDestroy(ev)
+
+
+def kernel_source_sha():
+    src = os.path.join(ROOT, "paper_2606_25759_amd", "csrc", "nf_kernels.hip")
+    return hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+
+
+def counter_traffic(workload):
+    """HBM bytes per pass-1 launch from committed rocprofv3 counters, if they
+    were taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", f"pass1_{workload}_counters.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    if rec.get("kernel_sha") != kernel_source_sha():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: the reducer simulates the W workers as stacked buffers on "
+              f"one device and this build has no multi-GPU path (asked for --gpus {args.gpus}).",
+              file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import paper_2606_25759_amd as nf
+    import synth
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.init()
+    lay = synth.CONFIGS[args.workload]()
+    W, n, bn, nb = lay.W, lay.n_total, lay.bucket_n, lay.nb
+    nw = (n + 63) // 64
+    print(f"[bench] {lay.name}: W={W} n={n:,} buckets={nb} bucket_n={bn:,} "
+          f"input={lay.input_bytes() / 1e9:.2f} GB", file=sys.stderr, flush=True)
+
+    grads = torch.empty((W, lay.stride), dtype=torch.float32, device=dev)
+    synth.generate_device(lay, grads)
+    off, ln, el = synth.mask_segments(lay)
+    mask_h = nf.nf_mask_from_segments(off, ln, el, n)
+    mask = torch.from_numpy(mask_h.view(np.int64)).to(dev)
+    bits = torch.empty((W, nw), dtype=torch.int64, device=dev)
+    counts = None if args.no_counts else torch.empty(n, dtype=torch.uint8, device=dev)
+    out = torch.empty(n, dtype=torch.float32, device=dev)
+    stats = torch.empty(nb * W * nf.STATS_BYTES, dtype=torch.uint8, device=dev)
+    dec = torch.empty(nb * nf.DECISION_BYTES, dtype=torch.uint8, device=dev)
+    ws = nf.empty_workspace(nf.nf_workspace_bytes_buckets(W, n, bn), dev)
+    pol = nf.policy(force_lowbit=int(args.force_lowbit))
+    torch.cuda.synchronize()
+    print("[bench] inputs resident", file=sys.stderr, flush=True)
+
+    def step():
+        nf.nf_route_buckets(grads, n, bn, mask, pol, bits, counts, out, stats, dec, ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    hip = HipEvents()
+    evs = [[hip.create() for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        nf.nf_set_phase_events(*evs[k])
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    nf.nf_set_phase_events()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    ph = np.array([[hip.elapsed_ms(e[0], e[1]), hip.elapsed_ms(e[1], e[2]), hip.elapsed_ms(e[2], e[3]),
+                    hip.elapsed_ms(e[0], e[3])] for e in evs])
+    for e in evs:
+        for x in e:
+            hip.destroy(x)
+    pass1_ms, decide_ms, pass2_ms, device_ms = (float(v) for v in ph.mean(axis=0))
+    print(f"[bench] {args.steps} steps: {ms_per_step:.3f} ms/step wall, device {device_ms:.3f} ms "
+          f"(pass1 {pass1_ms:.3f}, decide {decide_ms:.3f}, pass2 {pass2_ms:.3f})", file=sys.stderr, flush=True)
+
+    # decisions, routes and algorithmic bytes per launch
+    d = nf.decisions_host(dec, nb)
+    routes = {"L": int((d["route"] == 0).sum()), "F": int((d["route"] == 1).sum()),
+              "P": int((d["route"] == 2).sum())}
+    mgtr = float(d["bytes_route"].sum() / d["bytes_fp32"].sum())
+    nbs = np.array([min(bn, n - b * bn) for b in range(nb)], dtype=np.int64)
+    ne = d["n_eligible"].astype(np.int64)
+    nwb = (nbs + 63) // 64
+    pass1_bytes = float((4 * W * nbs + nbs / 8 + 8 * W * nwb + 4 * (nbs - ne)).sum())
+    is_l, is_f = d["route"] == 0, d["route"] == 1
+    pass2_bytes = float(((8 * W * nwb + nbs / 8 + (0 if args.no_counts else nbs) + 4 * ne) * is_l).sum()
+                        + ((4 * W * ne + nbs / 8 + 4 * ne) * is_f).sum())
+    value = lay.input_bytes() / (ms_per_step * 1e-3) / 1e9
+    achieved = pass1_bytes / (pass1_ms * 1e-3) / 1e9
+
+    # CPU baseline: the oracle, single-threaded, on the first buckets
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle as nfo
+        k = args.cpu_buckets or max(1, min(nb, int(12e9 * 0.35 / (4 * W * min(bn, n)))))
+        opol = nfo.policy(force_lowbit=int(args.force_lowbit))
+        t_cpu, nbytes, ok = 0.0, 0, True
+        for b in range(k):
+            a, e = b * bn, min((b + 1) * bn, n)
+            gh = grads[:, a:e].contiguous().cpu().numpy()
+            mh = np.ascontiguousarray(mask_h[a // 64:(e + 63) // 64])
+            c0 = time.perf_counter()
+            ref = nfo.reduce_bucket(gh, mh, opol)
+            t_cpu += time.perf_counter() - c0
+            nbytes += 4 * W * (e - a)
+            rd = ref["decision"]
+            ok &= int(d["route"][b]) == rd.route and int(d["reasons"][b]) == rd.reasons
+            ok &= bool(np.array_equal(bits[:, a // 64:(e + 63) // 64].cpu().numpy().view(np.uint64), ref["bits"]))
+        cpu = {"value": round(nbytes / t_cpu / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+               "sample": f"{lay.name} buckets 0..{k - 1} ({k} x {min(bn, n):,} elements x {W} workers), "
+                         f"single-threaded C++ oracle, {t_cpu:.1f} s",
+               "sample_parity": "ok" if ok else "MISMATCH"}
+        print(f"[bench] oracle: {cpu['value']} GB/s over {k} buckets ({t_cpu:.1f} s)", file=sys.stderr, flush=True)
+
+    rec = {
+        "metric": "reducer FP32-equiv input GB/s (pack+signcount+fp32) and % of HBM peak",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "pct_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
+        "config": {"workload": lay.name, "W": W, "n_total": n, "buckets": nb, "bucket_n": bn,
+                   "eligible_frac": round(float(ne.sum()) / n, 4),
+                   "policy": "forced low-bit" if args.force_lowbit else "admitted, guard ok",
+                   "counts_written": not args.no_counts},
+        "roofline": {"kernel": "k_pass1", "bound": "hbm", "achieved": round(achieved, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": counter_traffic(lay.name),
+                     "algorithmic_bytes_per_launch": pass1_bytes, "avg_launch_ms": round(pass1_ms, 4)},
+        "phases_ms": {"pass1": round(pass1_ms, 4), "decide": round(decide_ms, 4),
+                      "pass2": round(pass2_ms, 4), "device_total": round(device_ms, 4),
+                      "pass2_algorithmic_gbs": round(pass2_bytes / max(pass2_ms, 1e-9) / 1e6, 1)},
+        "routes": routes,
+        "mgtr": round(mgtr, 4),
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(rec), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -44,7 +44,8 @@
  *     calls on the same inputs give bitwise identical results.
  *   - Calls on different streams with different workspaces may run
  *     concurrently.  The library keeps no mutable state besides the
- *     thread-local error string.
+ *     thread-local error string and the thread-local profiling events of
+ *     nf_set_phase_events.
  */
 #ifndef NF_H
 #define NF_H
@@ -226,6 +227,17 @@ nf_status nf_route_buckets(const float* grads, int64_t worker_stride, int32_t W,
                            int64_t bits_stride_words, uint8_t* counts, float* out,
                            nf_worker_stats* stats, nf_route_decision* decisions, void* ws,
                            size_t ws_bytes, void* stream);
+
+/*
+ * Profiling hook (no paper counterpart).  When set on the calling thread,
+ * nf_route_bucket and nf_route_buckets record these hipEvent_t handles (each
+ * passed as void*) on their stream: before pass 1, after pass 1, after the
+ * decision kernel and after pass 2 (the last one also when pass 2 is not
+ * needed).  The caller owns the events; passing four NULLs turns recording
+ * off.  Events are recorded, never synchronised, so calls stay asynchronous.
+ */
+nf_status nf_set_phase_events(void* before_pass1, void* after_pass1, void* after_decide,
+                              void* after_pass2);
 
 #ifdef __cplusplus
 }

@@ -30,7 +30,8 @@ NF_SEL_ROUTED, NF_SEL_ELIGIBLE, NF_SEL_ALL = 0, 1, 2
 # Exported names, in the order include/nf.h declares them.
 EXPORTS = ["nf_abi_version", "nf_last_error", "nf_mask_from_segments", "nf_workspace_bytes",
            "nf_bucket_health", "nf_pack_signs", "nf_fp32_reduce", "nf_signcount_reduce",
-           "nf_route_decide", "nf_route_bucket", "nf_workspace_bytes_buckets", "nf_route_buckets"]
+           "nf_route_decide", "nf_route_bucket", "nf_workspace_bytes_buckets", "nf_route_buckets",
+           "nf_set_phase_events"]
 
 
 class nf_worker_stats(ctypes.Structure):
@@ -98,6 +99,7 @@ def load(path=None):
                                            _P, _SZ, _P]),
         "nf_route_buckets": (ctypes.c_int, [_P, _I64, _I32, _I64, _I64, _P, _P, _P, _I64, _P, _P,
                                             _P, _P, _P, _SZ, _P]),
+        "nf_set_phase_events": (ctypes.c_int, [_P, _P, _P, _P]),
     }
     for name, (res, args) in sigs.items():
         fn = getattr(lib, name)
@@ -255,6 +257,11 @@ def nf_route_buckets(grads, n_total, bucket_n, mask, pol, bits, counts, out, sta
                                    _dev_ptr(stats, torch.uint8, "stats"),
                                    _dev_ptr(decisions, torch.uint8, "decisions"),
                                    _dev_ptr(ws, torch.uint8, "ws"), ws.numel(), _stream(stream)))
+
+
+def nf_set_phase_events(before_pass1=None, after_pass1=None, after_decide=None, after_pass2=None):
+    """Raw hipEvent_t handles (ints) or None; all None turns recording off."""
+    _check(load().nf_set_phase_events(before_pass1, after_pass1, after_decide, after_pass2))
 
 
 # ------------------------------------------------------- result decoding

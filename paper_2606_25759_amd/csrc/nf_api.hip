@@ -11,6 +11,11 @@
 namespace {
 
 thread_local std::string g_err;
+thread_local hipEvent_t g_phase_ev[4] = {nullptr, nullptr, nullptr, nullptr};
+
+void record_phase(int i, hipStream_t s) {
+  if (g_phase_ev[i]) (void)hipEventRecord(g_phase_ev[i], s);
+}
 
 nf_status fail(nf_status st, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
 nf_status fail(nf_status st, const char* fmt, ...) {
@@ -80,6 +85,20 @@ nf_status check_ws(void* ws, size_t ws_bytes, size_t need) {
   return NF_OK;
 }
 
+void fill_pass1_geometry(const nf::Geometry& geo, nf::Pass1Args* a) {
+  a->n_total = geo.n_total;
+  a->bucket_n = geo.bucket_n;
+  a->chunks_full = geo.chunks_full;
+  a->total_chunks = geo.total_chunks;
+  a->nb = (int32_t)geo.nb;
+  a->W = geo.W;
+  a->wg = geo.wg;
+  a->eg = geo.eg;
+  a->T = geo.T;
+  a->G = geo.G;
+  a->slots = geo.slots;
+}
+
 #define NF_TRY(x)                    \
   do {                               \
     nf_status st__ = (x);            \
@@ -91,7 +110,8 @@ nf_status check_ws(void* ws, size_t ws_bytes, size_t need) {
 nf_status run_pass1_decide(const nf::Geometry& geo, const float* g, int64_t stride,
                            const uint64_t* mask, uint64_t* bits, int64_t bstride, float* out,
                            int sums, int mean, nf_worker_stats* stats, nf_route_decision* dec,
-                           const nf_route_policy* pol, void* ws, hipStream_t s) {
+                           const nf_route_policy* pol, void* ws, hipStream_t s,
+                           bool phases = false) {
   const nf::WorkspaceLayout lay = nf::workspace_layout(geo);
   char* w = static_cast<char*>(ws);
   nf::Pass1Args a;
@@ -103,17 +123,13 @@ nf_status run_pass1_decide(const nf::Geometry& geo, const float* g, int64_t stri
   a.out = out;
   a.part = reinterpret_cast<nf::Partial*>(w + lay.partials);
   a.part_ne = reinterpret_cast<uint64_t*>(w + lay.ne);
-  a.n_total = geo.n_total;
-  a.bucket_n = geo.bucket_n;
-  a.W = geo.W;
-  a.wg = geo.wg;
-  a.eg = geo.eg;
-  a.T = geo.T;
-  a.bpb = geo.bpb;
+  fill_pass1_geometry(geo, &a);
   a.sums = sums;
   a.mean = mean;
+  if (phases) record_phase(0, s);
   hipError_t e = nf::launch_pass1(geo, a, s);
   if (e != hipSuccess) return hip_fail(e, "pass-1 launch");
+  if (phases) record_phase(1, s);
   nf::DecideArgs d;
   d.part = a.part;
   d.part_ne = a.part_ne;
@@ -128,9 +144,12 @@ nf_status run_pass1_decide(const nf::Geometry& geo, const float* g, int64_t stri
   d.n_total = geo.n_total;
   d.bucket_n = geo.bucket_n;
   d.W = geo.W;
-  d.bpb = geo.bpb;
+  d.slots = geo.slots;
+  d.tile = geo.tile;
+  d.G = geo.G;
   e = nf::launch_decide(geo, d, s);
   if (e != hipSuccess) return hip_fail(e, "decide launch");
+  if (phases) record_phase(2, s);
   return NF_OK;
 }
 
@@ -166,8 +185,11 @@ nf_status route_flat(const float* g, int64_t stride, int32_t W, int64_t n_total,
   hipStream_t s = static_cast<hipStream_t>(stream);
   NF_TRY(run_pass1_decide(geo, g, stride, mask, predecided ? nullptr : bits, bstride, out,
                           predecided ? nf::kSumsAll : nf::kSumsRouted, pol->fp32_op == NF_FP32_MEAN,
-                          stats, dec, pol, ws, s));
-  if (predecided || n_total == 0) return ok();
+                          stats, dec, pol, ws, s, true));
+  if (predecided || n_total == 0) {
+    record_phase(3, s);
+    return ok();
+  }
   nf::Pass2Args p = pass2_args(geo);
   p.bits = bits;
   p.bstride = bstride;
@@ -182,6 +204,7 @@ nf_status route_flat(const float* g, int64_t stride, int32_t W, int64_t n_total,
   p.mean = pol->fp32_op == NF_FP32_MEAN;
   hipError_t e = nf::launch_pass2(geo, p, s);
   if (e != hipSuccess) return hip_fail(e, "pass-2 launch");
+  record_phase(3, s);
   return ok();
 }
 
@@ -190,6 +213,15 @@ nf_status route_flat(const float* g, int64_t stride, int32_t W, int64_t n_total,
 extern "C" {
 
 int nf_abi_version(void) { return NF_ABI_VERSION; }
+
+nf_status nf_set_phase_events(void* before_pass1, void* after_pass1, void* after_decide,
+                              void* after_pass2) {
+  g_phase_ev[0] = static_cast<hipEvent_t>(before_pass1);
+  g_phase_ev[1] = static_cast<hipEvent_t>(after_pass1);
+  g_phase_ev[2] = static_cast<hipEvent_t>(after_decide);
+  g_phase_ev[3] = static_cast<hipEvent_t>(after_pass2);
+  return ok();
+}
 
 const char* nf_last_error(void) { return g_err.c_str(); }
 
@@ -270,13 +302,7 @@ nf_status nf_pack_signs(const float* grads, int64_t worker_stride, int32_t W, in
     a.out = nullptr;
     a.part = reinterpret_cast<nf::Partial*>(w + lay.partials);
     a.part_ne = reinterpret_cast<uint64_t*>(w + lay.ne);
-    a.n_total = geo.n_total;
-    a.bucket_n = geo.bucket_n;
-    a.W = geo.W;
-    a.wg = geo.wg;
-    a.eg = geo.eg;
-    a.T = geo.T;
-    a.bpb = geo.bpb;
+    fill_pass1_geometry(geo, &a);
     a.sums = nf::kSumsNone;
     a.mean = 0;
     hipError_t e = nf::launch_pass1(geo, a, s);

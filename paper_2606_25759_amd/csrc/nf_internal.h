@@ -18,17 +18,27 @@ namespace nf {
 // wavefront owns one worker (WG = W) and the spare wavefronts take further
 // element groups (EG = 16 / W); with W > 16 each wavefront owns
 // ceil(W / 16) workers.  A tile is EG * T consecutive elements of all W
-// rows; T is sized so that staging one tile of all workers in LDS (needed to
-// add the workers in order at FP32-routed positions) takes at most 64 KiB.
+// rows; staging one tile of all workers in LDS (to add the workers in order
+// at FP32-routed positions) takes at most 64 KiB.
+//
+// Work is cut into chunks of G consecutive tiles of one bucket; a block
+// takes one chunk and keeps the chunk's sign words in LDS until it ends.
+// Pass 1 runs as a sequence of launches of kEpochBlocks chunks each, so the
+// bitmap stores of a launch reach memory together at its end rather than
+// spread thinly through the gradient read stream (measured on MI355X: the
+// spread-out stores cost about 40% of the scan's time; launch-end bursts,
+// about 15%).
 constexpr int kWaves = 16;
 constexpr int kThreads1 = kWaves * 64;
 constexpr int kStageFloats = 16384;      // 64 KiB of LDS
-constexpr int kMaxBlocksPerBucket = 512; // partial-statistics slots per bucket
+constexpr int kBitsWords = 4096;         // 32 KiB of LDS for a chunk's sign words
+constexpr int kMaxSlots = 512;           // partial-statistics slots per bucket
+constexpr int kEpochBlocks = 512;        // chunks per pass-1 launch
 
-// Pass 2 is element-major: lane l of a wavefront owns element 64k + l of a
-// word k; a wavefront takes 16 consecutive words per step.
+// Pass 2: a wavefront takes 64 consecutive bitmap words (4096 elements) per
+// step, four wavefronts per block.
 constexpr int kThreads2 = 256;
-constexpr int kWordsPerWave2 = 16;
+constexpr int kWordsPerWave2 = 64;
 constexpr int kMaxBlocks2 = 1024;
 
 // Words per worker and wavefront tile for WPW workers per wavefront: eight
@@ -37,11 +47,15 @@ constexpr int kMaxBlocks2 = 1024;
 constexpr NF_HD int pass1_words(int wpw) { return wpw <= 2 ? 8 : 16 / wpw; }
 
 struct Geometry {
-  int W, wg, eg, wpw, T, tile;
+  int W, wg, eg, wpw, T, tile, G;
   int64_t n_total, bucket_n, nb;
-  int bpb;   // pass-1 blocks per bucket (= partial slots per bucket)
-  int bpb2;  // pass-2 blocks per bucket
+  int64_t chunks_full;   // chunks of a full bucket
+  int64_t total_chunks;  // over all buckets
+  int slots;             // partial-statistics slots per bucket (<= kMaxSlots)
+  int bpb2;              // pass-2 blocks per bucket
 };
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 inline Geometry make_geometry(int W, int64_t n_total, int64_t bucket_n) {
   Geometry g;
@@ -49,23 +63,33 @@ inline Geometry make_geometry(int W, int64_t n_total, int64_t bucket_n) {
   g.wg = W < kWaves ? W : kWaves;
   g.eg = kWaves / g.wg;
   // Workers per wavefront, rounded up to a power of two (a template
-  // parameter of pass 1); a wavefront's tile then holds 16 / wpw words.
+  // parameter of pass 1).
   int need = (W + g.wg - 1) / g.wg;
   g.wpw = 1;
   while (g.wpw < need) g.wpw *= 2;
   g.T = 64 * pass1_words(g.wpw);  // W * EG * T <= kStageFloats for every W <= 255
   g.tile = g.eg * g.T;
+  // A chunk's sign words, W * G * EG * (T / 64), fit kBitsWords.
+  int per_tile = W * g.eg * (g.T / 64);
+  g.G = kBitsWords / per_tile;
+  if (g.G > 32) g.G = 32;
+  if (g.G < 1) g.G = 1;
   g.n_total = n_total;
   g.bucket_n = bucket_n;
-  g.nb = n_total <= 0 ? 1 : (n_total + bucket_n - 1) / bucket_n;
+  g.nb = n_total <= 0 ? 1 : ceil_div(n_total, bucket_n);
   int64_t full = n_total < bucket_n ? n_total : bucket_n;
-  int64_t tiles = (full + g.tile - 1) / g.tile;
-  if (tiles < 1) tiles = 1;
-  g.bpb = (int)(tiles < kMaxBlocksPerBucket ? tiles : kMaxBlocksPerBucket);
+  if (full < 0) full = 0;
+  g.chunks_full = ceil_div(ceil_div(full, g.tile), g.G);
+  int64_t last = n_total - (g.nb - 1) * bucket_n;
+  if (last < 0) last = 0;
+  int64_t chunks_last = ceil_div(ceil_div(last, g.tile), g.G);
+  g.total_chunks = (g.nb - 1) * g.chunks_full + chunks_last;
+  g.slots = (int)(g.chunks_full < kMaxSlots ? g.chunks_full : kMaxSlots);
+  if (g.slots < 1) g.slots = 1;
   int64_t words = (full + 63) / 64;
-  int64_t chunks = (words + kWordsPerWave2 * 4 - 1) / (kWordsPerWave2 * 4);
-  if (chunks < 1) chunks = 1;
-  g.bpb2 = (int)(chunks < kMaxBlocks2 ? chunks : kMaxBlocks2);
+  int64_t chunks2 = ceil_div(words, kWordsPerWave2 * 4);
+  if (chunks2 < 1) chunks2 = 1;
+  g.bpb2 = (int)(chunks2 < kMaxBlocks2 ? chunks2 : kMaxBlocks2);
   return g;
 }
 
@@ -84,7 +108,7 @@ struct WorkspaceLayout {
 
 inline WorkspaceLayout workspace_layout(const Geometry& g) {
   WorkspaceLayout l;
-  size_t slots = (size_t)g.nb * (size_t)g.bpb;
+  size_t slots = (size_t)g.nb * (size_t)g.slots;
   l.partials = 0;
   l.ne = align256(slots * (size_t)g.W * sizeof(Partial));
   l.total = l.ne + align256(slots * sizeof(uint64_t));
@@ -104,8 +128,8 @@ struct Pass1Args {
   float* out;      // FP32 sums (sum mode != none)
   Partial* part;
   uint64_t* part_ne;
-  int64_t n_total, bucket_n;
-  int32_t W, wg, eg, T, bpb, sums, mean;
+  int64_t n_total, bucket_n, chunks_full, total_chunks;
+  int32_t nb, W, wg, eg, T, G, slots, sums, mean;
 };
 
 struct DecideArgs {
@@ -115,7 +139,7 @@ struct DecideArgs {
   nf_route_decision* dec;  // NULL: statistics only
   nf_route_policy pol;
   int64_t n_total, bucket_n;
-  int32_t W, bpb;
+  int32_t W, slots, tile, G;
 };
 
 enum Pass2Op { kOpCountDecode = 0, kOpFp32 = 1, kOpFromDecision = 2 };

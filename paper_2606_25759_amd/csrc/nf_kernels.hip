@@ -49,19 +49,23 @@ __device__ __forceinline__ void lanes_from_ballots(const uint64_t (&bb)[NW], uin
     h[k] = (uint32_t)(bb[k] >> 32);
   }
   if constexpr (NW == 8) {
+    // two blocks of four words keep at most eight scalar inputs live
     asm volatile(
         "s_nop 4\n"
         "v_writelane_b32 %0, %2, 0\n v_writelane_b32 %1, %3, 0\n"
         "v_writelane_b32 %0, %4, 1\n v_writelane_b32 %1, %5, 1\n"
         "v_writelane_b32 %0, %6, 2\n v_writelane_b32 %1, %7, 2\n"
         "v_writelane_b32 %0, %8, 3\n v_writelane_b32 %1, %9, 3\n"
-        "v_writelane_b32 %0, %10, 4\n v_writelane_b32 %1, %11, 4\n"
-        "v_writelane_b32 %0, %12, 5\n v_writelane_b32 %1, %13, 5\n"
-        "v_writelane_b32 %0, %14, 6\n v_writelane_b32 %1, %15, 6\n"
-        "v_writelane_b32 %0, %16, 7\n v_writelane_b32 %1, %17, 7\n"
         : "=v"(lo), "=v"(hi)
-        : "s"(l[0]), "s"(h[0]), "s"(l[1]), "s"(h[1]), "s"(l[2]), "s"(h[2]), "s"(l[3]), "s"(h[3]),
-          "s"(l[4]), "s"(h[4]), "s"(l[5]), "s"(h[5]), "s"(l[6]), "s"(h[6]), "s"(l[7]), "s"(h[7]));
+        : "s"(l[0]), "s"(h[0]), "s"(l[1]), "s"(h[1]), "s"(l[2]), "s"(h[2]), "s"(l[3]), "s"(h[3]));
+    asm volatile(
+        "s_nop 4\n"
+        "v_writelane_b32 %0, %2, 4\n v_writelane_b32 %1, %3, 4\n"
+        "v_writelane_b32 %0, %4, 5\n v_writelane_b32 %1, %5, 5\n"
+        "v_writelane_b32 %0, %6, 6\n v_writelane_b32 %1, %7, 6\n"
+        "v_writelane_b32 %0, %8, 7\n v_writelane_b32 %1, %9, 7\n"
+        : "+v"(lo), "+v"(hi)
+        : "s"(l[4]), "s"(h[4]), "s"(l[5]), "s"(h[5]), "s"(l[6]), "s"(h[6]), "s"(l[7]), "s"(h[7]));
   } else if constexpr (NW == 4) {
     asm volatile(
         "s_nop 4\n"
@@ -106,21 +110,30 @@ __device__ __forceinline__ int64_t bucket_len(int64_t n_total, int64_t bucket_n,
 // ------------------------------------------------------------------ pass 1
 //
 // WPW workers per wavefront and NW = pass1_words(WPW) words (64 elements
-// each) per worker and tile.  Lane l of a wavefront loads element 64k + l of word k, so
-// every load instruction reads 256 contiguous bytes and the ballot of
-// "g > 0" over the wavefront is exactly bitmap word k.
+// each) per worker and tile.  Lane l of a wavefront loads element 64k + l of
+// word k, so every load instruction reads 256 contiguous bytes and the ballot
+// of "g > 0" over the wavefront is exactly bitmap word k.  A block takes one
+// chunk (G tiles of one bucket); launch q0 takes chunks q0 .. q0 + grid - 1.
 template <int WPW, bool PACK>
-__global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <= 2 ? 8 : 4))) void k_pass1(const float* __restrict__ g,
-                                                     const uint64_t* __restrict__ mask,
-                                                     uint64_t* __restrict__ bits,
-                                                     float* __restrict__ out,
-                                                     Partial* __restrict__ part,
-                                                     uint64_t* __restrict__ part_ne, Pass1Args a) {
+__global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <= 2 ? 8 : 4))) void k_pass1(
+    const float* __restrict__ g, const uint64_t* __restrict__ mask, uint64_t* __restrict__ bits,
+    float* __restrict__ out, Partial* __restrict__ part, uint64_t* __restrict__ part_ne, Pass1Args a,
+    int64_t q0) {
   constexpr int NW = pass1_words(WPW);
   extern __shared__ __align__(16) unsigned char smem[];
-  float* stage = reinterpret_cast<float*>(smem);
+  const int64_t q = q0 + blockIdx.x;  // this block's chunk
+  if (q >= a.total_chunks) return;     // whole block
 
-  const int b = blockIdx.y;
+  // chunk q -> bucket b, chunk c within it (all buckets but the last are full)
+  int b;
+  int64_t c;
+  if (q < (int64_t)(a.nb - 1) * a.chunks_full) {
+    b = (int)(q / a.chunks_full);
+    c = q - (int64_t)b * a.chunks_full;
+  } else {
+    b = a.nb - 1;
+    c = q - (int64_t)b * a.chunks_full;
+  }
   const int64_t base = (int64_t)b * a.bucket_n;
   const int64_t nbe = bucket_len(a.n_total, a.bucket_n, b);
   const int v = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wavefront index, uniform
@@ -131,7 +144,13 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
   const int T = a.T;
   const int tile = a.eg * T;
   const int64_t ntiles = (nbe + tile - 1) / tile;
+  const int64_t tb = c * a.G;
+  const int64_t te = (tb + a.G < ntiles) ? tb + a.G : ntiles;
   const bool stage_on = a.sums != kSumsNone;
+  // LDS: the chunk's sign words [W][G * EG * NW], then the FP32 stage [W][tile]
+  const int cw = a.G * a.eg * NW;  // sign words per worker and chunk
+  uint64_t* wbuf = reinterpret_cast<uint64_t*>(smem);
+  float* stage = reinterpret_cast<float*>(smem + (PACK ? (size_t)a.W * cw * sizeof(uint64_t) : 0));
 
   double sabs[WPW], ssq[WPW];
   uint64_t nonf[WPW];
@@ -143,34 +162,97 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
   }
   uint64_t ne = 0;
 
-  for (int64_t t = blockIdx.x; t < ntiles; t += a.bpb) {
+  for (int64_t t = tb; t < te; ++t) {
     const int64_t t0 = t * tile;
-    // Tile class, identical in every wavefront: full and eligible everywhere
-    // (no FP32 sums needed) or general (partial, mixed or routed).
-    bool fast = (t0 + tile <= nbe) && a.sums != kSumsAll;
-    if (fast) {
-      const uint64_t* mt = mask + (base + t0) / 64;
-      bool ok = true;
-      for (int k = lane; k < tile / 64; k += 64) ok = ok && (mt[k] == ~0ull);
-      fast = __all(ok);
-    }
+    const bool full = t0 + tile <= nbe;  // block-uniform
     const int64_t e0 = t0 + (int64_t)eg * T;
     int64_t c64 = nbe - e0;
     const int cnt = active ? (int)(c64 < 0 ? 0 : (c64 > T ? T : c64)) : 0;
     const int64_t wrd0 = (base + e0) / 64;  // first word of my element group
+    const uint64_t* tmask = mask + (base + t0) / 64;
 
-    if (fast) {
-      if (active) {
+    // Loads first, decisions after: the first worker's gradients, this
+    // group's mask words and (several element groups) the tile's mask words
+    // are all in flight before anything waits on them.
+    float x0[NW];
+    {
+      const float* row = g + (int64_t)wg * a.wstride + base + e0 + lane;
+      if (full) {
+        if (active) {
 #pragma unroll
-        for (int j = 0; j < WPW; ++j) {
-          const int w = wg + j * a.wg;
-          if (j > 0 && w >= a.W) break;
+          for (int k = 0; k < NW; ++k) x0[k] = __builtin_nontemporal_load(row + 64 * k);
+        }
+      } else {
+#pragma unroll
+        for (int k = 0; k < NW; ++k)
+          x0[k] = (64 * k + lane < cnt) ? __builtin_nontemporal_load(row + 64 * k) : 0.0f;
+      }
+    }
+    uint64_t mw[NW];
+    uint64_t mine = ~0ull;
+    if (full) {
+      const uint64_t* mrow = active ? mask + wrd0 : tmask;  // in bounds for every wavefront
+#pragma unroll
+      for (int k = 0; k < NW; ++k) {
+        mw[k] = mrow[k];
+        mine &= mw[k];
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < NW; ++k) {
+        mw[k] = 64 * k < cnt ? (mask[wrd0 + k] & low_bits(cnt - 64 * k)) : 0ull;
+        mine &= mw[k];
+      }
+    }
+    // The tile needs the LDS stage (FP32 sums in worker order) unless every
+    // element of it is eligible.  With one element group per block the
+    // tile's words are every wavefront's own; otherwise every wavefront reads
+    // them all, so the decision is block-uniform either way.
+    bool tile_all = full && mine == ~0ull;
+    if (a.eg > 1 && full) {
+      uint64_t acc = ~0ull;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int k = lane + 64 * r;
+        if (k < tile / 64) acc &= tmask[k];
+      }
+      tile_all = __all(acc == ~0ull);
+    }
+    const bool mine_all = full && mine == ~0ull;
+    const bool stage_tile = stage_on && (a.sums == kSumsAll || !tile_all);
+    if (active && wg == 0) {
+      if (mine_all) {
+        ne += (uint64_t)(64 * NW);
+      } else {
+#pragma unroll
+        for (int k = 0; k < NW; ++k) ne += __popcll(mw[k]);
+      }
+    }
+
+    if (active) {
+      const int nwv = (cnt + 63) / 64;
+#pragma unroll
+      for (int j = 0; j < WPW; ++j) {
+        const int w = wg + j * a.wg;
+        if (j > 0 && w >= a.W) break;
+        float x[NW];
+        if (j == 0) {
+#pragma unroll
+          for (int k = 0; k < NW; ++k) x[k] = x0[k];
+        } else {
           const float* row = g + (int64_t)w * a.wstride + base + e0 + lane;
-          float x[NW];
+          if (full) {
 #pragma unroll
-          for (int k = 0; k < NW; ++k) x[k] = __builtin_nontemporal_load(row + 64 * k);
-          double s1 = 0.0, s2 = 0.0;
-          uint64_t bb[NW];
+            for (int k = 0; k < NW; ++k) x[k] = __builtin_nontemporal_load(row + 64 * k);
+          } else {
+#pragma unroll
+            for (int k = 0; k < NW; ++k)
+              x[k] = (64 * k + lane < cnt) ? __builtin_nontemporal_load(row + 64 * k) : 0.0f;
+          }
+        }
+        double s1 = 0.0, s2 = 0.0;
+        uint64_t bb[NW];
+        if (mine_all) {
 #pragma unroll
           for (int k = 0; k < NW; ++k) {
             if (PACK) bb[k] = __ballot(x[k] > 0.0f);
@@ -178,37 +260,7 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
             s2 = __builtin_fma(d, d, s2);
             s1 += __builtin_fabs(d);
           }
-          if (PACK) {
-            uint32_t wlo, whi;
-            lanes_from_ballots<NW>(bb, wlo, whi);
-            if (lane < NW) bits[(int64_t)w * a.bstride + wrd0 + lane] = ((uint64_t)whi << 32) | wlo;
-          }
-          if (__ballot(!finite64(s2))) {
-#pragma unroll
-            for (int k = 0; k < NW; ++k) nonf[j] += __popcll(__ballot(!finite32(x[k])));
-          }
-          sabs[j] += s1;
-          ssq[j] += s2;
-        }
-        if (wg == 0) ne += (uint64_t)T;
-      }
-    } else {
-      if (active) {
-        const uint64_t* mrow = mask + wrd0;
-        uint64_t mw[NW];
-#pragma unroll
-        for (int k = 0; k < NW; ++k) mw[k] = 64 * k < cnt ? (mrow[k] & low_bits(cnt - 64 * k)) : 0ull;
-        const int nwv = (cnt + 63) / 64;
-#pragma unroll
-        for (int j = 0; j < WPW; ++j) {
-          const int w = wg + j * a.wg;
-          if (j > 0 && w >= a.W) break;
-          const float* row = g + (int64_t)w * a.wstride + base + e0 + lane;
-          float x[NW];
-#pragma unroll
-          for (int k = 0; k < NW; ++k) x[k] = (64 * k + lane < cnt) ? __builtin_nontemporal_load(row + 64 * k) : 0.0f;
-          double s1 = 0.0, s2 = 0.0;
-          uint64_t bb[NW];
+        } else {
 #pragma unroll
           for (int k = 0; k < NW; ++k) {
             if (PACK) bb[k] = __ballot(x[k] > 0.0f) & mw[k];
@@ -216,49 +268,103 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
             s2 = __builtin_fma(d, d, s2);
             s1 += ((mw[k] >> lane) & 1ull) ? __builtin_fabs(d) : 0.0;
           }
-          if (PACK) {
-            uint32_t wlo, whi;
-            lanes_from_ballots<NW>(bb, wlo, whi);
-            if (lane < nwv) bits[(int64_t)w * a.bstride + wrd0 + lane] = ((uint64_t)whi << 32) | wlo;
-          }
-          if (__ballot(!finite64(s2))) {
-#pragma unroll
-            for (int k = 0; k < NW; ++k) nonf[j] += __popcll(__ballot(!finite32(x[k])));
-          }
-          sabs[j] += s1;
-          ssq[j] += s2;
-          if (stage_on) {
-            float* st = stage + (int64_t)w * tile + eg * T + lane;
-#pragma unroll
-            for (int k = 0; k < NW; ++k) st[64 * k] = x[k];
-          }
         }
-        if (wg == 0) {
+        if (PACK) {
+          uint32_t wlo, whi;
+          lanes_from_ballots<NW>(bb, wlo, whi);
+          // word k of this group and tile -> chunk word ((t - tb) * EG + eg) * NW + k
+          if (lane < nwv) wbuf[w * cw + ((t - tb) * a.eg + eg) * NW + lane] = ((uint64_t)whi << 32) | wlo;
+        }
+        if (__ballot(!finite64(s2))) {
 #pragma unroll
-          for (int k = 0; k < NW; ++k) ne += __popcll(mw[k]);
+          for (int k = 0; k < NW; ++k) nonf[j] += __popcll(__ballot(!finite32(x[k])));
+        }
+        sabs[j] += s1;
+        ssq[j] += s2;
+        if (stage_tile) {
+          float* st = stage + (int64_t)w * tile + eg * T + lane;
+#pragma unroll
+          for (int k = 0; k < NW; ++k) st[64 * k] = x[k];
         }
       }
-      if (stage_on) {
-        __syncthreads();
-        // Workers added in order w = 0..W-1 at each staged position.
-        const int lim = (int)((nbe - t0) < tile ? (nbe - t0) : tile);
-        for (int e = threadIdx.x; e < lim; e += kThreads1) {
-          const int64_t i = base + t0 + e;
-          const bool routed = !((mask[i >> 6] >> (i & 63)) & 1ull);
-          if (a.sums == kSumsAll || routed) {
-            float s = stage[e];
-            for (int w = 1; w < a.W; ++w) s = s + stage[w * tile + e];
-            if (a.mean) s = s / (float)a.W;
-            out[i] = s;
-          }
+    }
+    if (stage_tile) {
+      __syncthreads();
+      // Workers added in order w = 0..W-1 at each staged position; wavefront
+      // v takes words v, v + 16, ... of the tile.
+      const int lim = (int)((nbe - t0) < tile ? (nbe - t0) : tile);
+      const int nwt = (lim + 63) / 64;
+      for (int kw = v; kw < nwt; kw += kWaves) {
+        const int e = kw * 64 + lane;
+        const uint64_t pick = (a.sums == kSumsAll ? ~0ull : ~tmask[kw]) & low_bits(lim - kw * 64);
+        if ((pick >> lane) & 1ull) {
+          float s = stage[e];
+          for (int w = 1; w < a.W; ++w) s = s + stage[w * tile + e];
+          if (a.mean) s = s / (float)a.W;
+          out[base + t0 + e] = s;
         }
-        __syncthreads();
       }
+      __syncthreads();
     }
   }
 
-  // Block partials: wavefront sums, then element groups in order.
+  const int64_t slot = (int64_t)b * a.slots + (c % kMaxSlots);
+  const bool first = c < kMaxSlots;
+  if (a.eg == 1) {
+    // One element group: each worker lives in exactly one wavefront, which
+    // stores its own rows of sign words and its own partials, so the block
+    // ends without a barrier.
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    const int64_t e_beg = tb * tile;
+    const int64_t e_end = (te * tile < nbe) ? te * tile : nbe;
+    const int valid = te > tb ? (int)((e_end - e_beg + 63) / 64) : 0;
+    const int64_t gw0 = (base + e_beg) / 64;
+#pragma unroll
+    for (int j = 0; j < WPW; ++j) {
+      const int w = wg + j * a.wg;
+      if (w >= a.W) break;
+      if (PACK)
+        for (int o = lane; o < valid; o += 64) bits[(int64_t)w * a.bstride + gw0 + o] = wbuf[w * cw + o];
+      const double s1 = wave_sum(sabs[j]);
+      const double s2 = wave_sum(ssq[j]);
+      if (lane == 0) {
+        Partial p;
+        p.sabs = s1;
+        p.ssq = s2;
+        p.nonfinite = nonf[j];
+        if (!first) {
+          const Partial o = part[slot * a.W + w];
+          p.sabs = o.sabs + p.sabs;
+          p.ssq = o.ssq + p.ssq;
+          p.nonfinite = o.nonfinite + p.nonfinite;
+        }
+        part[slot * a.W + w] = p;
+      }
+    }
+    if (wg == 0 && lane == 0) part_ne[slot] = first ? ne : part_ne[slot] + ne;
+    return;
+  }
+
   __syncthreads();
+  // The chunk's sign words, row by row, as coalesced stores.
+  if (PACK && te > tb) {
+    const int64_t e_beg = tb * tile;
+    const int64_t e_end = (te * tile < nbe) ? te * tile : nbe;
+    const int valid = (int)((e_end - e_beg + 63) / 64);
+    const int64_t gw0 = (base + e_beg) / 64;
+    for (int i = threadIdx.x; i < a.W * valid; i += kThreads1) {
+      const int w = i / valid;
+      const int o = i - w * valid;
+      bits[(int64_t)w * a.bstride + gw0 + o] = wbuf[w * cw + o];
+    }
+    __syncthreads();
+  }
+
+  // Block partials: wavefront sums, then element groups in order.  Chunk c
+  // of bucket b goes to slot c % kMaxSlots; chunks beyond the first
+  // kMaxSlots add to it, always in launch order.
   Partial* red = reinterpret_cast<Partial*>(smem);
   uint64_t* red_ne = reinterpret_cast<uint64_t*>(red + a.eg * a.W);
   if (active) {
@@ -279,21 +385,26 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
     if (wg == 0 && lane == 0) red_ne[eg] = ne;
   }
   __syncthreads();
-  const int64_t slot = (int64_t)b * a.bpb + blockIdx.x;
   for (int w = threadIdx.x; w < a.W; w += kThreads1) {
     Partial p = red[w];
     for (int e = 1; e < a.eg; ++e) {
-      const Partial q = red[e * a.W + w];
-      p.sabs += q.sabs;
-      p.ssq += q.ssq;
-      p.nonfinite += q.nonfinite;
+      const Partial q2 = red[e * a.W + w];
+      p.sabs += q2.sabs;
+      p.ssq += q2.ssq;
+      p.nonfinite += q2.nonfinite;
+    }
+    if (!first) {
+      const Partial o = part[slot * a.W + w];
+      p.sabs = o.sabs + p.sabs;
+      p.ssq = o.ssq + p.ssq;
+      p.nonfinite = o.nonfinite + p.nonfinite;
     }
     part[slot * a.W + w] = p;
   }
   if (threadIdx.x == 0) {
     uint64_t s = 0;
     for (int e = 0; e < a.eg; ++e) s += red_ne[e];
-    part_ne[slot] = s;
+    part_ne[slot] = first ? s : part_ne[slot] + s;
   }
 }
 
@@ -306,11 +417,15 @@ __global__ __launch_bounds__(256) void k_decide(DecideArgs a) {
   const int b = blockIdx.x;
   const int v = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wavefront index, uniform
   const int lane = threadIdx.x & 63;
-  const Partial* P = a.part + (int64_t)b * a.bpb * a.W;
+  const Partial* P = a.part + (int64_t)b * a.slots * a.W;
+  // slots written for this bucket: one per chunk, at most kMaxSlots
+  const int64_t nbe = bucket_len(a.n_total, a.bucket_n, b);
+  const int64_t chunks = ((nbe + a.tile - 1) / a.tile + a.G - 1) / a.G;
+  const int used = (int)(chunks < a.slots ? chunks : a.slots);
   for (int w = v; w < a.W; w += 4) {
     double s1 = 0.0, s2 = 0.0;
     uint64_t nf = 0;
-    for (int k = lane; k < a.bpb; k += 64) {
+    for (int k = lane; k < used; k += 64) {
       const Partial p = P[(int64_t)k * a.W + w];
       s1 += p.sabs;
       s2 += p.ssq;
@@ -327,7 +442,7 @@ __global__ __launch_bounds__(256) void k_decide(DecideArgs a) {
   }
   if (v == 0) {
     uint64_t s = 0;
-    for (int k = lane; k < a.bpb; k += 64) s += a.part_ne[(int64_t)b * a.bpb + k];
+    for (int k = lane; k < used; k += 64) s += a.part_ne[(int64_t)b * a.slots + k];
     s = wave_sum_u64(s);
     if (lane == 0) ne_s = s;
   }
@@ -347,18 +462,40 @@ __global__ __launch_bounds__(256) void k_decide(DecideArgs a) {
   __syncthreads();
   if (threadIdx.x == 0) {
     nf_route_decision d;
-    const int64_t n = bucket_len(a.n_total, a.bucket_n, b);
-    decide_from(st, a.W, n, (int64_t)ne_s, a.pol, kfin, med_s, &d);
+    decide_from(st, a.W, nbe, (int64_t)ne_s, a.pol, kfin, med_s, &d);
     a.dec[b] = d;
   }
 }
 
 // ------------------------------------------------------------------ pass 2
+//
+// A wavefront takes 64 consecutive bitmap words (4096 elements) per step.
+// Counting (route L): lane l loads word k0 + l of every worker row (one
+// 512-byte coalesced load per worker) and adds the W words into a
+// bit-sliced counter, planes P[0..B) with bit j of P[b] = bit b of the count
+// of element 64(k0+l) + j.  Eight words at a time go through a carry-save
+// tree of full adders (Harley-Seal), the rest ripple in.  The planes are then
+// transposed through LDS so that lane j decodes element j of each word: its
+// count selects fl32(scale * q[c]) from an LDS table, and every store is a
+// coalesced 64- or 256-byte row.  Fallback (route F) and the standalone FP32
+// reduction add the workers in order at the selected positions instead.
+constexpr int kRec = 12;  // dwords per (word, half) record: 8 planes, mask half, pad
+
+struct FullAdd {
+  uint64_t sum, carry;
+};
+
+__device__ __forceinline__ FullAdd full_add(uint64_t a, uint64_t b, uint64_t c) {
+  const uint64_t t = a ^ b;
+  return FullAdd{t ^ c, (a & b) | (c & t)};
+}
+
 __global__ __launch_bounds__(kThreads2) void k_pass2(
     const uint64_t* __restrict__ bits, const float* __restrict__ g, const uint64_t* __restrict__ mask,
     const nf_route_decision* __restrict__ dec, const float* __restrict__ scale_p,
     uint8_t* __restrict__ counts, float* __restrict__ out, Pass2Args a) {
   __shared__ float tab[256];
+  __shared__ __align__(16) uint32_t rec[4][64 * 2 * kRec];
   const int b = blockIdx.y;
   const int64_t base = (int64_t)b * a.bucket_n;
   const int64_t nbe = bucket_len(a.n_total, a.bucket_n, b);
@@ -386,64 +523,129 @@ __global__ __launch_bounds__(kThreads2) void k_pass2(
   const int64_t wbase = base / 64;
   const int v = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wavefront index, uniform
   const int lane = threadIdx.x & 63;
-  constexpr int K = kWordsPerWave2;
-  for (int64_t ch = (int64_t)blockIdx.x * 4 + v; ch * K < nwords; ch += (int64_t)a.bpb2 * 4) {
-    const int64_t k0 = ch * K;
-    const int nk = (int)((nwords - k0) < K ? (nwords - k0) : K);
+  const int half = lane >> 5;
+  const int sh = lane & 31;
+  int nplanes = 1;
+  while ((1 << nplanes) <= a.W) ++nplanes;  // counts 0..W need nplanes bits
+  uint32_t* my = rec[v];
+
+  for (int64_t ch = (int64_t)blockIdx.x * 4 + v; ch * 64 < nwords; ch += (int64_t)a.bpb2 * 4) {
+    const int64_t k0 = ch * 64;
+    const int nk = (int)((nwords - k0) < 64 ? (nwords - k0) : 64);
     if (op == kOpCountDecode) {
-      uint32_t c[K];
+      // ---- bit-sliced counts, lane = word k0 + lane
+      const bool valid = lane < nk;
+      const uint64_t* col = bits + wbase + k0 + lane;
+      uint64_t P[8];
 #pragma unroll
-      for (int k = 0; k < K; ++k) c[k] = 0;
-      for (int w = 0; w < a.W; ++w) {
-        const uint64_t* brow = bits + (int64_t)w * a.bstride + wbase + k0;
-        if (nk == K) {
+      for (int q = 0; q < 8; ++q) P[q] = 0;
+      int w = 0;
+      for (; w + 8 <= a.W; w += 8) {
+        uint64_t x[8];
 #pragma unroll
-          for (int k = 0; k < K; ++k) c[k] = add_lane_bit(c[k], brow[k]);
-        } else {
+        for (int i = 0; i < 8; ++i) x[i] = valid ? col[(int64_t)(w + i) * a.bstride] : 0ull;
+        FullAdd f0 = full_add(P[0], x[0], x[1]);
+        FullAdd f1 = full_add(f0.sum, x[2], x[3]);
+        FullAdd f2 = full_add(P[1], f0.carry, f1.carry);
+        FullAdd f3 = full_add(f1.sum, x[4], x[5]);
+        FullAdd f4 = full_add(f3.sum, x[6], x[7]);
+        FullAdd f5 = full_add(f2.sum, f3.carry, f4.carry);
+        FullAdd f6 = full_add(P[2], f2.carry, f5.carry);
+        P[0] = f4.sum;
+        P[1] = f5.sum;
+        P[2] = f6.sum;
+        uint64_t c = f6.carry;  // weight 8
 #pragma unroll
-          for (int k = 0; k < K; ++k)
-            if (k < nk) c[k] = add_lane_bit(c[k], brow[k]);
-        }
-      }
-#pragma unroll
-      for (int k = 0; k < K; ++k) {
-        if (k >= nk) break;
-        const int64_t i = (k0 + k) * 64 + lane;
-        if (i < nbe) {
-          if (counts) counts[base + i] = (uint8_t)c[k];
-          if (out && ((mask[wbase + k0 + k] >> lane) & 1ull)) out[base + i] = tab[c[k]];
-        }
-      }
-    } else {
-      float s[K];
-      uint64_t selw[K];
-#pragma unroll
-      for (int k = 0; k < K; ++k) {
-        uint64_t m = 0;
-        if (k < nk) {
-          const uint64_t mw = mask ? mask[wbase + k0 + k] : ~0ull;
-          m = sel == NF_SEL_ALL ? ~0ull : (sel == NF_SEL_ELIGIBLE ? mw : ~mw);
-          m &= low_bits(nbe - (k0 + k) * 64);
-        }
-        selw[k] = m;
-        s[k] = 0.0f;
-      }
-      for (int w = 0; w < a.W; ++w) {
-        const float* row = g + (int64_t)w * a.wstride + base + k0 * 64 + lane;
-#pragma unroll
-        for (int k = 0; k < K; ++k) {
-          if ((selw[k] >> lane) & 1ull) {
-            const float x = __builtin_nontemporal_load(row + 64 * k);
-            s[k] = w == 0 ? x : s[k] + x;
+        for (int q = 3; q < 8; ++q) {
+          if (q < nplanes) {
+            const uint64_t t = P[q] & c;
+            P[q] ^= c;
+            c = t;
           }
         }
       }
+      for (; w < a.W; ++w) {
+        uint64_t c = valid ? col[(int64_t)w * a.bstride] : 0ull;
 #pragma unroll
-      for (int k = 0; k < K; ++k) {
-        if ((selw[k] >> lane) & 1ull) {
-          float y = s[k];
-          if (a.mean) y = y / (float)a.W;
-          out[base + (k0 + k) * 64 + lane] = y;
+        for (int q = 0; q < 8; ++q) {
+          if (q < nplanes) {
+            const uint64_t t = P[q] & c;
+            P[q] ^= c;
+            c = t;
+          }
+        }
+      }
+      const uint64_t mw = (valid && mask) ? mask[wbase + k0 + lane] : 0ull;
+      // ---- transpose through LDS: record (word, half) holds the planes' and
+      // the mask's 32-bit halves
+      uint4* r0 = reinterpret_cast<uint4*>(my + (lane * 2) * kRec);
+      uint4* r1 = reinterpret_cast<uint4*>(my + (lane * 2 + 1) * kRec);
+      r0[0] = make_uint4((uint32_t)P[0], (uint32_t)P[1], (uint32_t)P[2], (uint32_t)P[3]);
+      r0[1] = make_uint4((uint32_t)P[4], (uint32_t)P[5], (uint32_t)P[6], (uint32_t)P[7]);
+      r0[2] = make_uint4((uint32_t)mw, 0u, 0u, 0u);
+      r1[0] = make_uint4((uint32_t)(P[0] >> 32), (uint32_t)(P[1] >> 32), (uint32_t)(P[2] >> 32),
+                         (uint32_t)(P[3] >> 32));
+      r1[1] = make_uint4((uint32_t)(P[4] >> 32), (uint32_t)(P[5] >> 32), (uint32_t)(P[6] >> 32),
+                         (uint32_t)(P[7] >> 32));
+      r1[2] = make_uint4((uint32_t)(mw >> 32), 0u, 0u, 0u);
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      // ---- decode, lane = element j of word k0 + kk
+      for (int kk = 0; kk < nk; ++kk) {
+        const uint4* r = reinterpret_cast<const uint4*>(my + (kk * 2 + half) * kRec);
+        const uint4 p03 = r[0];
+        const uint4 p47 = r[1];
+        const uint32_t mh = r[2].x;
+        uint32_t c = ((p03.x >> sh) & 1u) | (((p03.y >> sh) & 1u) << 1) | (((p03.z >> sh) & 1u) << 2) |
+                     (((p03.w >> sh) & 1u) << 3);
+        if (nplanes > 4)
+          c |= (((p47.x >> sh) & 1u) << 4) | (((p47.y >> sh) & 1u) << 5) | (((p47.z >> sh) & 1u) << 6) |
+               (((p47.w >> sh) & 1u) << 7);
+        const int64_t i = (k0 + kk) * 64 + lane;
+        if (i < nbe) {
+          if (counts) counts[base + i] = (uint8_t)c;
+          if (out && ((mh >> sh) & 1u)) out[base + i] = tab[c];
+        }
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    } else {
+      constexpr int K = 16;
+      for (int s0 = 0; s0 < nk; s0 += K) {
+        const int64_t kb = k0 + s0;
+        const int nks = (nk - s0) < K ? (nk - s0) : K;
+        float sacc[K];
+        uint64_t selw[K];
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+          uint64_t m = 0;
+          if (k < nks) {
+            const uint64_t mw = mask ? mask[wbase + kb + k] : ~0ull;
+            m = sel == NF_SEL_ALL ? ~0ull : (sel == NF_SEL_ELIGIBLE ? mw : ~mw);
+            m &= low_bits(nbe - (kb + k) * 64);
+          }
+          selw[k] = m;
+          sacc[k] = 0.0f;
+        }
+        for (int w = 0; w < a.W; ++w) {
+          const float* row = g + (int64_t)w * a.wstride + base + kb * 64 + lane;
+#pragma unroll
+          for (int k = 0; k < K; ++k) {
+            if ((selw[k] >> lane) & 1ull) {
+              const float x = __builtin_nontemporal_load(row + 64 * k);
+              sacc[k] = w == 0 ? x : sacc[k] + x;
+            }
+          }
+        }
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+          if ((selw[k] >> lane) & 1ull) {
+            float y = sacc[k];
+            if (a.mean) y = y / (float)a.W;
+            out[base + (kb + k) * 64 + lane] = y;
+          }
         }
       }
     }
@@ -454,20 +656,41 @@ __global__ __launch_bounds__(kThreads2) void k_pass2(
 
 template <bool PACK>
 static hipError_t pass1_dispatch(const Geometry& geo, const Pass1Args& a, hipStream_t s) {
-  const dim3 grid((unsigned)geo.bpb, (unsigned)geo.nb);
   const dim3 block(kThreads1);
-  size_t red = (size_t)geo.eg * geo.W * sizeof(Partial) + (size_t)geo.eg * sizeof(uint64_t);
-  size_t smem = a.sums != kSumsNone ? (size_t)geo.W * geo.tile * sizeof(float) : 0;
+  const int cw = geo.G * geo.eg * pass1_words(geo.wpw);
+  size_t smem = PACK ? (size_t)geo.W * cw * sizeof(uint64_t) : 0;
+  if (a.sums != kSumsNone) smem += (size_t)geo.W * geo.tile * sizeof(float);
+  const size_t red = (size_t)geo.eg * geo.W * sizeof(Partial) + (size_t)geo.eg * sizeof(uint64_t);
   if (smem < red) smem = red;
-  switch (geo.wpw) {
-    case 1: hipLaunchKernelGGL((k_pass1<1, PACK>), grid, block, smem, s, a.g, a.mask, a.bits, a.out, a.part, a.part_ne, a); break;
-    case 2: hipLaunchKernelGGL((k_pass1<2, PACK>), grid, block, smem, s, a.g, a.mask, a.bits, a.out, a.part, a.part_ne, a); break;
-    case 4: hipLaunchKernelGGL((k_pass1<4, PACK>), grid, block, smem, s, a.g, a.mask, a.bits, a.out, a.part, a.part_ne, a); break;
-    case 8: hipLaunchKernelGGL((k_pass1<8, PACK>), grid, block, smem, s, a.g, a.mask, a.bits, a.out, a.part, a.part_ne, a); break;
-    case 16: hipLaunchKernelGGL((k_pass1<16, PACK>), grid, block, smem, s, a.g, a.mask, a.bits, a.out, a.part, a.part_ne, a); break;
-    default: return hipErrorInvalidValue;
+  if (smem > 65536) {
+    // Above 64 KiB of dynamic LDS the kernel must opt in (gfx950 has 160 KiB per CU).
+    hipError_t e = hipSuccess;
+    switch (geo.wpw) {
+      case 1: e = hipFuncSetAttribute((const void*)k_pass1<1, PACK>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem); break;
+      case 2: e = hipFuncSetAttribute((const void*)k_pass1<2, PACK>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem); break;
+      case 4: e = hipFuncSetAttribute((const void*)k_pass1<4, PACK>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem); break;
+      case 8: e = hipFuncSetAttribute((const void*)k_pass1<8, PACK>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem); break;
+      case 16: e = hipFuncSetAttribute((const void*)k_pass1<16, PACK>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem); break;
+      default: return hipErrorInvalidValue;
+    }
+    if (e != hipSuccess) return e;
   }
-  return hipGetLastError();
+  // One launch per kEpochBlocks chunks (see the geometry notes).
+  for (int64_t q0 = 0; q0 < geo.total_chunks; q0 += kEpochBlocks) {
+    const int64_t left = geo.total_chunks - q0;
+    const dim3 grid((unsigned)(left < kEpochBlocks ? left : kEpochBlocks));
+    switch (geo.wpw) {
+      case 1: hipLaunchKernelGGL((k_pass1<1, PACK>), grid, block, smem, s, a.g, a.mask, a.bits, a.out, a.part, a.part_ne, a, q0); break;
+      case 2: hipLaunchKernelGGL((k_pass1<2, PACK>), grid, block, smem, s, a.g, a.mask, a.bits, a.out, a.part, a.part_ne, a, q0); break;
+      case 4: hipLaunchKernelGGL((k_pass1<4, PACK>), grid, block, smem, s, a.g, a.mask, a.bits, a.out, a.part, a.part_ne, a, q0); break;
+      case 8: hipLaunchKernelGGL((k_pass1<8, PACK>), grid, block, smem, s, a.g, a.mask, a.bits, a.out, a.part, a.part_ne, a, q0); break;
+      case 16: hipLaunchKernelGGL((k_pass1<16, PACK>), grid, block, smem, s, a.g, a.mask, a.bits, a.out, a.part, a.part_ne, a, q0); break;
+      default: return hipErrorInvalidValue;
+    }
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 hipError_t launch_pass1(const Geometry& geo, const Pass1Args& a, hipStream_t s) {
