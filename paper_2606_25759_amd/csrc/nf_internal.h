@@ -31,9 +31,19 @@ namespace nf {
 constexpr int kWaves = 16;
 constexpr int kThreads1 = kWaves * 64;
 constexpr int kStageFloats = 16384;      // 64 KiB of LDS
-constexpr int kBitsWords = 4096;         // 32 KiB of LDS for a chunk's sign words
-constexpr int kMaxSlots = 512;           // partial-statistics slots per bucket
-constexpr int kEpochBlocks = 512;        // chunks per pass-1 launch
+#ifndef NF_BITS_WORDS
+#define NF_BITS_WORDS 4096
+#endif
+#ifndef NF_EPOCH_BLOCKS
+#define NF_EPOCH_BLOCKS 512
+#endif
+#ifndef NF_MAX_G
+#define NF_MAX_G 32
+#endif
+constexpr int kBitsWords = NF_BITS_WORDS;      // LDS words for a chunk's sign words (32 KiB)
+constexpr int kMaxSlots = 512;                 // partial-statistics slots per bucket
+constexpr int kEpochBlocks = NF_EPOCH_BLOCKS;  // chunks per pass-1 launch
+constexpr int kMaxG = NF_MAX_G;                // tiles per chunk at most
 
 // Pass 2: a wavefront takes 64 consecutive bitmap words (4096 elements) per
 // step, four wavefronts per block.
@@ -72,7 +82,7 @@ inline Geometry make_geometry(int W, int64_t n_total, int64_t bucket_n) {
   // A chunk's sign words, W * G * EG * (T / 64), fit kBitsWords.
   int per_tile = W * g.eg * (g.T / 64);
   g.G = kBitsWords / per_tile;
-  if (g.G > 32) g.G = 32;
+  if (g.G > kMaxG) g.G = kMaxG;
   if (g.G < 1) g.G = 1;
   g.n_total = n_total;
   g.bucket_n = bucket_n;

@@ -11,6 +11,8 @@
 //
 // The path is bound by HBM bandwidth, so there is no MFMA: every step is a
 // streaming scan with a handful of VALU operations per element and worker.
+#include <hip/hip_ext.h>
+
 #include "nf_internal.h"
 
 namespace nf {
@@ -115,7 +117,7 @@ __device__ __forceinline__ int64_t bucket_len(int64_t n_total, int64_t bucket_n,
 // of "g > 0" over the wavefront is exactly bitmap word k.  A block takes one
 // chunk (G tiles of one bucket); launch q0 takes chunks q0 .. q0 + grid - 1.
 template <int WPW, bool PACK>
-__global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <= 2 ? 8 : 4))) void k_pass1(
+__global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <= 2 ? 8 : 4, WPW <= 2 ? 8 : 4))) void k_pass1(
     const float* __restrict__ g, const uint64_t* __restrict__ mask, uint64_t* __restrict__ bits,
     float* __restrict__ out, Partial* __restrict__ part, uint64_t* __restrict__ part_ne, Pass1Args a,
     int64_t q0) {
@@ -162,7 +164,116 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
   }
   uint64_t ne = 0;
 
-  for (int64_t t = tb; t < te; ++t) {
+  // Fast chunks: every tile full and every element eligible, and no FP32
+  // sums over all elements.  Then the loop needs no mask, bound or stage
+  // work, and the next tile is in flight while one is examined (two
+  // register buffers, tiles taken in pairs).  The per-tile instruction
+  // count is what limits this loop: the ballots are the bitmap words as
+  // they are, and addresses advance by constants.  Every issue makes the
+  // same number of loads (past the chunk's end, in an idle wavefront or for
+  // a missing worker it reads the bucket's first tile), so that the
+  // compiler's wait counts leave the next tile in flight.
+  constexpr int NX = WPW * NW;
+  const bool all_full = te * tile <= nbe;
+  float xa[NX], xb[NX];
+  // Row pointers of this wavefront's workers at its element group, and the
+  // bucket's first tile for loads that are not needed.
+  const float* rp[WPW];
+#pragma unroll
+  for (int j = 0; j < WPW; ++j) {
+    const int w = wg + j * a.wg;
+    rp[j] = g + (int64_t)(w < a.W ? w : wg) * a.wstride + base + (int64_t)eg * T + lane;
+  }
+  const float* dp = g + (int64_t)wg * a.wstride + base + lane;
+  auto issue_words = [&](int64_t tt, float (&X)[NX]) {
+    const bool ok = active && tt < te;
+    const int64_t o = tt * tile;
+#pragma unroll
+    for (int j = 0; j < WPW; ++j) {
+      const float* row = (ok && (j == 0 || wg + j * a.wg < a.W)) ? rp[j] + o : dp;
+#pragma unroll
+      for (int k = 0; k < NW; ++k) X[j * NW + k] = __builtin_nontemporal_load(row + 64 * k);
+    }
+  };
+  // Loads whose values are not needed: waiting for them where they die
+  // keeps the compiler from waiting for them later, with the next tile in
+  // flight.
+  auto consume = [&](const float (&X)[NX]) {
+#pragma unroll
+    for (int k = 0; k < NX; ++k) asm volatile("" ::"v"(X[k]));
+  };
+  // The mask load goes out first, unpredicated, so that only it is waited
+  // for before the barrier.
+  bool chunk_fast;
+  {
+    const int64_t wbeg = (base + tb * tile) / 64;
+    const int nwc = all_full ? (int)((te - tb) * (tile / 64)) : 0;
+    uint64_t m0 = ~0ull;
+    if (all_full) {
+      m0 = mask[wbeg + ((int)threadIdx.x < nwc ? (int)threadIdx.x : nwc - 1)];
+      issue_words(tb, xa);
+    }
+    int some_not = !all_full || ((int)threadIdx.x < nwc && m0 != ~0ull);
+    for (int i = threadIdx.x + kThreads1; i < nwc; i += kThreads1) some_not |= mask[wbeg + i] != ~0ull;
+    chunk_fast = !__syncthreads_or(some_not) && a.sums != kSumsAll;
+    if (all_full && !chunk_fast) consume(xa);
+  }
+  auto fast_body = [&](int64_t t, float (&X)[NX], float (&Xn)[NX]) {
+    issue_words(t + 1, Xn);
+    if (!active) {
+      consume(X);
+      return;
+    }
+    const int ti = (int)(t - tb);
+#pragma unroll
+    for (int j = 0; j < WPW; ++j) {
+      const int w = wg + j * a.wg;
+      const float* x = &X[j * NW];
+      if (j > 0 && w >= a.W) {
+#pragma unroll
+        for (int k = 0; k < NW; ++k) asm volatile("" ::"v"(x[k]));
+        continue;
+      }
+      double s1 = 0.0, s2 = 0.0;
+      uint64_t bb[NW];
+#pragma unroll
+      for (int k = 0; k < NW; ++k) {
+        if (PACK) bb[k] = __ballot(x[k] > 0.0f);
+        const double d = (double)x[k];
+        s2 = __builtin_fma(d, d, s2);
+        s1 += __builtin_fabs(d);
+      }
+      if (PACK) {
+        uint32_t wlo, whi;
+        lanes_from_ballots<NW>(bb, wlo, whi);
+        if (lane < NW) wbuf[w * cw + (ti * a.eg + eg) * NW + lane] = ((uint64_t)whi << 32) | wlo;
+      }
+      if (__ballot(!finite64(s2))) {
+#pragma unroll
+        for (int k = 0; k < NW; ++k) nonf[j] += __popcll(__ballot(!finite32(x[k])));
+      }
+      sabs[j] += s1;
+      ssq[j] += s2;
+    }
+  };
+  if (chunk_fast) {
+    if (active && wg == 0) ne = (uint64_t)(te - tb) * (uint64_t)T;
+    // Pairs of tiles in a loop with a single exit, then the odd tile: the
+    // loop head is reached only with xa in flight.
+    int64_t t = tb;
+    for (int64_t p = (te - tb) >> 1; p > 0; --p, t += 2) {
+      fast_body(t, xa, xb);
+      fast_body(t + 1, xb, xa);
+    }
+    if ((te - tb) & 1) {
+      fast_body(t, xa, xb);
+      consume(xb);
+    } else {
+      consume(xa);
+    }
+  }
+
+  for (int64_t t = chunk_fast ? te : tb; t < te; ++t) {
     const int64_t t0 = t * tile;
     const bool full = t0 + tile <= nbe;  // block-uniform
     const int64_t e0 = t0 + (int64_t)eg * T;
@@ -675,16 +786,22 @@ static hipError_t pass1_dispatch(const Geometry& geo, const Pass1Args& a, hipStr
     }
     if (e != hipSuccess) return e;
   }
-  // One launch per kEpochBlocks chunks (see the geometry notes).
+  // One launch per kEpochBlocks chunks (see the geometry notes).  The first
+  // launch is ordered after earlier work on the stream; later ones may
+  // start while the one before drains, which is safe when no two chunks of
+  // a bucket share a partial slot (every chunk then writes only its own
+  // slot and sign words).  The next ordered launch (decide) waits for all.
+  const uint32_t overlap = geo.chunks_full <= kMaxSlots ? hipExtAnyOrderLaunch : 0u;
   for (int64_t q0 = 0; q0 < geo.total_chunks; q0 += kEpochBlocks) {
     const int64_t left = geo.total_chunks - q0;
     const dim3 grid((unsigned)(left < kEpochBlocks ? left : kEpochBlocks));
+    const uint32_t fl = q0 > 0 ? overlap : 0u;
     switch (geo.wpw) {
-      case 1: hipLaunchKernelGGL((k_pass1<1, PACK>), grid, block, smem, s, a.g, a.mask, a.bits, a.out, a.part, a.part_ne, a, q0); break;
-      case 2: hipLaunchKernelGGL((k_pass1<2, PACK>), grid, block, smem, s, a.g, a.mask, a.bits, a.out, a.part, a.part_ne, a, q0); break;
-      case 4: hipLaunchKernelGGL((k_pass1<4, PACK>), grid, block, smem, s, a.g, a.mask, a.bits, a.out, a.part, a.part_ne, a, q0); break;
-      case 8: hipLaunchKernelGGL((k_pass1<8, PACK>), grid, block, smem, s, a.g, a.mask, a.bits, a.out, a.part, a.part_ne, a, q0); break;
-      case 16: hipLaunchKernelGGL((k_pass1<16, PACK>), grid, block, smem, s, a.g, a.mask, a.bits, a.out, a.part, a.part_ne, a, q0); break;
+      case 1: hipExtLaunchKernelGGL((k_pass1<1, PACK>), grid, block, smem, s, nullptr, nullptr, fl, a.g, a.mask, a.bits, a.out, a.part, a.part_ne, a, q0); break;
+      case 2: hipExtLaunchKernelGGL((k_pass1<2, PACK>), grid, block, smem, s, nullptr, nullptr, fl, a.g, a.mask, a.bits, a.out, a.part, a.part_ne, a, q0); break;
+      case 4: hipExtLaunchKernelGGL((k_pass1<4, PACK>), grid, block, smem, s, nullptr, nullptr, fl, a.g, a.mask, a.bits, a.out, a.part, a.part_ne, a, q0); break;
+      case 8: hipExtLaunchKernelGGL((k_pass1<8, PACK>), grid, block, smem, s, nullptr, nullptr, fl, a.g, a.mask, a.bits, a.out, a.part, a.part_ne, a, q0); break;
+      case 16: hipExtLaunchKernelGGL((k_pass1<16, PACK>), grid, block, smem, s, nullptr, nullptr, fl, a.g, a.mask, a.bits, a.out, a.part, a.part_ne, a, q0); break;
       default: return hipErrorInvalidValue;
     }
     const hipError_t e = hipGetLastError();
