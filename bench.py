@@ -8,12 +8,18 @@ fallback), for all W stacked workers.  Inputs are generated on the device
 before the timed region and stay resident in HBM.
 
 Metric: FP32-equivalent input GB/s = 4 * W * n_total / step time, and its
-fraction of the 8 TB/s HBM peak.  The JSON line also carries the roofline of
-the dominant kernel (pass 1), timed with HIP events that the library records
-on its own launch stream, and the oracle timed on the host as a CPU
-baseline on a bounded sample of the same workload.
+fraction of the 8 TB/s HBM peak.  The JSON line also carries
+  roofline      the dominant kernel (pass 1): algorithmic bytes per launch
+                over its average launch time, from HIP events the library
+                records on its own launch stream; `traffic` is the counter-
+                measured HBM bytes per launch from a committed rocprofv3 run
+                of the current kernel source (else null)
+  cpu_baseline  the oracle, single-threaded on one pinned host core, on a
+                bounded sample of the same workload
+  achievable    a plain streaming read of the same input (reference rate)
 
   python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload gpt1p3b]
+  python bench.py --calibrate-copy     (copy kernel of known size, for counters)
 """
 import argparse
 import ctypes
@@ -27,6 +33,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, AMD specification
+COPY_CAL_BYTES = 4 << 30  # bytes read (and written) by the calibration copy
 
 
 def parse():
@@ -41,6 +48,9 @@ def parse():
     ap.add_argument("--cpu-buckets", type=int, default=None,
                     help="buckets of the oracle's CPU sample (default: about 12 s of work)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-probe", action="store_true", help="skip the streaming-read reference")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run the copy kernel of known traffic (counter calibration)")
     return ap.parse_args()
 
 
@@ -53,7 +63,6 @@ class HipEvents:
         self.rt.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
                                                 ctypes.c_void_p]
         self.rt.hipEventDestroy.argtypes = [ctypes.c_void_p]
-        self.rt.hipEventSynchronize.argtypes = [ctypes.c_void_p]
 
     def create(self):
         ev = ctypes.c_void_p()
@@ -88,6 +97,39 @@ def counter_traffic(workload):
     return rec.get("hbm_bytes_per_launch")
 
 
+def host_cpu():
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return model, os.cpu_count()
+
+
+def calibrate_copy():
+    import torch
+    import synth
+    n = COPY_CAL_BYTES // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        synth.copy(src, dst)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    reps = 5
+    for _ in range(reps):
+        synth.copy(src, dst)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / reps
+    print(json.dumps({"kernel": "k_copy", "bytes_read_per_dispatch": COPY_CAL_BYTES,
+                      "bytes_written_per_dispatch": COPY_CAL_BYTES, "ms": round(ms, 4),
+                      "gbs_each_way": round(COPY_CAL_BYTES / ms / 1e6, 1)}), flush=True)
+    return 0
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -99,12 +141,15 @@ def main():
     import numpy as np
     import torch
 
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.init()
+    if args.calibrate_copy:
+        return calibrate_copy()
+
     import paper_2606_25759_amd as nf
     import synth
 
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
-    torch.cuda.init()
     lay = synth.CONFIGS[args.workload]()
     W, n, bn, nb = lay.W, lay.n_total, lay.bucket_n, lay.nb
     nw = (n + 63) // 64
@@ -123,6 +168,7 @@ def main():
     dec = torch.empty(nb * nf.DECISION_BYTES, dtype=torch.uint8, device=dev)
     ws = nf.empty_workspace(nf.nf_workspace_bytes_buckets(W, n, bn), dev)
     pol = nf.policy(force_lowbit=int(args.force_lowbit))
+    launches = nf.nf_pass1_launches(W, n, bn)
     torch.cuda.synchronize()
     print("[bench] inputs resident", file=sys.stderr, flush=True)
 
@@ -150,10 +196,12 @@ def main():
         for x in e:
             hip.destroy(x)
     pass1_ms, decide_ms, pass2_ms, device_ms = (float(v) for v in ph.mean(axis=0))
+    dev_med, dev_min = float(np.median(ph[:, 3])), float(ph[:, 3].min())
     print(f"[bench] {args.steps} steps: {ms_per_step:.3f} ms/step wall, device {device_ms:.3f} ms "
-          f"(pass1 {pass1_ms:.3f}, decide {decide_ms:.3f}, pass2 {pass2_ms:.3f})", file=sys.stderr, flush=True)
+          f"(median {dev_med:.3f}, min {dev_min:.3f}; pass1 {pass1_ms:.3f}, decide {decide_ms:.3f}, "
+          f"pass2 {pass2_ms:.3f})", file=sys.stderr, flush=True)
 
-    # decisions, routes and algorithmic bytes per launch
+    # decisions, routes and algorithmic bytes
     d = nf.decisions_host(dec, nb)
     routes = {"L": int((d["route"] == 0).sum()), "F": int((d["route"] == 1).sum()),
               "P": int((d["route"] == 2).sum())}
@@ -161,34 +209,58 @@ def main():
     nbs = np.array([min(bn, n - b * bn) for b in range(nb)], dtype=np.int64)
     ne = d["n_eligible"].astype(np.int64)
     nwb = (nbs + 63) // 64
-    pass1_bytes = float((4 * W * nbs + nbs / 8 + 8 * W * nwb + 4 * (nbs - ne)).sum())
+    # pass 1: gradients once, mask once, sign words out, FP32 sums at routed positions out
+    pass1_bytes = float((4 * W * nbs + 8 * nwb + 8 * W * nwb + 4 * (nbs - ne)).sum())
     is_l, is_f = d["route"] == 0, d["route"] == 1
-    pass2_bytes = float(((8 * W * nwb + nbs / 8 + (0 if args.no_counts else nbs) + 4 * ne) * is_l).sum()
-                        + ((4 * W * ne + nbs / 8 + 4 * ne) * is_f).sum())
+    pass2_bytes = float(((8 * W * nwb + 8 * nwb + (0 if args.no_counts else nbs) + 4 * ne) * is_l).sum()
+                        + ((4 * W * ne + 8 * nwb + 4 * ne) * is_f).sum())
     value = lay.input_bytes() / (ms_per_step * 1e-3) / 1e9
     achieved = pass1_bytes / (pass1_ms * 1e-3) / 1e9
 
-    # CPU baseline: the oracle, single-threaded, on the first buckets
+    # reference: one plain streaming read of the same gradients
+    achievable = None
+    if not args.no_probe:
+        sink = torch.zeros(1024, dtype=torch.float32, device=dev)
+        synth.read_probe(grads, sink)
+        torch.cuda.synchronize()
+        a0 = time.perf_counter()
+        for _ in range(3):
+            synth.read_probe(grads, sink)
+        torch.cuda.synchronize()
+        probe_ms = (time.perf_counter() - a0) * 1e3 / 3
+        achievable = round(4 * grads.numel() / (probe_ms * 1e-3) / 1e9, 1)
+        print(f"[bench] streaming read of the input: {achievable} GB/s", file=sys.stderr, flush=True)
+
+    # CPU baseline: the oracle, single-threaded, pinned to one core, on the first buckets
     cpu = None
     if not args.no_cpu_baseline:
         import oracle as nfo
         k = args.cpu_buckets or max(1, min(nb, int(12e9 * 0.35 / (4 * W * min(bn, n)))))
         opol = nfo.policy(force_lowbit=int(args.force_lowbit))
+        model, ncpu = host_cpu()
+        old_aff = os.sched_getaffinity(0)
+        core = min(old_aff)
         t_cpu, nbytes, ok = 0.0, 0, True
-        for b in range(k):
-            a, e = b * bn, min((b + 1) * bn, n)
-            gh = grads[:, a:e].contiguous().cpu().numpy()
-            mh = np.ascontiguousarray(mask_h[a // 64:(e + 63) // 64])
-            c0 = time.perf_counter()
-            ref = nfo.reduce_bucket(gh, mh, opol)
-            t_cpu += time.perf_counter() - c0
-            nbytes += 4 * W * (e - a)
-            rd = ref["decision"]
-            ok &= int(d["route"][b]) == rd.route and int(d["reasons"][b]) == rd.reasons
-            ok &= bool(np.array_equal(bits[:, a // 64:(e + 63) // 64].cpu().numpy().view(np.uint64), ref["bits"]))
+        try:
+            os.sched_setaffinity(0, {core})
+            for b in range(k):
+                a, e = b * bn, min((b + 1) * bn, n)
+                gh = grads[:, a:e].contiguous().cpu().numpy()
+                mh = np.ascontiguousarray(mask_h[a // 64:(e + 63) // 64])
+                c0 = time.perf_counter()
+                ref = nfo.reduce_bucket(gh, mh, opol)
+                t_cpu += time.perf_counter() - c0
+                nbytes += 4 * W * (e - a)
+                rd = ref["decision"]
+                ok &= int(d["route"][b]) == rd.route and int(d["reasons"][b]) == rd.reasons
+                ok &= bool(np.array_equal(bits[:, a // 64:(e + 63) // 64].cpu().numpy().view(np.uint64),
+                                          ref["bits"]))
+        finally:
+            os.sched_setaffinity(0, old_aff)
         cpu = {"value": round(nbytes / t_cpu / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
                "sample": f"{lay.name} buckets 0..{k - 1} ({k} x {min(bn, n):,} elements x {W} workers), "
-                         f"single-threaded C++ oracle, {t_cpu:.1f} s",
+                         f"single-threaded C++ oracle pinned to core {core} of {ncpu} ({model}), "
+                         f"{t_cpu:.1f} s",
                "sample_parity": "ok" if ok else "MISMATCH"}
         print(f"[bench] oracle: {cpu['value']} GB/s over {k} buckets ({t_cpu:.1f} s)", file=sys.stderr, flush=True)
 
@@ -210,13 +282,17 @@ def main():
                    "eligible_frac": round(float(ne.sum()) / n, 4),
                    "policy": "forced low-bit" if args.force_lowbit else "admitted, guard ok",
                    "counts_written": not args.no_counts},
+        "device_ms": {"mean": round(device_ms, 4), "median": round(dev_med, 4), "min": round(dev_min, 4)},
         "roofline": {"kernel": "k_pass1", "bound": "hbm", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": counter_traffic(lay.name),
-                     "algorithmic_bytes_per_launch": pass1_bytes, "avg_launch_ms": round(pass1_ms, 4)},
+                     "launches_per_step": launches,
+                     "algorithmic_bytes_per_launch": round(pass1_bytes / launches),
+                     "avg_launch_ms": round(pass1_ms / launches, 5)},
         "phases_ms": {"pass1": round(pass1_ms, 4), "decide": round(decide_ms, 4),
                       "pass2": round(pass2_ms, 4), "device_total": round(device_ms, 4),
                       "pass2_algorithmic_gbs": round(pass2_bytes / max(pass2_ms, 1e-9) / 1e6, 1)},
+        "achievable_read_gbs": achievable,
         "routes": routes,
         "mgtr": round(mgtr, 4),
         "cpu_baseline": cpu,

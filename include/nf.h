@@ -239,6 +239,14 @@ nf_status nf_route_buckets(const float* grads, int64_t worker_stride, int32_t W,
 nf_status nf_set_phase_events(void* before_pass1, void* after_pass1, void* after_decide,
                               void* after_pass2);
 
+/*
+ * Profiling query (no paper counterpart): the number of pass-1 kernel
+ * launches that one nf_route_buckets call with these sizes makes (pass 1
+ * runs in launches of a fixed number of element chunks).  0 for n_total = 0
+ * or invalid sizes.  Pure host function.
+ */
+int64_t nf_pass1_launches(int32_t W, int64_t n_total, int64_t bucket_n);
+
 #ifdef __cplusplus
 }
 #endif

@@ -31,7 +31,7 @@ NF_SEL_ROUTED, NF_SEL_ELIGIBLE, NF_SEL_ALL = 0, 1, 2
 EXPORTS = ["nf_abi_version", "nf_last_error", "nf_mask_from_segments", "nf_workspace_bytes",
            "nf_bucket_health", "nf_pack_signs", "nf_fp32_reduce", "nf_signcount_reduce",
            "nf_route_decide", "nf_route_bucket", "nf_workspace_bytes_buckets", "nf_route_buckets",
-           "nf_set_phase_events"]
+           "nf_set_phase_events", "nf_pass1_launches"]
 
 
 class nf_worker_stats(ctypes.Structure):
@@ -100,6 +100,7 @@ def load(path=None):
         "nf_route_buckets": (ctypes.c_int, [_P, _I64, _I32, _I64, _I64, _P, _P, _P, _I64, _P, _P,
                                             _P, _P, _P, _SZ, _P]),
         "nf_set_phase_events": (ctypes.c_int, [_P, _P, _P, _P]),
+        "nf_pass1_launches": (_I64, [_I32, _I64, _I64]),
     }
     for name, (res, args) in sigs.items():
         fn = getattr(lib, name)
@@ -262,6 +263,11 @@ def nf_route_buckets(grads, n_total, bucket_n, mask, pol, bits, counts, out, sta
 def nf_set_phase_events(before_pass1=None, after_pass1=None, after_decide=None, after_pass2=None):
     """Raw hipEvent_t handles (ints) or None; all None turns recording off."""
     _check(load().nf_set_phase_events(before_pass1, after_pass1, after_decide, after_pass2))
+
+
+def nf_pass1_launches(W, n_total, bucket_n):
+    """Pass-1 kernel launches of one nf_route_buckets call (profiling)."""
+    return int(load().nf_pass1_launches(W, n_total, bucket_n))
 
 
 # ------------------------------------------------------- result decoding
