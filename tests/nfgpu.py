@@ -66,7 +66,8 @@ def check_decision(d, rd, what=""):
     assert float(d["bytes_route"]) == rd.bytes_route and float(d["bytes_fp32"]) == rd.bytes_fp32, \
         f"{what} modeled bytes"
     s, rs = np.float32(d["scale"]), np.float32(rd.scale)
-    assert s == rs or abs(float(s) - float(rs)) <= REL_TOL * abs(float(rs)), f"{what} scale {s} {rs}"
+    assert s == rs or (np.isnan(s) and np.isnan(rs)) or abs(float(s) - float(rs)) <= REL_TOL * abs(float(rs)), \
+        f"{what} scale {s} {rs}"
 
 
 def check_output(out, ref, mask_words, n, W, decision, decode_mode, what=""):
