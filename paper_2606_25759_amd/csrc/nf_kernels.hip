@@ -204,7 +204,7 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
   };
   // The mask load goes out first, unpredicated, so that only it is waited
   // for before the barrier.
-  bool chunk_fast;
+  bool chunk_fast, chunk_routed;
   {
     const int64_t wbeg = (base + tb * tile) / 64;
     const int nwc = all_full ? (int)((te - tb) * (tile / 64)) : 0;
@@ -213,10 +213,101 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
       m0 = mask[wbeg + ((int)threadIdx.x < nwc ? (int)threadIdx.x : nwc - 1)];
       issue_words(tb, xa);
     }
-    int some_not = !all_full || ((int)threadIdx.x < nwc && m0 != ~0ull);
-    for (int i = threadIdx.x + kThreads1; i < nwc; i += kThreads1) some_not |= mask[wbeg + i] != ~0ull;
+    const bool mine = (int)threadIdx.x < nwc;
+    int some_not = !all_full || (mine && m0 != ~0ull);
+    int some_set = !all_full || (mine && m0 != 0ull);
+    for (int i = threadIdx.x + kThreads1; i < nwc; i += kThreads1) {
+      const uint64_t m1 = mask[wbeg + i];
+      some_not |= m1 != ~0ull;
+      some_set |= m1 != 0ull;
+    }
     chunk_fast = !__syncthreads_or(some_not) && a.sums != kSumsAll;
+    // Every element routed to FP32 (all tiles full, no mask bit set).
+    chunk_routed = WPW == 1 && stage_on && !__syncthreads_or(some_set);
     if (all_full && !chunk_fast) consume(xa);
+  }
+
+  // Chunks with every element routed to FP32 (one worker per wavefront):
+  // element-major, without the LDS stage or block barriers.  Lane l of
+  // wavefront v takes element 64s + l for steps s = v, v + 16, ..., loads
+  // that element of every worker (one 256-byte coalesced load per worker),
+  // adds them in worker order in FP32 and keeps each worker's FP64 sum of
+  // squares in its own register.  Nothing is eligible, so the sign words
+  // are 0 and every |g| sum over eligible elements is 0.
+  if (chunk_routed) {
+    constexpr int WR = kWaves;  // workers at most on this path
+    double q2[WR];
+    uint64_t nf2[WR];
+#pragma unroll
+    for (int w = 0; w < WR; ++w) {
+      q2[w] = 0.0;
+      nf2[w] = 0;
+    }
+    const int64_t c0 = base + tb * tile;
+    const int nsteps = (int)((te - tb) * (tile / 64));
+    for (int st = v; st < nsteps; st += kWaves) {
+      const int64_t e = c0 + (int64_t)st * 64 + lane;
+      float x[WR];
+#pragma unroll
+      for (int w = 0; w < WR; ++w) x[w] = w < a.W ? __builtin_nontemporal_load(g + (int64_t)w * a.wstride + e) : 0.0f;
+      float sum = x[0];
+#pragma unroll
+      for (int w = 1; w < WR; ++w)
+        if (w < a.W) sum = sum + x[w];
+      out[e] = a.mean ? sum / (float)a.W : sum;
+#pragma unroll
+      for (int w = 0; w < WR; ++w) {
+        const double d = (double)x[w];
+        q2[w] = __builtin_fma(d, d, q2[w]);
+      }
+      // A non-finite value in any worker makes the sum non-finite.
+      if (__ballot(!finite32(sum))) {
+#pragma unroll
+        for (int w = 0; w < WR; ++w) nf2[w] += __popcll(__ballot(!finite32(x[w])));
+      }
+    }
+    // Zero sign words for the chunk, row by row.
+    if (PACK) {
+      const int64_t gw0 = c0 / 64;
+      for (int i = threadIdx.x; i < a.W * nsteps; i += kThreads1) {
+        const int w = i / nsteps;
+        bits[(int64_t)w * a.bstride + gw0 + (i - w * nsteps)] = 0ull;
+      }
+    }
+    // Block partials: wavefront sums, then wavefronts in order.
+    Partial* red = reinterpret_cast<Partial*>(smem);
+#pragma unroll
+    for (int w = 0; w < WR; ++w) {
+      const double s2 = wave_sum(q2[w]);
+      if (lane == 0 && w < a.W) {
+        Partial p;
+        p.sabs = 0.0;
+        p.ssq = s2;
+        p.nonfinite = nf2[w];
+        red[v * a.W + w] = p;
+      }
+    }
+    __syncthreads();
+    const int64_t slot = (int64_t)b * a.slots + (c % kMaxSlots);
+    const bool first = c < kMaxSlots;
+    if ((int)threadIdx.x < a.W) {
+      const int w = threadIdx.x;
+      Partial p = red[w];
+      for (int v2 = 1; v2 < kWaves; ++v2) {
+        const Partial q3 = red[v2 * a.W + w];
+        p.ssq += q3.ssq;
+        p.nonfinite += q3.nonfinite;
+      }
+      if (!first) {
+        const Partial o = part[slot * a.W + w];
+        p.sabs = o.sabs + p.sabs;
+        p.ssq = o.ssq + p.ssq;
+        p.nonfinite = o.nonfinite + p.nonfinite;
+      }
+      part[slot * a.W + w] = p;
+    }
+    if (threadIdx.x == 0 && first) part_ne[slot] = 0;  // later chunks of the slot add nothing
+    return;
   }
   auto fast_body = [&](int64_t t, float (&X)[NX], float (&Xn)[NX]) {
     issue_words(t + 1, Xn);
