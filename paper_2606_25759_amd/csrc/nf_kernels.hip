@@ -725,8 +725,6 @@ __global__ __launch_bounds__(kThreads2) void k_pass2(
   const int64_t wbase = base / 64;
   const int v = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wavefront index, uniform
   const int lane = threadIdx.x & 63;
-  const int half = lane >> 5;
-  const int sh = lane & 31;
   int nplanes = 1;
   while ((1 << nplanes) <= a.W) ++nplanes;  // counts 0..W need nplanes bits
   uint32_t* my = rec[v];
@@ -793,21 +791,57 @@ __global__ __launch_bounds__(kThreads2) void k_pass2(
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-      // ---- decode, lane = element j of word k0 + kk
-      for (int kk = 0; kk < nk; ++kk) {
-        const uint4* r = reinterpret_cast<const uint4*>(my + (kk * 2 + half) * kRec);
+      // ---- decode: per 256 elements (four words), lane l takes elements
+      // 4l .. 4l + 3, i.e. nibble l % 16 of word l / 16.  A nibble of each
+      // plane spreads into the low bits of four bytes by one multiply
+      // (copies of the nibble at bits 0, 7, 14, 21 put its bit i at bit 8i),
+      // so the four counts form one 32-bit word: one dword store of counts
+      // and, where all four elements are eligible, one 16-byte store of
+      // decoded values.
+      const bool c4 = counts && ((reinterpret_cast<uintptr_t>(counts + base) & 3) == 0);
+      const bool o16 = out && ((reinterpret_cast<uintptr_t>(out + base) & 15) == 0);
+      for (int grp = 0; grp * 4 < nk; ++grp) {
+        const int kk = grp * 4 + (lane >> 4);
+        const int shn = 4 * (lane & 7);
+        const uint4* r = reinterpret_cast<const uint4*>(my + (kk * 2 + ((lane >> 3) & 1)) * kRec);
         const uint4 p03 = r[0];
         const uint4 p47 = r[1];
-        const uint32_t mh = r[2].x;
-        uint32_t c = ((p03.x >> sh) & 1u) | (((p03.y >> sh) & 1u) << 1) | (((p03.z >> sh) & 1u) << 2) |
-                     (((p03.w >> sh) & 1u) << 3);
+        const uint32_t mnib = (r[2].x >> shn) & 15u;
+        auto spread = [&](uint32_t plane) { return (((plane >> shn) & 15u) * 0x00204081u) & 0x01010101u; };
+        uint32_t cw4 = spread(p03.x) | (spread(p03.y) << 1) | (spread(p03.z) << 2) | (spread(p03.w) << 3);
         if (nplanes > 4)
-          c |= (((p47.x >> sh) & 1u) << 4) | (((p47.y >> sh) & 1u) << 5) | (((p47.z >> sh) & 1u) << 6) |
-               (((p47.w >> sh) & 1u) << 7);
-        const int64_t i = (k0 + kk) * 64 + lane;
-        if (i < nbe) {
-          if (counts) counts[base + i] = (uint8_t)c;
-          if (out && ((mh >> sh) & 1u)) out[base + i] = tab[c];
+          cw4 |= (spread(p47.x) << 4) | (spread(p47.y) << 5) | (spread(p47.z) << 6) | (spread(p47.w) << 7);
+        const int64_t i0 = (k0 + grp * 4) * 64 + 4 * lane;  // first of my four elements in the bucket
+        if (kk >= nk || i0 >= nbe) continue;
+        if (i0 + 3 < nbe) {
+          if (c4) {
+            *reinterpret_cast<uint32_t*>(counts + base + i0) = cw4;
+          } else if (counts) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) counts[base + i0 + e] = (uint8_t)(cw4 >> (8 * e));
+          }
+          if (out) {
+            if (o16 && mnib == 15u) {
+              float4 y;
+              y.x = tab[cw4 & 255u];
+              y.y = tab[(cw4 >> 8) & 255u];
+              y.z = tab[(cw4 >> 16) & 255u];
+              y.w = tab[cw4 >> 24];
+              *reinterpret_cast<float4*>(out + base + i0) = y;
+            } else {
+#pragma unroll
+              for (int e = 0; e < 4; ++e)
+                if ((mnib >> e) & 1u) out[base + i0 + e] = tab[(cw4 >> (8 * e)) & 255u];
+            }
+          }
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            if (i0 + e < nbe) {
+              if (counts) counts[base + i0 + e] = (uint8_t)(cw4 >> (8 * e));
+              if (out && ((mnib >> e) & 1u)) out[base + i0 + e] = tab[(cw4 >> (8 * e)) & 255u];
+            }
+          }
         }
       }
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
