@@ -28,7 +28,7 @@ class Policy(ctypes.Structure):
     _fields_ = [("admitted", ctypes.c_int), ("veto", ctypes.c_int),
                 ("guard_ok", ctypes.c_int), ("force_lowbit", ctypes.c_int),
                 ("decode_mode", ctypes.c_int), ("fp32_op", ctypes.c_int),
-                ("kappa", ctypes.c_double)]
+                ("kappa", ctypes.c_double), ("format", ctypes.c_int), ("tau", ctypes.c_float)]
 
 
 class Decision(ctypes.Structure):
@@ -68,6 +68,12 @@ def load(path=None):
         "nfo_output": (None, [_P, _I64, _P, _P, _P, ctypes.c_float, _I32, _P]),
         "nfo_reduce_bucket": (ctypes.c_int, [_P, _I64, _I32, _I64, _P, _P, _P, _I64,
                                              _P, _P, _P, _P]),
+        "nfo_ternary_threshold": (ctypes.c_float, [_P, _I64, ctypes.c_float]),
+        "nfo_pack_ternary": (None, [_P, _I64, _I32, _I64, _P, _P, _P, _P, _I64]),
+        "nfo_ternary_decode_table": (None, [_I32, _I32, _P]),
+        "nfo_ternary_output": (None, [_P, _I64, _P, _P, _P, _P, ctypes.c_float, _I32, _I32, _P]),
+        "nfo_reduce_bucket_ternary": (ctypes.c_int, [_P, _I64, _I32, _I64, _P, _P, _P, _P, _I64,
+                                                     _P, _P, _P, _P, _P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -89,8 +95,8 @@ def _grads(g):
 
 
 def policy(admitted=1, veto=0, guard_ok=1, force_lowbit=0, decode_mode=DECODE_SOFT,
-           fp32_op=OP_SUM, kappa=4.0):
-    return Policy(admitted, veto, guard_ok, force_lowbit, decode_mode, fp32_op, kappa)
+           fp32_op=OP_SUM, kappa=4.0, format=0, tau=0.5):
+    return Policy(admitted, veto, guard_ok, force_lowbit, decode_mode, fp32_op, kappa, format, tau)
 
 
 def mask_from_segments(off, length, eligible, n, lib=None):
@@ -203,3 +209,63 @@ def reduce_bucket(g, mask, pol=None, lib=None):
     if rc != 0:
         raise ValueError("invalid arguments")
     return dict(bits=bits[:, :nw], counts=c[:n], out=out[:n], stats=st, decision=d)
+
+
+# ---------------------------------------------------------- G-Ternary
+
+FORMAT_BINARY, FORMAT_TERNARY = 0, 1
+
+
+def ternary_threshold(stats_w, n_eligible, tau, lib=None):
+    """theta for one worker's stats record (STATS_DTYPE scalar or 1-array)."""
+    lib = lib or load()
+    st = np.ascontiguousarray(np.atleast_1d(stats_w)[:1], dtype=STATS_DTYPE)
+    return np.float32(lib.nfo_ternary_threshold(_ptr(st), n_eligible, ctypes.c_float(tau)))
+
+
+def pack_ternary(g, mask, theta, lib=None):
+    """(pos, neg) planes [W, ceil(n/64)] with per-worker thresholds theta."""
+    lib = lib or load()
+    g, stride = _grads(g)
+    W, n = g.shape
+    nw = (n + 63) // 64
+    pos = np.zeros((W, max(nw, 1)), dtype=np.uint64)
+    neg = np.zeros((W, max(nw, 1)), dtype=np.uint64)
+    th = np.ascontiguousarray(theta, dtype=np.float32)
+    lib.nfo_pack_ternary(_ptr(g), stride, W, n, _ptr(np.ascontiguousarray(mask, np.uint64)), _ptr(th),
+                         _ptr(pos), _ptr(neg), pos.shape[1])
+    return pos[:, :nw], neg[:, :nw]
+
+
+def ternary_decode_table(W, mode=DECODE_SOFT, lib=None):
+    """q[d + W] for d in [-W, W]."""
+    lib = lib or load()
+    q = np.zeros(2 * W + 1, dtype=np.float32)
+    lib.nfo_ternary_decode_table(W, mode, _ptr(q))
+    return q
+
+
+def reduce_bucket_ternary(g, mask, pol, lib=None):
+    """Whole bucket, G-Ternary payload.  Returns dict(pos, neg, cpos, cneg,
+    out, stats, decision)."""
+    lib = lib or load()
+    g, stride = _grads(g)
+    W, n = g.shape
+    nw = (n + 63) // 64
+    pos = np.zeros((W, max(nw, 1)), dtype=np.uint64)
+    neg = np.zeros((W, max(nw, 1)), dtype=np.uint64)
+    cp = np.zeros(max(n, 1), dtype=np.uint8)
+    cn = np.zeros(max(n, 1), dtype=np.uint8)
+    out = np.zeros(max(n, 1), dtype=np.float32)
+    st = np.zeros(W, dtype=STATS_DTYPE)
+    d = Decision()
+    m = np.ascontiguousarray(mask, np.uint64)
+    if m.size == 0:
+        m = np.zeros(1, np.uint64)
+    rc = lib.nfo_reduce_bucket_ternary(_ptr(g), stride, W, n, _ptr(m), ctypes.byref(pol), _ptr(pos),
+                                       _ptr(neg), pos.shape[1], _ptr(cp), _ptr(cn), _ptr(out), _ptr(st),
+                                       ctypes.byref(d))
+    if rc != 0:
+        raise ValueError("invalid arguments")
+    return dict(pos=pos[:, :nw], neg=neg[:, :nw], cpos=cp[:n], cneg=cn[:n], out=out[:n], stats=st,
+                decision=d)

@@ -43,6 +43,21 @@
  *       before L.
  *   R14 Modeled bytes per worker (§3.2 MGTR): FP32 = 4n; the selected route
  *       is n_E/8 + 4 (one FP32 scale) + 4 n_F for L and 4n for F and P.
+ *
+ * G-Ternary (§2.2 adds a zero-gating rule to the sign route; §5.2 applies
+ * the gating pattern around the vote; the paper fixes neither the rule nor
+ * its point):
+ *   R18 Gating is on the write side, before aggregation (§2.2), per worker:
+ *       theta_w = fl32(tau * fl32(S_w / n_E)), S_w the worker's FP64 |g| sum
+ *       over eligible elements (R8), tau >= 0 a policy input (default 0.5).
+ *       An eligible element with |g| < theta_w (FP32 comparison) is gated to
+ *       0.  NaN compares false, so it is never gated and never votes.
+ *   R19 The payload is two positional planes per worker (R2 layout): pos =
+ *       eligible, not gated and g > 0; neg = eligible, not gated and g < 0.
+ *   R20 Counts c+ and c- per coordinate; d = c+ - c-; SOFT q_d = fl32(d / W),
+ *       MAJORITY q_d = sign(d) (0 at d = 0); the output is fl32(scale * q_d)
+ *       with the scale of R5.  Routes, reasons and FP32 positions as above.
+ *   R21 MGTR for the ternary L route: 2 n_E / 8 + 4 + 4 n_F bytes per worker.
  */
 #include "nfo.h"
 
@@ -170,8 +185,9 @@ void nfo_decide(const nfo_stats* stats, int32_t W, int64_t n,
   d->scale = nfo_scale(stats, W, n_eligible);
   d->n_eligible = n_eligible;
   d->bytes_fp32 = 4.0 * (double)n;
-  if (route == NFO_ROUTE_L)
-    d->bytes_route = (double)n_eligible / 8.0 + 4.0 +
+  if (route == NFO_ROUTE_L)  /* one bit (R14) or two planes (R21) per element */
+    d->bytes_route = (p->format == NFO_FORMAT_TERNARY ? 2.0 : 1.0) *
+                         (double)n_eligible / 8.0 + 4.0 +
                      4.0 * (double)(n - n_eligible);
   else
     d->bytes_route = 4.0 * (double)n;
@@ -241,7 +257,8 @@ int nfo_reduce_bucket(const float* g, int64_t stride, int32_t W, int64_t n,
                       const uint64_t* mask, const nfo_policy* p,
                       uint64_t* bits, int64_t bits_stride, uint8_t* counts,
                       float* out, nfo_stats* stats, nfo_decision* d) {
-  if (W < 1 || W > 255 || n < 0 || stride < n || bits_stride < (n + 63) / 64)
+  if (W < 1 || W > 255 || n < 0 || stride < n || bits_stride < (n + 63) / 64 ||
+      p->format != NFO_FORMAT_BINARY)
     return -1;
   int64_t n_eligible = nfo_count_eligible(mask, n);          /* step 3 */
   nfo_health(g, stride, W, n, mask, stats);
@@ -259,6 +276,87 @@ int nfo_reduce_bucket(const float* g, int64_t stride, int32_t W, int64_t n,
     nfo_fp32_path(g + i0, stride, W, m, p->fp32_op, y);
     nfo_output(mask + i0 / 64, m, counts + i0, y, q, d->scale, d->route,
                out + i0);
+  }
+  return 0;
+}
+
+/* ---- G-Ternary: gate threshold (§2.2, R18) ------------------------------ */
+float nfo_ternary_threshold(const nfo_stats* st, int64_t n_eligible, float tau) {
+  if (n_eligible <= 0) return 0.0f;
+  float mean_abs = (float)(st->sum_abs_elig / (double)n_eligible);
+  return tau * mean_abs;
+}
+
+/* ---- G-Ternary: write-side payload (§2.2, R18, R19) --------------------- */
+void nfo_pack_ternary(const float* g, int64_t stride, int32_t W, int64_t n,
+                      const uint64_t* mask, const float* theta, uint64_t* pos,
+                      uint64_t* neg, int64_t bits_stride) {
+  int64_t nwords = (n + 63) / 64;
+  for (int32_t w = 0; w < W; ++w) {
+    const float* row = g + (int64_t)w * stride;
+    uint64_t* prow = pos + (int64_t)w * bits_stride;
+    uint64_t* nrow = neg + (int64_t)w * bits_stride;
+    for (int64_t k = 0; k < nwords; ++k) {
+      prow[k] = 0;
+      nrow[k] = 0;
+    }
+    for (int64_t i = 0; i < n; ++i) {
+      if (!mask_bit(mask, i)) continue;
+      float x = row[i];
+      if (fabsf(x) < theta[w]) continue;  /* gated to 0 */
+      if (x > 0.0f) prow[i / 64] |= (uint64_t)1 << (i % 64);
+      if (x < 0.0f) nrow[i / 64] |= (uint64_t)1 << (i % 64);
+    }
+  }
+}
+
+/* ---- G-Ternary: decode table over the vote difference (§5.2, R20) ------- */
+void nfo_ternary_decode_table(int32_t W, int32_t mode, float* q) {
+  for (int32_t d = -W; d <= W; ++d) {
+    if (mode == NFO_DECODE_MAJORITY)
+      q[d + W] = d > 0 ? 1.0f : (d < 0 ? -1.0f : 0.0f);
+    else
+      q[d + W] = (float)d / (float)W;
+  }
+}
+
+void nfo_ternary_output(const uint64_t* mask, int64_t n, const uint8_t* cpos,
+                        const uint8_t* cneg, const float* y, const float* q,
+                        float scale, int32_t W, int32_t route, float* out) {
+  for (int64_t i = 0; i < n; ++i) {
+    if (route == NFO_ROUTE_L && mask_bit(mask, i))
+      out[i] = scale * q[(int32_t)cpos[i] - (int32_t)cneg[i] + W];
+    else
+      out[i] = y[i];
+  }
+}
+
+/* ---- the whole bucket, G-Ternary payload (§3.3 steps 3-7, R18-R21) ------ */
+int nfo_reduce_bucket_ternary(const float* g, int64_t stride, int32_t W,
+                              int64_t n, const uint64_t* mask,
+                              const nfo_policy* p, uint64_t* pos, uint64_t* neg,
+                              int64_t bits_stride, uint8_t* cpos, uint8_t* cneg,
+                              float* out, nfo_stats* stats, nfo_decision* d) {
+  if (W < 1 || W > 255 || n < 0 || stride < n || bits_stride < (n + 63) / 64 ||
+      p->format != NFO_FORMAT_TERNARY || !(p->tau >= 0.0f))
+    return -1;
+  int64_t n_eligible = nfo_count_eligible(mask, n);          /* step 3 */
+  nfo_health(g, stride, W, n, mask, stats);
+  nfo_decide(stats, W, n, n_eligible, p, d);                 /* steps 4, 6 */
+  float theta[256];
+  for (int32_t w = 0; w < W; ++w)
+    theta[w] = nfo_ternary_threshold(&stats[w], n_eligible, p->tau);
+  nfo_pack_ternary(g, stride, W, n, mask, theta, pos, neg, bits_stride); /* 5 */
+  nfo_counts(pos, bits_stride, W, n, cpos);                  /* step 7 */
+  nfo_counts(neg, bits_stride, W, n, cneg);
+  float q[511];
+  nfo_ternary_decode_table(W, p->decode_mode, q);
+  for (int64_t i0 = 0; i0 < n; i0 += 4096) {
+    int64_t m = n - i0 < 4096 ? n - i0 : 4096;
+    float y[4096];
+    nfo_fp32_path(g + i0, stride, W, m, p->fp32_op, y);
+    nfo_ternary_output(mask + i0 / 64, m, cpos + i0, cneg + i0, y, q, d->scale,
+                       W, d->route, out + i0);
   }
   return 0;
 }

@@ -10,7 +10,8 @@
  * Sources (NEURON-Fabric, arXiv 2606.25759):
  *   - §2.2 (Low-bit gradient aggregation): G-Binary is a one-bit sign-count
  *     route; workers send a compact direction payload and the reducer
- *     returns an aggregate direction.
+ *     returns an aggregate direction.  G-Ternary adds a zero-gating rule
+ *     that suppresses selected entries before aggregation.
  *   - §3.2 (Calibration-to-runtime interface): route states L / F / P and the
  *     modeled gradient-communication traffic ratio (MGTR) equation.
  *   - §3.3 (Runtime execution), steps 3-7: classify bucket contents, encode
@@ -27,8 +28,8 @@
  *   - §6.4 (Endpoint-capacity guard): the guard outcome is a comparison the
  *     caller supplies; a rejected bucket stays on FP32.
  *
- * Readings where the paper is silent are fixed here and numbered R1..R14;
- * each function names the readings it applies.
+ * Readings where the paper is silent are fixed in nfo.cpp and numbered
+ * R1..R21; each function names the readings it applies.
  *
  * Layouts: gradients are W rows of FP32, row w starting at g + w*stride.
  * Masks and sign bitmaps are little-endian uint64 words, LSB-first: bit j of
@@ -60,6 +61,8 @@ enum {
 
 enum { NFO_DECODE_SOFT = 0, NFO_DECODE_MAJORITY = 1 };
 enum { NFO_OP_SUM = 0, NFO_OP_MEAN = 1 };
+/* Payload formats of §2.2: G-Binary (sign counts), G-Ternary (zero gating). */
+enum { NFO_FORMAT_BINARY = 0, NFO_FORMAT_TERNARY = 1 };
 
 typedef struct {
   uint64_t nonfinite;   /* count of non-finite values of worker w over all n   */
@@ -75,6 +78,9 @@ typedef struct {
   int decode_mode;   /* NFO_DECODE_SOFT or NFO_DECODE_MAJORITY         */
   int fp32_op;       /* NFO_OP_SUM or NFO_OP_MEAN                      */
   double kappa;      /* norm-spike ratio on L2 norms (R12)             */
+  int format;        /* NFO_FORMAT_BINARY or NFO_FORMAT_TERNARY        */
+  float tau;         /* G-Ternary gate, in units of the worker's mean
+                        |g| over eligible elements (R18)              */
 } nfo_policy;
 
 typedef struct {
@@ -117,11 +123,34 @@ void nfo_output(const uint64_t* mask, int64_t n, const uint8_t* counts,
 
 /* The whole bucket, steps in the order of §3.3.  bits, counts, out and
  * stats are always written (bits and counts are computed for every route).
- * Returns 0, or -1 on invalid arguments. */
+ * Returns 0, or -1 on invalid arguments or a format other than binary. */
 int nfo_reduce_bucket(const float* g, int64_t stride, int32_t W, int64_t n,
                       const uint64_t* mask, const nfo_policy* p,
                       uint64_t* bits, int64_t bits_stride, uint8_t* counts,
                       float* out, nfo_stats* stats, nfo_decision* d);
+
+/* ---- G-Ternary (§2.2 zero gating; readings R18-R21) ---------------------
+ * A worker's gate threshold from its statistics: fl32(tau * fl32(S / n_E))
+ * with S its |g| sum over eligible elements; 0 when n_E = 0 (R18). */
+float nfo_ternary_threshold(const nfo_stats* st, int64_t n_eligible, float tau);
+/* Two planes per worker (R19): pos bit = eligible, not gated, g > 0; neg
+ * bit = eligible, not gated, g < 0; gated means |g| < theta[w]. */
+void nfo_pack_ternary(const float* g, int64_t stride, int32_t W, int64_t n,
+                      const uint64_t* mask, const float* theta, uint64_t* pos,
+                      uint64_t* neg, int64_t bits_stride);
+/* q[d + W] for d = c+ - c- in [-W, W] (R20). */
+void nfo_ternary_decode_table(int32_t W, int32_t mode, float* q /* 2W+1 */);
+void nfo_ternary_output(const uint64_t* mask, int64_t n, const uint8_t* cpos,
+                        const uint8_t* cneg, const float* y, const float* q,
+                        float scale, int32_t W, int32_t route, float* out);
+/* The whole bucket with the G-Ternary payload: pos and neg planes, c+ and c-
+ * counts, out, stats and the decision (the MGTR bytes of R21).  Returns 0,
+ * or -1 on invalid arguments or a format other than ternary. */
+int nfo_reduce_bucket_ternary(const float* g, int64_t stride, int32_t W,
+                              int64_t n, const uint64_t* mask,
+                              const nfo_policy* p, uint64_t* pos, uint64_t* neg,
+                              int64_t bits_stride, uint8_t* cpos, uint8_t* cneg,
+                              float* out, nfo_stats* stats, nfo_decision* d);
 
 #ifdef __cplusplus
 }

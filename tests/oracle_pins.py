@@ -626,11 +626,191 @@ def pin_health_routes(lib):
         assert r["decision"].reasons == bit | nfo.R_FORCED, "forced reasons"
 
 
+# ------------------------------------------------------------- G-Ternary
+
+
+def model_theta(S, nE, tau):
+    """R18 from IEEE arithmetic: double division, then FP32 rounding, then an
+    FP32 product (numpy float32 scalars)."""
+    if nE <= 0:
+        return np.float32(0.0)
+    return np.float32(np.float32(tau) * np.float32(float(S) / nE))
+
+
+def model_planes(g, m, theta):
+    """R19 written from its definition, element by element."""
+    W, n = g.shape
+    pos = np.zeros((W, n), dtype=np.uint8)
+    neg = np.zeros((W, n), dtype=np.uint8)
+    with np.errstate(invalid="ignore"):
+        for w in range(W):
+            for i in range(n):
+                x = np.float32(g[w, i])
+                if not m[i] or np.abs(x) < theta[w]:
+                    continue
+                pos[w, i] = 1 if x > 0 else 0
+                neg[w, i] = 1 if x < 0 else 0
+    return pos, neg
+
+
+def unpack_rows(words, n):
+    words = np.atleast_2d(np.asarray(words, dtype=np.uint64))
+    return np.array([[int((int(r[i // 64]) >> (i % 64)) & 1) for i in range(n)] for r in words], dtype=np.uint8)
+
+
+def stats_rec(S):
+    st = np.zeros(1, dtype=nfo.STATS_DTYPE)
+    st["sum_abs_elig"] = S
+    return st
+
+
+def pin_ternary_threshold(lib):
+    """R18 against IEEE arithmetic and exact rationals, including a case where
+    rounding once (instead of twice) gives a different threshold."""
+    rng = np.random.default_rng(31)
+    for _ in range(200):
+        S = float(rng.random() * 10.0 ** int(rng.integers(-8, 4)))
+        nE = int(rng.integers(1, 10 ** 6))
+        tau = float(np.float32(rng.random() * 3))
+        got = nfo.ternary_threshold(stats_rec(S), nE, tau, lib=lib)
+        assert same_f32(got, model_theta(S, nE, tau)), f"theta S={S} nE={nE} tau={tau}"
+    assert nfo.ternary_threshold(stats_rec(5.0), 0, 0.5, lib=lib) == 0.0, "theta without eligible elements"
+    # dyadic: (3/4) * 0.5 exactly
+    assert nfo.ternary_threshold(stats_rec(3.0), 4, 0.5, lib=lib) == np.float32(0.375), "theta dyadic"
+    # S / n_E = 1 + 2^-24 + 2^-30: fl32 rounds it up to 1 + 2^-23; times 3 is
+    # 3 + 1.5 ulp, a tie that goes to 3 + 2^-21.  Rounding the exact product
+    # once would give 3 + 2^-22.
+    S = 1.0 + 2.0 ** -24 + 2.0 ** -30
+    want = f32_round(Fraction(3) * Fraction(float(np.float32(S))))
+    assert want == np.float32(3 + 2.0 ** -21)
+    got = nfo.ternary_threshold(stats_rec(S), 1, 3.0, lib=lib)
+    assert same_f32(got, want), f"theta double rounding: {got!r} != {want!r}"
+
+
+def pin_pack_ternary_bruteforce(lib):
+    """Every value class around the threshold, with signed zeros, NaN and
+    infinities, masks with holes, a different threshold per worker."""
+    for W in (1, 2, 3):
+        theta = np.array([0.25, 1.0, 2.5][:W], dtype=np.float32)
+        vals = []
+        for t in theta:
+            for v in (t, np.nextafter(t, np.float32(0)), np.nextafter(t, np.float32(np.inf)), 2 * t, t / 2):
+                vals += [v, -v]
+        vals += [0.0, -0.0, np.nan, np.inf, -np.inf, 1e-45, -1e-45, 3.4e38, -3.4e38]
+        vals = np.array(vals, dtype=np.float32)
+        n = 3 * len(vals)
+        rng = np.random.default_rng(W)
+        g = np.stack([np.concatenate([np.roll(vals, w + k) for k in range(3)]) for w in range(W)]).astype(np.float32)
+        m = (rng.random(n) < 0.8).astype(np.uint8)
+        pos, neg = nfo.pack_ternary(g, mask_of(m), theta, lib=lib)
+        mp, mn = model_planes(g, m, theta)
+        assert np.array_equal(unpack_rows(pos, n), mp), f"pos plane W={W}"
+        assert np.array_equal(unpack_rows(neg, n), mn), f"neg plane W={W}"
+        assert not np.any(unpack_rows(pos, n) & unpack_rows(neg, n)), "an element in both planes"
+
+
+def pin_ternary_decode_table(lib):
+    for W in (1, 2, 3, 5, 16, 64, 127, 255):
+        q = nfo.ternary_decode_table(W, nfo.DECODE_SOFT, lib=lib)
+        want = np.array([f32_round(Fraction(d, W)) for d in range(-W, W + 1)], dtype=np.float32)
+        assert same_f32(q, want), f"ternary SOFT table W={W}"
+        q = nfo.ternary_decode_table(W, nfo.DECODE_MAJORITY, lib=lib)
+        want = np.array([np.sign(d) for d in range(-W, W + 1)], dtype=np.float32)
+        assert same_f32(q, want), f"ternary MAJORITY table W={W}"
+
+
+def pin_ternary_tau0_is_binary(lib):
+    """tau = 0 and no zero or NaN: the vote difference is 2c - W, so every
+    output equals the binary route's bit for bit."""
+    rng = np.random.default_rng(33)
+    for W in (1, 2, 5, 16):
+        for mode in (nfo.DECODE_SOFT, nfo.DECODE_MAJORITY):
+            n = 333
+            g = gauss(rng, W, n)
+            g[g == 0] = 1e-3
+            m = (rng.random(n) < 0.85).astype(np.uint8)
+            words = mask_of(m)
+            rb = nfo.reduce_bucket(g, words, nfo.policy(decode_mode=mode), lib=lib)
+            rt = nfo.reduce_bucket_ternary(g, words, nfo.policy(decode_mode=mode, format=1, tau=0.0), lib=lib)
+            assert same_f32(rt["out"], rb["out"]), f"tau=0 output W={W} mode={mode}"
+            assert np.array_equal(rt["pos"], rb["bits"]), "tau=0 pos plane = sign bits"
+            assert np.array_equal(rt["cpos"], rb["counts"]), "tau=0 c+"
+            assert np.array_equal(rt["cneg"], np.where(m == 1, W - rb["counts"].astype(int), 0)), "tau=0 c-"
+
+
+def pin_ternary_gate_all(lib):
+    """A threshold above every value gates everything: no votes, output 0 at
+    eligible positions, FP32 at routed ones."""
+    rng = np.random.default_rng(34)
+    W, n = 6, 200
+    g = gauss(rng, W, n)
+    m = (rng.random(n) < 0.7).astype(np.uint8)
+    r = nfo.reduce_bucket_ternary(g, mask_of(m), nfo.policy(format=1, tau=1e30), lib=lib)
+    assert not r["pos"].any() and not r["neg"].any(), "gate all: planes"
+    assert not r["cpos"].any() and not r["cneg"].any(), "gate all: counts"
+    e = m == 1
+    assert np.all(r["out"][e] == 0.0), "gate all: decoded 0"
+    assert same_f32(r["out"][~e], model_fp32_sum(g)[~e]), "gate all: routed positions"
+
+
+def pin_ternary_whole_bucket(lib):
+    """Dyadic tiny buckets (every FP64 step of the oracle exact): all outputs
+    against the models, plus the two-plane MGTR bytes of R21."""
+    rng = np.random.default_rng(35)
+    for trial in range(24):
+        W = int(rng.integers(1, 6))
+        n = int(rng.integers(1, 140))
+        g = (rng.integers(-40, 41, (W, n)) / 64.0).astype(np.float32)
+        m = (rng.random(n) < 0.75).astype(np.uint8)
+        tau = float([0.0, 0.5, 1.0, 1.5][trial % 4])
+        mode = nfo.DECODE_SOFT if trial % 3 else nfo.DECODE_MAJORITY
+        r = nfo.reduce_bucket_ternary(g, mask_of(m), nfo.policy(format=1, tau=tau, decode_mode=mode,
+                                                                  force_lowbit=1), lib=lib)
+        nE = int(m.sum())
+        theta = np.array([model_theta(sum(abs(frac(g[w, i])) for i in range(n) if m[i]), nE, tau)
+                          for w in range(W)], dtype=np.float32)
+        mp, mn = model_planes(g, m, theta)
+        assert np.array_equal(unpack_rows(r["pos"], n), mp) and np.array_equal(unpack_rows(r["neg"], n), mn), \
+            f"planes trial {trial}"
+        cp, cn = mp.sum(axis=0), mn.sum(axis=0)
+        assert np.array_equal(r["cpos"], cp) and np.array_equal(r["cneg"], cn), f"counts trial {trial}"
+        scale = model_scale_exact(g, m)
+        assert same_f32(r["decision"].scale, scale), f"scale trial {trial}"
+        y = model_fp32_sum(g)
+        for i in range(n):
+            if m[i]:
+                d = int(cp[i]) - int(cn[i])
+                q = np.float32(np.sign(d)) if mode == nfo.DECODE_MAJORITY else f32_round(Fraction(d, W))
+                want = f32_round(frac(scale) * frac(q))
+            else:
+                want = y[i]
+            assert same_f32(r["out"][i], want), f"output trial {trial} i={i}"
+        assert r["decision"].bytes_route == 2 * nE / 8 + 4 + 4 * (n - nE), f"MGTR bytes trial {trial}"
+
+
+def pin_ternary_negation(lib):
+    """Negating every gradient swaps the planes and negates the decoded values."""
+    rng = np.random.default_rng(36)
+    W, n = 7, 257
+    g = gauss(rng, W, n)
+    m = (rng.random(n) < 0.8).astype(np.uint8)
+    words = mask_of(m)
+    pol = nfo.policy(format=1, tau=0.5)
+    a = nfo.reduce_bucket_ternary(g, words, pol, lib=lib)
+    b = nfo.reduce_bucket_ternary(-g, words, pol, lib=lib)
+    assert np.array_equal(a["pos"], b["neg"]) and np.array_equal(a["neg"], b["pos"]), "negation planes"
+    e = m == 1
+    assert np.array_equal(a["out"][e], -b["out"][e]), "negation decoded values"
+
+
 ALL_PINS = [pin_mask_from_segments, pin_pack_bruteforce, pin_counts_invariants, pin_fp32_path,
             pin_health, pin_scale, pin_decode_table, pin_whole_bucket_bruteforce,
             pin_appendix_example, pin_w1, pin_negation, pin_scaling, pin_all_fp32_mask,
             pin_route_truth_table, pin_norm_spike_median, pin_spike_construction,
-            pin_route_correctness, pin_health_routes]
+            pin_route_correctness, pin_health_routes,
+            pin_ternary_threshold, pin_pack_ternary_bruteforce, pin_ternary_decode_table,
+            pin_ternary_tau0_is_binary, pin_ternary_gate_all, pin_ternary_whole_bucket,
+            pin_ternary_negation]
 
 
 def run_all(lib):

@@ -63,9 +63,14 @@ MUTANTS = [
     ("forced_reason_missing", "    r |= NFO_R_FORCED;\n", ""),
     ("bytes_without_scale", "(double)n_eligible / 8.0 + 4.0 +", "(double)n_eligible / 8.0 +"),
     ("bytes_bits_not_bytes", "(double)n_eligible / 8.0 + 4.0 +", "(double)n_eligible + 4.0 +"),
-    ("output_decodes_routed", "    if (route == NFO_ROUTE_L && mask_bit(mask, i))", "    if (route == NFO_ROUTE_L)"),
+    ("output_decodes_routed", "    if (route == NFO_ROUTE_L && mask_bit(mask, i))\n      out[i] = scale * q[counts[i]];",
+     "    if (route == NFO_ROUTE_L)\n      out[i] = scale * q[counts[i]];"),
     ("output_count_off_by_one", "out[i] = scale * q[counts[i]];", "out[i] = scale * q[counts[i] ? counts[i] - 1 : 0];"),
-    ("output_ignores_route", "    if (route == NFO_ROUTE_L && mask_bit(mask, i))", "    if (mask_bit(mask, i))"),
+    ("output_ignores_route", "    if (route == NFO_ROUTE_L && mask_bit(mask, i))\n      out[i] = scale * q[counts[i]];",
+     "    if (mask_bit(mask, i))\n      out[i] = scale * q[counts[i]];"),
+    ("tern_output_decodes_routed",
+     "    if (route == NFO_ROUTE_L && mask_bit(mask, i))\n      out[i] = scale * q[(int32_t)cpos[i]",
+     "    if (route == NFO_ROUTE_L)\n      out[i] = scale * q[(int32_t)cpos[i]"),
     ("mask_ignores_eligibility", "    if (!eligible[s]) continue;  /* FP32-only segment: bits stay 0 */\n", ""),
     ("mask_short_segment", "for (int64_t i = off[s]; i < off[s] + len[s]; ++i)",
      "for (int64_t i = off[s]; i + 1 < off[s] + len[s]; ++i)"),
@@ -74,6 +79,20 @@ MUTANTS = [
      "  for (int64_t i = 0; i < n; ++i) c += 1;"),
     ("health_skips_last_element", "    for (int64_t i = 0; i < n; ++i) {\n      double x",
      "    for (int64_t i = 0; i + 1 < n; ++i) {\n      double x"),
+    # G-Ternary (R18-R21)
+    ("tern_gate_le", "if (fabsf(x) < theta[w]) continue;", "if (fabsf(x) <= theta[w]) continue;"),
+    ("tern_gate_signed", "if (fabsf(x) < theta[w]) continue;", "if (x < theta[w]) continue;"),
+    ("tern_neg_includes_zero", "if (x < 0.0f) nrow[i / 64]", "if (x <= 0.0f) nrow[i / 64]"),
+    ("tern_ignores_mask", "      if (!mask_bit(mask, i)) continue;\n      float x = row[i];", "      float x = row[i];"),
+    ("tern_vote_reversed", "q[(int32_t)cpos[i] - (int32_t)cneg[i] + W]", "q[(int32_t)cneg[i] - (int32_t)cpos[i] + W]"),
+    ("tern_threshold_rounded_once",
+     "  float mean_abs = (float)(st->sum_abs_elig / (double)n_eligible);\n  return tau * mean_abs;",
+     "  return (float)((double)tau * (st->sum_abs_elig / (double)n_eligible));"),
+    ("tern_threshold_sum_not_mean", "(float)(st->sum_abs_elig / (double)n_eligible)", "(float)(st->sum_abs_elig)"),
+    ("tern_bytes_one_plane", "(p->format == NFO_FORMAT_TERNARY ? 2.0 : 1.0)", "1.0"),
+    ("tern_majority_tie", "q[d + W] = d > 0 ? 1.0f", "q[d + W] = d >= 0 ? 1.0f"),
+    ("tern_counts_neg_from_pos", "nfo_counts(neg, bits_stride, W, n, cneg);", "nfo_counts(pos, bits_stride, W, n, cneg);"),
+    ("tern_decode_by_reciprocal", "q[d + W] = (float)d / (float)W;", "q[d + W] = (float)d * (1.0f / (float)W);"),
 ]
 
 
