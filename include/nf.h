@@ -57,7 +57,7 @@
 extern "C" {
 #endif
 
-#define NF_ABI_VERSION 1
+#define NF_ABI_VERSION 2
 
 typedef enum {
   NF_OK = 0,
@@ -86,6 +86,9 @@ enum {
 enum { NF_DECODE_SOFT = 0, NF_DECODE_MAJORITY = 1 };
 enum { NF_FP32_SUM = 0, NF_FP32_MEAN = 1 };
 enum { NF_SEL_ROUTED = 0, NF_SEL_ELIGIBLE = 1, NF_SEL_ALL = 2 };
+/* Low-bit payload formats (§2.2): G-Binary sign counts; G-Ternary adds
+ * write-side zero gating and a second (negative) plane. */
+enum { NF_FORMAT_BINARY = 0, NF_FORMAT_TERNARY = 1 };
 
 /* Per-worker health of one bucket. */
 typedef struct {
@@ -103,6 +106,10 @@ typedef struct {
   int32_t decode_mode;   /* NF_DECODE_SOFT (default) or NF_DECODE_MAJORITY     */
   int32_t fp32_op;       /* NF_FP32_SUM (default) or NF_FP32_MEAN              */
   double kappa;          /* norm-spike ratio on L2 norms, > 0 (default 4.0)    */
+  int32_t format;        /* NF_FORMAT_BINARY (default) or NF_FORMAT_TERNARY    */
+  float tau;             /* G-Ternary gate in units of each worker's mean |g|
+                            over eligible elements, finite and >= 0 (default
+                            0.5; see nf_ternary_threshold)                     */
 } nf_route_policy;
 
 /* Route decision of one bucket (40 bytes). */
@@ -114,7 +121,9 @@ typedef struct {
   uint32_t reserved;    /* 0                                                   */
   int64_t n_eligible;   /* n_E: mask bits set in [0, n)                        */
   double bytes_route;   /* modeled payload bytes per worker of this route:
-                           n_E/8 + 4 + 4(n - n_E) for L, 4n for F and P        */
+                           b*n_E/8 + 4 + 4(n - n_E) for L with b = 1 bit per
+                           element (binary) or 2 (ternary's two planes);
+                           4n for F and P                                      */
   double bytes_fp32;    /* matched FP32 payload bytes per worker: 4n (§3.2)    */
 } nf_route_decision;
 
@@ -181,6 +190,42 @@ nf_status nf_signcount_reduce(const uint64_t* bits, int64_t bits_stride_words, i
                               int32_t decode_mode, uint8_t* counts, float* out, void* stream);
 
 /*
+ * G-Ternary write-side threshold (§2.2's zero gating, applied before
+ * aggregation; host, pure function): for each worker w,
+ * theta[w] = fl32(tau * fl32(stats[w].sum_abs_elig / n_eligible)), i.e. tau
+ * times the worker's mean |g| over eligible elements; 0 when n_eligible = 0.
+ */
+nf_status nf_ternary_threshold(const nf_worker_stats* stats_host, int32_t W, int64_t n_eligible,
+                               float tau, float* theta_host);
+
+/*
+ * G-Ternary write-side payload (§2.2, §3.3 step 5): two positional planes
+ * per worker in the layout of the sign bitmaps.  Row w (0 <= w < W) is the
+ * positive plane, row W + w the negative plane of worker w: bit j of word k
+ * is set when element 64k+j is eligible, not gated (|g| < theta[w] gates it
+ * to 0, an FP32 comparison) and g > 0 (positive) or g < 0 (negative).  NaN
+ * is never gated and never set.  theta_dev: W floats (device), e.g. from
+ * nf_ternary_threshold.  bits holds 2W rows of bits_stride_words words; all
+ * ceil(n/64) words of each row are written, zero padded.  No workspace.
+ */
+nf_status nf_pack_ternary(const float* grads, int64_t worker_stride, int32_t W, int64_t n,
+                          const uint64_t* mask, const float* theta_dev, uint64_t* bits,
+                          int64_t bits_stride_words, void* stream);
+
+/*
+ * G-Ternary read side (§3.3 step 7, §5.2 vote and scaled write-back):
+ * c+_i and c-_i are the per-coordinate counts of the positive rows (0..W-1)
+ * and negative rows (W..2W-1) of bits; d_i = c+_i - c-_i.  counts (nullable)
+ * receives 2n bytes: c+ in [0, n), c- in [n, 2n).  out (nullable) receives
+ * fl32(scale * q[d_i]) at mask = 1 (others untouched) with scale =
+ * *scale_dev and q[d] = fl32(d / W) (NF_DECODE_SOFT) or sign(d)
+ * (NF_DECODE_MAJORITY).  No workspace.
+ */
+nf_status nf_ternary_reduce(const uint64_t* bits, int64_t bits_stride_words, int32_t W, int64_t n,
+                            const uint64_t* mask, const float* scale_dev, int32_t decode_mode,
+                            uint8_t* counts, float* out, void* stream);
+
+/*
  * Route decision from statistics (host, pure function; the rules the device
  * path applies).  Reasons as listed above; route by precedence P (not
  * admitted, or no eligible element) > forced L > F (veto, guard, non-finite,
@@ -204,6 +249,12 @@ nf_status nf_route_decide(const nf_worker_stats* stats_host, int32_t W, int64_t 
  * Always written: out[0..n), stats[0..W), *decision.  bits: written unless
  * the policy fixed the route before reading.  counts (nullable): written
  * when the route is L.
+ * With policy format NF_FORMAT_TERNARY the low-bit route carries the
+ * G-Ternary payload instead: pass 1 builds no sign payload; for route L the
+ * per-worker thresholds come from the statistics (nf_ternary_threshold with
+ * policy tau), a second read of the eligible elements writes the two planes
+ * into bits (2W rows, as nf_pack_ternary), and the count and decode of
+ * nf_ternary_reduce follow; counts (nullable) then receives 2n bytes.
  */
 nf_status nf_route_bucket(const float* grads, int64_t worker_stride, int32_t W, int64_t n,
                           const uint64_t* mask, const nf_route_policy* policy_host,
@@ -218,7 +269,8 @@ nf_status nf_route_bucket(const float* grads, int64_t worker_stride, int32_t W, 
  * of the mask, of the bitmap rows (from word b*bucket_n/64), of counts and of
  * out; nb = ceil(n_total / bucket_n).  bucket_n must be a multiple of 64
  * unless bucket_n >= n_total.  stats is [nb][W], decisions is [nb] (device).
- * Per bucket, the results equal those of nf_route_bucket on that bucket.
+ * Per bucket, the results equal those of nf_route_bucket on that bucket (with
+ * the ternary format, c- of bucket b starts at counts + n_total + b*bucket_n).
  */
 size_t nf_workspace_bytes_buckets(int32_t W, int64_t n_total, int64_t bucket_n);
 nf_status nf_route_buckets(const float* grads, int64_t worker_stride, int32_t W,

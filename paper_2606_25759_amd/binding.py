@@ -26,12 +26,14 @@ NF_REASON_NONFINITE, NF_REASON_ZERO_WORKER, NF_REASON_NORM_SPIKE, NF_REASON_FORC
 NF_DECODE_SOFT, NF_DECODE_MAJORITY = 0, 1
 NF_FP32_SUM, NF_FP32_MEAN = 0, 1
 NF_SEL_ROUTED, NF_SEL_ELIGIBLE, NF_SEL_ALL = 0, 1, 2
+NF_FORMAT_BINARY, NF_FORMAT_TERNARY = 0, 1
 
 # Exported names, in the order include/nf.h declares them.
 EXPORTS = ["nf_abi_version", "nf_last_error", "nf_mask_from_segments", "nf_workspace_bytes",
            "nf_bucket_health", "nf_pack_signs", "nf_fp32_reduce", "nf_signcount_reduce",
            "nf_route_decide", "nf_route_bucket", "nf_workspace_bytes_buckets", "nf_route_buckets",
-           "nf_set_phase_events", "nf_pass1_launches"]
+           "nf_set_phase_events", "nf_pass1_launches", "nf_ternary_threshold", "nf_pack_ternary",
+           "nf_ternary_reduce"]
 
 
 class nf_worker_stats(ctypes.Structure):
@@ -43,7 +45,7 @@ class nf_route_policy(ctypes.Structure):
     _fields_ = [("admitted", ctypes.c_int32), ("veto", ctypes.c_int32),
                 ("guard_ok", ctypes.c_int32), ("force_lowbit", ctypes.c_int32),
                 ("decode_mode", ctypes.c_int32), ("fp32_op", ctypes.c_int32),
-                ("kappa", ctypes.c_double)]
+                ("kappa", ctypes.c_double), ("format", ctypes.c_int32), ("tau", ctypes.c_float)]
 
 
 class nf_route_decision(ctypes.Structure):
@@ -101,6 +103,9 @@ def load(path=None):
                                             _P, _P, _P, _SZ, _P]),
         "nf_set_phase_events": (ctypes.c_int, [_P, _P, _P, _P]),
         "nf_pass1_launches": (_I64, [_I32, _I64, _I64]),
+        "nf_ternary_threshold": (ctypes.c_int, [_P, _I32, _I64, ctypes.c_float, _P]),
+        "nf_pack_ternary": (ctypes.c_int, [_P, _I64, _I32, _I64, _P, _P, _P, _I64, _P]),
+        "nf_ternary_reduce": (ctypes.c_int, [_P, _I64, _I32, _I64, _P, _P, _I32, _P, _P, _P]),
     }
     for name, (res, args) in sigs.items():
         fn = getattr(lib, name)
@@ -188,8 +193,9 @@ def nf_workspace_bytes_buckets(W, n_total, bucket_n):
 
 
 def policy(admitted=1, veto=0, guard_ok=1, force_lowbit=0, decode_mode=NF_DECODE_SOFT,
-           fp32_op=NF_FP32_SUM, kappa=4.0):
-    return nf_route_policy(admitted, veto, guard_ok, force_lowbit, decode_mode, fp32_op, kappa)
+           fp32_op=NF_FP32_SUM, kappa=4.0, format=NF_FORMAT_BINARY, tau=0.5):
+    return nf_route_policy(admitted, veto, guard_ok, force_lowbit, decode_mode, fp32_op, kappa, format,
+                           tau)
 
 
 def nf_route_decide(stats, n, n_eligible, pol=None):
@@ -235,6 +241,32 @@ def nf_signcount_reduce(bits, W, n, mask, scale, decode_mode, counts, out, strea
                                       _dev_ptr(scale, torch.float32, "scale"), decode_mode,
                                       _dev_ptr(counts, torch.uint8, "counts"),
                                       _dev_ptr(out, torch.float32, "out"), _stream(stream)))
+
+
+def nf_ternary_threshold(stats, n_eligible, tau):
+    """Host thresholds from a numpy STATS_DTYPE array; returns float32 [W]."""
+    st = np.ascontiguousarray(stats, dtype=STATS_DTYPE)
+    theta = np.zeros(len(st), dtype=np.float32)
+    _check(load().nf_ternary_threshold(st.ctypes.data, len(st), n_eligible, tau, theta.ctypes.data))
+    return theta
+
+
+def nf_pack_ternary(grads, n, mask, theta, bits, stream=None):
+    """bits: int64 device tensor of 2W rows (positive planes, then negative)."""
+    g, stride, W = _rows(grads)
+    b, bstride = _bits_rows(bits)
+    if bits.shape[0] < 2 * W:
+        raise ValueError("bits needs 2W rows")
+    _check(load().nf_pack_ternary(g, stride, W, n, _words(mask), _dev_ptr(theta, torch.float32, "theta"), b,
+                                  bstride, _stream(stream)))
+
+
+def nf_ternary_reduce(bits, W, n, mask, scale, decode_mode, counts, out, stream=None):
+    """counts (nullable): 2n uint8 (c+ then c-); out (nullable): n float32."""
+    b, bstride = _bits_rows(bits)
+    _check(load().nf_ternary_reduce(b, bstride, W, n, _words(mask), _dev_ptr(scale, torch.float32, "scale"),
+                                    decode_mode, _dev_ptr(counts, torch.uint8, "counts"),
+                                    _dev_ptr(out, torch.float32, "out"), _stream(stream)))
 
 
 def nf_route_bucket(grads, n, mask, pol, bits, counts, out, stats, decision, ws, stream=None):

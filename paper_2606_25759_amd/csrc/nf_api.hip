@@ -74,6 +74,10 @@ nf_status check_policy(const nf_route_policy* p) {
     return fail(NF_ERR_INVALID_ARG, "decode_mode=%d", p->decode_mode);
   if (p->fp32_op != NF_FP32_SUM && p->fp32_op != NF_FP32_MEAN)
     return fail(NF_ERR_INVALID_ARG, "fp32_op=%d", p->fp32_op);
+  if (p->format != NF_FORMAT_BINARY && p->format != NF_FORMAT_TERNARY)
+    return fail(NF_ERR_INVALID_ARG, "format=%d", p->format);
+  if (p->format == NF_FORMAT_TERNARY && !(p->tau >= 0.0f && p->tau - p->tau == 0.0f))
+    return fail(NF_ERR_INVALID_ARG, "tau must be finite and >= 0");
   return NF_OK;
 }
 
@@ -181,14 +185,41 @@ nf_status route_flat(const float* g, int64_t stride, int32_t W, int64_t n_total,
   // or guard-rejected (and not forced): then no sign payload is built and
   // pass 1 writes the FP32 sums at every position.
   const bool predecided = !pol->admitted || (!pol->force_lowbit && (pol->veto || !pol->guard_ok));
+  const bool ternary = pol->format == NF_FORMAT_TERNARY;
   if (!predecided) NF_TRY(check_bits(bits, bstride, n_total, W));
   hipStream_t s = static_cast<hipStream_t>(stream);
-  NF_TRY(run_pass1_decide(geo, g, stride, mask, predecided ? nullptr : bits, bstride, out,
+  // The G-Ternary payload needs each worker's threshold, known only once the
+  // bucket has been read: pass 1 then builds no sign payload.
+  NF_TRY(run_pass1_decide(geo, g, stride, mask, (predecided || ternary) ? nullptr : bits, bstride, out,
                           predecided ? nf::kSumsAll : nf::kSumsRouted, pol->fp32_op == NF_FP32_MEAN,
                           stats, dec, pol, ws, s, true));
   if (predecided || n_total == 0) {
     record_phase(3, s);
     return ok();
+  }
+  if (ternary) {
+    nf::TernArgs t;
+    memset(&t, 0, sizeof t);
+    t.g = g;
+    t.wstride = stride;
+    t.mask = mask;
+    t.bits = bits;
+    t.bstride = bstride;
+    t.dec = dec;
+    t.stats = stats;
+    t.cpos = counts;
+    t.cneg = counts ? counts + n_total : nullptr;
+    t.out = out;
+    t.tau = pol->tau;
+    t.n_total = n_total;
+    t.bucket_n = geo.bucket_n;
+    t.W = W;
+    t.decode_mode = pol->decode_mode;
+    t.bpb2 = geo.bpb2;
+    hipError_t e = nf::launch_ternary_pack(geo, t, s);
+    if (e != hipSuccess) return hip_fail(e, "ternary pack launch");
+    e = nf::launch_ternary_reduce(geo, t, s);
+    if (e != hipSuccess) return hip_fail(e, "ternary reduce launch");
   }
   nf::Pass2Args p = pass2_args(geo);
   p.bits = bits;
@@ -199,7 +230,7 @@ nf_status route_flat(const float* g, int64_t stride, int32_t W, int64_t n_total,
   p.dec = dec;
   p.counts = counts;
   p.out = out;
-  p.op = nf::kOpFromDecision;
+  p.op = ternary ? nf::kOpFallbackOnly : nf::kOpFromDecision;
   p.decode_mode = pol->decode_mode;
   p.mean = pol->fp32_op == NF_FP32_MEAN;
   hipError_t e = nf::launch_pass2(geo, p, s);
@@ -368,6 +399,77 @@ nf_status nf_signcount_reduce(const uint64_t* bits, int64_t bits_stride_words, i
   p.decode_mode = decode_mode;
   hipError_t e = nf::launch_pass2(geo, p, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "signcount launch");
+  return ok();
+}
+
+nf_status nf_ternary_threshold(const nf_worker_stats* stats_host, int32_t W, int64_t n_eligible,
+                               float tau, float* theta_host) {
+  if (W < 1 || W > 255) return fail(NF_ERR_INVALID_ARG, "W=%d outside [1, 255]", W);
+  if (n_eligible < 0) return fail(NF_ERR_INVALID_ARG, "n_eligible < 0");
+  if (!stats_host || !theta_host) return fail(NF_ERR_INVALID_ARG, "NULL stats or theta");
+  if (!(tau >= 0.0f && tau - tau == 0.0f)) return fail(NF_ERR_INVALID_ARG, "tau must be finite and >= 0");
+  for (int w = 0; w < W; ++w) theta_host[w] = nf::ternary_threshold(stats_host[w], n_eligible, tau);
+  return ok();
+}
+
+nf_status nf_pack_ternary(const float* grads, int64_t worker_stride, int32_t W, int64_t n,
+                          const uint64_t* mask, const float* theta_dev, uint64_t* bits,
+                          int64_t bits_stride_words, void* stream) {
+  NF_TRY(check_grads(grads, worker_stride, W, n));
+  NF_TRY(check_mask(mask, n));
+  NF_TRY(check_bits(bits, bits_stride_words, n, W));
+  if (n > 0 && !theta_dev) return fail(NF_ERR_INVALID_ARG, "theta_dev is NULL");
+  if (!aligned(theta_dev, 4)) return fail(NF_ERR_ALIGNMENT, "theta not 4-byte aligned");
+  if (n == 0) return ok();
+  const nf::Geometry geo = nf::make_geometry(W, n, n);
+  nf::TernArgs t;
+  memset(&t, 0, sizeof t);
+  t.g = grads;
+  t.wstride = worker_stride;
+  t.mask = mask;
+  t.bits = bits;
+  t.bstride = bits_stride_words;
+  t.theta = theta_dev;
+  t.n_total = n;
+  t.bucket_n = n;
+  t.W = W;
+  t.bpb2 = geo.bpb2;
+  hipError_t e = nf::launch_ternary_pack(geo, t, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "ternary pack launch");
+  return ok();
+}
+
+nf_status nf_ternary_reduce(const uint64_t* bits, int64_t bits_stride_words, int32_t W, int64_t n,
+                            const uint64_t* mask, const float* scale_dev, int32_t decode_mode,
+                            uint8_t* counts, float* out, void* stream) {
+  if (W < 1 || W > 255) return fail(NF_ERR_INVALID_ARG, "W=%d outside [1, 255]", W);
+  if (n < 0) return fail(NF_ERR_INVALID_ARG, "n < 0");
+  NF_TRY(check_bits(bits, bits_stride_words, n, W));
+  if (decode_mode != NF_DECODE_SOFT && decode_mode != NF_DECODE_MAJORITY)
+    return fail(NF_ERR_INVALID_ARG, "decode_mode=%d", decode_mode);
+  if (out) {
+    NF_TRY(check_mask(mask, n));
+    if (!scale_dev) return fail(NF_ERR_INVALID_ARG, "scale_dev is NULL");
+    if (!aligned(out, 4) || !aligned(scale_dev, 4)) return fail(NF_ERR_ALIGNMENT, "out/scale not 4-byte aligned");
+  }
+  if (n == 0 || (!out && !counts)) return ok();
+  const nf::Geometry geo = nf::make_geometry(W, n, n);
+  nf::TernArgs t;
+  memset(&t, 0, sizeof t);
+  t.mask = mask;
+  t.bits = const_cast<uint64_t*>(bits);
+  t.bstride = bits_stride_words;
+  t.scale = scale_dev;
+  t.cpos = counts;
+  t.cneg = counts ? counts + n : nullptr;
+  t.out = out;
+  t.n_total = n;
+  t.bucket_n = n;
+  t.W = W;
+  t.decode_mode = decode_mode;
+  t.bpb2 = geo.bpb2;
+  hipError_t e = nf::launch_ternary_reduce(geo, t, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "ternary reduce launch");
   return ok();
 }
 

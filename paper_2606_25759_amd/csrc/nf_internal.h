@@ -152,7 +152,29 @@ struct DecideArgs {
   int32_t W, slots, tile, G;
 };
 
-enum Pass2Op { kOpCountDecode = 0, kOpFp32 = 1, kOpFromDecision = 2 };
+// kOpFallbackOnly: route-driven, FP32 sums of the buckets routed F only.
+enum Pass2Op { kOpCountDecode = 0, kOpFp32 = 1, kOpFromDecision = 2, kOpFallbackOnly = 3 };
+
+// G-Ternary pack and count/decode.  Route-driven (dec != NULL): only the
+// buckets routed L, thresholds from stats and tau.  Standalone: one bucket,
+// thresholds theta[W] and scale *scale.
+struct TernArgs {
+  const float* g;
+  int64_t wstride;
+  const uint64_t* mask;
+  uint64_t* bits;  // 2W rows: positive planes 0..W-1, negative planes W..2W-1
+  int64_t bstride;
+  const nf_route_decision* dec;
+  const nf_worker_stats* stats;  // [bucket][W]
+  const float* theta;
+  const float* scale;
+  uint8_t* cpos;  // nullable
+  uint8_t* cneg;  // nullable
+  float* out;     // nullable
+  float tau;
+  int64_t n_total, bucket_n;
+  int32_t W, decode_mode, bpb2;
+};
 
 struct Pass2Args {
   const uint64_t* bits;
@@ -220,9 +242,26 @@ NF_HD inline void decide_from(const nf_worker_stats* st, int W, int64_t n, int64
   d->reserved = 0;
   d->n_eligible = ne;
   d->bytes_fp32 = 4.0 * (double)n;
+  // one bit (binary) or two planes (ternary) per eligible element
   d->bytes_route = route == NF_ROUTE_LOWBIT
-                       ? (double)ne / 8.0 + 4.0 + 4.0 * (double)(n - ne)
+                       ? (p.format == NF_FORMAT_TERNARY ? 2.0 : 1.0) * (double)ne / 8.0 + 4.0 +
+                             4.0 * (double)(n - ne)
                        : 4.0 * (double)n;
+}
+
+// G-Ternary write-side threshold: tau times the worker's mean |g| over
+// eligible elements, the mean rounded to FP32 first; 0 without eligible
+// elements.
+NF_HD inline float ternary_threshold(const nf_worker_stats& st, int64_t ne, float tau) {
+  if (ne <= 0) return 0.0f;
+  const float mean_abs = (float)(st.sum_abs_elig / (double)ne);
+  return tau * mean_abs;
+}
+
+// G-Ternary decode of the vote difference d = c+ - c- in [-W, W].
+NF_HD inline float decode_qt(int d, int W, int mode) {
+  if (mode == NF_DECODE_MAJORITY) return d > 0 ? 1.0f : (d < 0 ? -1.0f : 0.0f);
+  return (float)d / (float)W;
 }
 
 // Rank of worker w among the finite sums of squares (ties by index).
@@ -248,5 +287,7 @@ NF_HD inline float decode_q(int c, int W, int mode) {
 hipError_t launch_pass1(const Geometry& geo, const Pass1Args& a, hipStream_t s);
 hipError_t launch_decide(const Geometry& geo, const DecideArgs& a, hipStream_t s);
 hipError_t launch_pass2(const Geometry& geo, const Pass2Args& a, hipStream_t s);
+hipError_t launch_ternary_pack(const Geometry& geo, const TernArgs& a, hipStream_t s);
+hipError_t launch_ternary_reduce(const Geometry& geo, const TernArgs& a, hipStream_t s);
 
 }  // namespace nf

@@ -692,6 +692,52 @@ __device__ __forceinline__ FullAdd full_add(uint64_t a, uint64_t b, uint64_t c) 
   return FullAdd{t ^ c, (a & b) | (c & t)};
 }
 
+// Bit-sliced count of one bitmap word position over W rows (row w at
+// col[w * bstride]): P[b] holds bit b of each element's count, for the
+// nplanes planes that counts 0..W need.  Eight words at a time go through a
+// carry-save tree of full adders (Harley-Seal), the rest ripple in.
+__device__ __forceinline__ void count_column(const uint64_t* col, int64_t bstride, int W, bool valid,
+                                             int nplanes, uint64_t (&P)[8]) {
+#pragma unroll
+  for (int q = 0; q < 8; ++q) P[q] = 0;
+  int w = 0;
+  for (; w + 8 <= W; w += 8) {
+    uint64_t x[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[i] = valid ? col[(int64_t)(w + i) * bstride] : 0ull;
+    FullAdd f0 = full_add(P[0], x[0], x[1]);
+    FullAdd f1 = full_add(f0.sum, x[2], x[3]);
+    FullAdd f2 = full_add(P[1], f0.carry, f1.carry);
+    FullAdd f3 = full_add(f1.sum, x[4], x[5]);
+    FullAdd f4 = full_add(f3.sum, x[6], x[7]);
+    FullAdd f5 = full_add(f2.sum, f3.carry, f4.carry);
+    FullAdd f6 = full_add(P[2], f2.carry, f5.carry);
+    P[0] = f4.sum;
+    P[1] = f5.sum;
+    P[2] = f6.sum;
+    uint64_t c = f6.carry;  // weight 8
+#pragma unroll
+    for (int q = 3; q < 8; ++q) {
+      if (q < nplanes) {
+        const uint64_t t = P[q] & c;
+        P[q] ^= c;
+        c = t;
+      }
+    }
+  }
+  for (; w < W; ++w) {
+    uint64_t c = valid ? col[(int64_t)w * bstride] : 0ull;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      if (q < nplanes) {
+        const uint64_t t = P[q] & c;
+        P[q] ^= c;
+        c = t;
+      }
+    }
+  }
+}
+
 __global__ __launch_bounds__(kThreads2) void k_pass2(
     const uint64_t* __restrict__ bits, const float* __restrict__ g, const uint64_t* __restrict__ mask,
     const nf_route_decision* __restrict__ dec, const float* __restrict__ scale_p,
@@ -704,7 +750,11 @@ __global__ __launch_bounds__(kThreads2) void k_pass2(
   int op = a.op;
   int sel = a.select;
   float scale = 0.0f;
-  if (op == kOpFromDecision) {
+  if (op == kOpFallbackOnly) {
+    if (dec[b].route != NF_ROUTE_FALLBACK) return;  // whole block
+    op = kOpFp32;
+    sel = NF_SEL_ELIGIBLE;
+  } else if (op == kOpFromDecision) {
     const int route = dec[b].route;
     if (route == NF_ROUTE_PLAIN) return;  // whole block: pass 1 wrote every position
     if (route == NF_ROUTE_LOWBIT) {
@@ -735,46 +785,8 @@ __global__ __launch_bounds__(kThreads2) void k_pass2(
     if (op == kOpCountDecode) {
       // ---- bit-sliced counts, lane = word k0 + lane
       const bool valid = lane < nk;
-      const uint64_t* col = bits + wbase + k0 + lane;
       uint64_t P[8];
-#pragma unroll
-      for (int q = 0; q < 8; ++q) P[q] = 0;
-      int w = 0;
-      for (; w + 8 <= a.W; w += 8) {
-        uint64_t x[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) x[i] = valid ? col[(int64_t)(w + i) * a.bstride] : 0ull;
-        FullAdd f0 = full_add(P[0], x[0], x[1]);
-        FullAdd f1 = full_add(f0.sum, x[2], x[3]);
-        FullAdd f2 = full_add(P[1], f0.carry, f1.carry);
-        FullAdd f3 = full_add(f1.sum, x[4], x[5]);
-        FullAdd f4 = full_add(f3.sum, x[6], x[7]);
-        FullAdd f5 = full_add(f2.sum, f3.carry, f4.carry);
-        FullAdd f6 = full_add(P[2], f2.carry, f5.carry);
-        P[0] = f4.sum;
-        P[1] = f5.sum;
-        P[2] = f6.sum;
-        uint64_t c = f6.carry;  // weight 8
-#pragma unroll
-        for (int q = 3; q < 8; ++q) {
-          if (q < nplanes) {
-            const uint64_t t = P[q] & c;
-            P[q] ^= c;
-            c = t;
-          }
-        }
-      }
-      for (; w < a.W; ++w) {
-        uint64_t c = valid ? col[(int64_t)w * a.bstride] : 0ull;
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          if (q < nplanes) {
-            const uint64_t t = P[q] & c;
-            P[q] ^= c;
-            c = t;
-          }
-        }
-      }
+      count_column(bits + wbase + k0 + lane, a.bstride, a.W, valid, nplanes, P);
       const uint64_t mw = (valid && mask) ? mask[wbase + k0 + lane] : 0ull;
       // ---- transpose through LDS: record (word, half) holds the planes' and
       // the mask's 32-bit halves
@@ -888,6 +900,198 @@ __global__ __launch_bounds__(kThreads2) void k_pass2(
   }
 }
 
+// ---------------------------------------------------------------- G-Ternary
+//
+// Pack (write side): a wavefront takes 64 consecutive words of one worker
+// row.  Lane l loads element 64k + l of word k where it is eligible (256-byte
+// coalesced loads; words without an eligible element are not read); two
+// ballots give the word of each plane, which lane 0 parks in LDS, and the
+// 64 words of a plane leave in one coalesced 512-byte store.
+__global__ __launch_bounds__(kThreads2) void k_tpack(TernArgs a) {
+  __shared__ uint64_t park[4][2][64];
+  const int b = blockIdx.y;
+  if (a.dec && a.dec[b].route != NF_ROUTE_LOWBIT) return;  // whole block
+  const int64_t base = (int64_t)b * a.bucket_n;
+  const int64_t nbe = bucket_len(a.n_total, a.bucket_n, b);
+  const int64_t nwords = (nbe + 63) / 64;
+  const int64_t wbase = base / 64;
+  const int64_t items = (nwords + 63) / 64 * a.W;  // (64-word group, worker) pairs
+  const int v = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wavefront index, uniform
+  const int lane = threadIdx.x & 63;
+  uint64_t* ppos = park[v][0];
+  uint64_t* pneg = park[v][1];
+  for (int64_t it = (int64_t)blockIdx.x * 4 + v; it < items; it += (int64_t)a.bpb2 * 4) {
+    const int64_t grp = it / a.W;
+    const int w = (int)(it - grp * a.W);
+    const float th = a.dec ? ternary_threshold(a.stats[(int64_t)b * a.W + w], a.dec[b].n_eligible, a.tau)
+                           : a.theta[w];
+    const int64_t k0 = grp * 64;
+    const int nk = (int)((nwords - k0) < 64 ? (nwords - k0) : 64);
+    const float* row = a.g + (int64_t)w * a.wstride + base + k0 * 64 + lane;
+    for (int kb = 0; kb < nk; kb += 8) {
+      uint64_t mk[8];
+      float x[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int64_t k = k0 + kb + j;
+        uint64_t m = 0;
+        if (kb + j < nk) {
+          m = a.mask[wbase + k];
+          if (k == nwords - 1) m &= low_bits(nbe - k * 64);
+        }
+        mk[j] = m;
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        x[j] = ((mk[j] >> lane) & 1ull) ? __builtin_nontemporal_load(row + 64 * (kb + j)) : 0.0f;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const bool keep = !(__builtin_fabsf(x[j]) < th);  // gated to 0 below the threshold
+        const uint64_t pw = __ballot(keep && x[j] > 0.0f) & mk[j];
+        const uint64_t nw = __ballot(keep && x[j] < 0.0f) & mk[j];
+        if (lane == 0 && kb + j < nk) {
+          ppos[kb + j] = pw;
+          pneg[kb + j] = nw;
+        }
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    if (lane < nk) {
+      a.bits[(int64_t)w * a.bstride + wbase + k0 + lane] = ppos[lane];
+      a.bits[(int64_t)(a.W + w) * a.bstride + wbase + k0 + lane] = pneg[lane];
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+}
+
+// Count and decode (read side), as pass 2 with two counters: lane l counts
+// word k0 + l of the positive rows and of the negative rows; the planes of
+// both go through LDS so that each lane decodes four consecutive elements
+// (one nibble per plane, spread into four count bytes by a multiply) from
+// the difference of the two counts, d = c+ - c-, through a table of
+// fl32(scale * q[d]).
+constexpr int kRecT = 20;  // dwords per (word, half): 8 + 8 plane halves, mask half, pad
+
+__global__ __launch_bounds__(kThreads2) void k_tpass2(TernArgs a) {
+  __shared__ float tab[2 * 255 + 1];
+  __shared__ __align__(16) uint32_t rec[4][64 * 2 * kRecT];
+  const int b = blockIdx.y;
+  float scale = 0.0f;
+  if (a.dec) {
+    if (a.dec[b].route != NF_ROUTE_LOWBIT) return;  // whole block
+    scale = a.dec[b].scale;
+  } else if (a.out) {
+    scale = *a.scale;
+  }
+  if (a.out) {
+    for (int d = threadIdx.x; d <= 2 * a.W; d += kThreads2) tab[d] = scale * decode_qt(d - a.W, a.W, a.decode_mode);
+    __syncthreads();
+  }
+  const int64_t base = (int64_t)b * a.bucket_n;
+  const int64_t nbe = bucket_len(a.n_total, a.bucket_n, b);
+  const int64_t nwords = (nbe + 63) / 64;
+  const int64_t wbase = base / 64;
+  const int v = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wavefront index, uniform
+  const int lane = threadIdx.x & 63;
+  int nplanes = 1;
+  while ((1 << nplanes) <= a.W) ++nplanes;  // counts 0..W need nplanes bits
+  uint32_t* my = rec[v];
+  const bool c4 = a.cpos && a.cneg && ((reinterpret_cast<uintptr_t>(a.cpos + base) & 3) == 0) &&
+                  ((reinterpret_cast<uintptr_t>(a.cneg + base) & 3) == 0);
+  const bool o16 = a.out && ((reinterpret_cast<uintptr_t>(a.out + base) & 15) == 0);
+
+  for (int64_t ch = (int64_t)blockIdx.x * 4 + v; ch * 64 < nwords; ch += (int64_t)a.bpb2 * 4) {
+    const int64_t k0 = ch * 64;
+    const int nk = (int)((nwords - k0) < 64 ? (nwords - k0) : 64);
+    const bool valid = lane < nk;
+    uint64_t P[8], N[8];
+    count_column(a.bits + wbase + k0 + lane, a.bstride, a.W, valid, nplanes, P);
+    count_column(a.bits + (int64_t)a.W * a.bstride + wbase + k0 + lane, a.bstride, a.W, valid, nplanes, N);
+    const uint64_t mw = (valid && a.mask) ? a.mask[wbase + k0 + lane] : 0ull;
+    uint4* r0 = reinterpret_cast<uint4*>(my + (lane * 2) * kRecT);
+    uint4* r1 = reinterpret_cast<uint4*>(my + (lane * 2 + 1) * kRecT);
+    r0[0] = make_uint4((uint32_t)P[0], (uint32_t)P[1], (uint32_t)P[2], (uint32_t)P[3]);
+    r0[1] = make_uint4((uint32_t)P[4], (uint32_t)P[5], (uint32_t)P[6], (uint32_t)P[7]);
+    r0[2] = make_uint4((uint32_t)N[0], (uint32_t)N[1], (uint32_t)N[2], (uint32_t)N[3]);
+    r0[3] = make_uint4((uint32_t)N[4], (uint32_t)N[5], (uint32_t)N[6], (uint32_t)N[7]);
+    r0[4] = make_uint4((uint32_t)mw, 0u, 0u, 0u);
+    r1[0] = make_uint4((uint32_t)(P[0] >> 32), (uint32_t)(P[1] >> 32), (uint32_t)(P[2] >> 32), (uint32_t)(P[3] >> 32));
+    r1[1] = make_uint4((uint32_t)(P[4] >> 32), (uint32_t)(P[5] >> 32), (uint32_t)(P[6] >> 32), (uint32_t)(P[7] >> 32));
+    r1[2] = make_uint4((uint32_t)(N[0] >> 32), (uint32_t)(N[1] >> 32), (uint32_t)(N[2] >> 32), (uint32_t)(N[3] >> 32));
+    r1[3] = make_uint4((uint32_t)(N[4] >> 32), (uint32_t)(N[5] >> 32), (uint32_t)(N[6] >> 32), (uint32_t)(N[7] >> 32));
+    r1[4] = make_uint4((uint32_t)(mw >> 32), 0u, 0u, 0u);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    for (int grp = 0; grp * 4 < nk; ++grp) {
+      const int kk = grp * 4 + (lane >> 4);
+      const int shn = 4 * (lane & 7);
+      const uint4* r = reinterpret_cast<const uint4*>(my + (kk * 2 + ((lane >> 3) & 1)) * kRecT);
+      const uint4 p03 = r[0];
+      const uint4 p47 = r[1];
+      const uint4 n03 = r[2];
+      const uint4 n47 = r[3];
+      const uint32_t mnib = (r[4].x >> shn) & 15u;
+      auto spread = [&](uint32_t plane) { return (((plane >> shn) & 15u) * 0x00204081u) & 0x01010101u; };
+      uint32_t cp4 = spread(p03.x) | (spread(p03.y) << 1) | (spread(p03.z) << 2) | (spread(p03.w) << 3);
+      uint32_t cn4 = spread(n03.x) | (spread(n03.y) << 1) | (spread(n03.z) << 2) | (spread(n03.w) << 3);
+      if (nplanes > 4) {
+        cp4 |= (spread(p47.x) << 4) | (spread(p47.y) << 5) | (spread(p47.z) << 6) | (spread(p47.w) << 7);
+        cn4 |= (spread(n47.x) << 4) | (spread(n47.y) << 5) | (spread(n47.z) << 6) | (spread(n47.w) << 7);
+      }
+      const int64_t i0 = (k0 + grp * 4) * 64 + 4 * lane;  // first of my four elements in the bucket
+      if (kk >= nk || i0 >= nbe) continue;
+      auto value = [&](int e) {
+        return tab[(int)((cp4 >> (8 * e)) & 255u) - (int)((cn4 >> (8 * e)) & 255u) + a.W];
+      };
+      if (i0 + 3 < nbe) {
+        if (c4) {
+          *reinterpret_cast<uint32_t*>(a.cpos + base + i0) = cp4;
+          *reinterpret_cast<uint32_t*>(a.cneg + base + i0) = cn4;
+        } else if (a.cpos && a.cneg) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            a.cpos[base + i0 + e] = (uint8_t)(cp4 >> (8 * e));
+            a.cneg[base + i0 + e] = (uint8_t)(cn4 >> (8 * e));
+          }
+        }
+        if (a.out) {
+          if (o16 && mnib == 15u) {
+            float4 y;
+            y.x = value(0);
+            y.y = value(1);
+            y.z = value(2);
+            y.w = value(3);
+            *reinterpret_cast<float4*>(a.out + base + i0) = y;
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if ((mnib >> e) & 1u) a.out[base + i0 + e] = value(e);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          if (i0 + e < nbe) {
+            if (a.cpos && a.cneg) {
+              a.cpos[base + i0 + e] = (uint8_t)(cp4 >> (8 * e));
+              a.cneg[base + i0 + e] = (uint8_t)(cn4 >> (8 * e));
+            }
+            if (a.out && ((mnib >> e) & 1u)) a.out[base + i0 + e] = value(e);
+          }
+        }
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+}
+
 // --------------------------------------------------------------- launchers
 
 template <bool PACK>
@@ -941,6 +1145,16 @@ hipError_t launch_pass1(const Geometry& geo, const Pass1Args& a, hipStream_t s) 
 
 hipError_t launch_decide(const Geometry& geo, const DecideArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(k_decide, dim3((unsigned)geo.nb), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_ternary_pack(const Geometry& geo, const TernArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(k_tpack, dim3((unsigned)geo.bpb2, (unsigned)geo.nb), dim3(kThreads2), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_ternary_reduce(const Geometry& geo, const TernArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(k_tpass2, dim3((unsigned)geo.bpb2, (unsigned)geo.nb), dim3(kThreads2), 0, s, a);
   return hipGetLastError();
 }
 

@@ -46,10 +46,11 @@ def rel_close(a, b, tol=REL_TOL):
     b = np.asarray(b, np.float64)
     both_nan = np.isnan(a) & np.isnan(b)
     same_inf = np.isinf(a) & np.isinf(b) & (np.sign(a) == np.sign(b))
-    ok = both_nan | same_inf | (np.abs(a - b) <= tol * np.abs(b)) | (a == b)
-    return bool(np.all(ok)), (float(np.max(np.abs(a - b)[~(both_nan | same_inf)] /
-                                          np.maximum(np.abs(b[~(both_nan | same_inf)]), 1e-300)))
-                              if np.any(~(both_nan | same_inf)) else 0.0)
+    with np.errstate(invalid="ignore"):  # inf - inf where both are infinite: covered by same_inf
+        ok = both_nan | same_inf | (np.abs(a - b) <= tol * np.abs(b)) | (a == b)
+        return bool(np.all(ok)), (float(np.max(np.abs(a - b)[~(both_nan | same_inf)] /
+                                              np.maximum(np.abs(b[~(both_nan | same_inf)]), 1e-300)))
+                                  if np.any(~(both_nan | same_inf)) else 0.0)
 
 
 def check_stats(gpu_st, ref_st, what=""):
@@ -144,7 +145,7 @@ def oracle_bucket(g_host, mask_words, n, pol, b=0, bucket_n=None):
 def oracle_policy(pol):
     return nfo.policy(admitted=pol.admitted, veto=pol.veto, guard_ok=pol.guard_ok,
                       force_lowbit=pol.force_lowbit, decode_mode=pol.decode_mode,
-                      fp32_op=pol.fp32_op, kappa=pol.kappa)
+                      fp32_op=pol.fp32_op, kappa=pol.kappa, format=pol.format, tau=pol.tau)
 
 
 def check_route(res, g_host, mask_words, n, pol, bucket_n=None, with_counts=True, what="",

@@ -31,10 +31,10 @@ def test_exports_every_declared_function():
 
 
 def test_abi_version_and_struct_sizes():
-    assert nf.nf_abi_version() == 1
+    assert nf.nf_abi_version() == 2
     assert ctypes.sizeof(nf.nf_worker_stats) == 24 == nf.STATS_DTYPE.itemsize
     assert ctypes.sizeof(nf.nf_route_decision) == 40 == nf.DECISION_DTYPE.itemsize
-    assert ctypes.sizeof(nf.nf_route_policy) == 32
+    assert ctypes.sizeof(nf.nf_route_policy) == 40
 
 
 @pytest.mark.parametrize("n", [0, 1, 63, 64, 65, 1000, 100_003])
@@ -66,12 +66,27 @@ def test_route_decide_host_matches_oracle():
         ne = int(rng.integers(0, n + 1))
         kw = dict(admitted=int(rng.integers(0, 2)), veto=int(rng.integers(0, 2)),
                   guard_ok=int(rng.integers(0, 2)), force_lowbit=int(rng.integers(0, 2)),
-                  kappa=float(rng.choice([1.0, 2.0, 4.0, 3.5])))
+                  kappa=float(rng.choice([1.0, 2.0, 4.0, 3.5])), format=int(rng.integers(0, 2)))
         d = nf.nf_route_decide(st, n, ne, nf.policy(**kw))
         rd = nfo.decide(st, n, ne, nfo.policy(**kw))
         assert (d.route, d.reasons, d.n_eligible) == (rd.route, rd.reasons, rd.n_eligible), trial
         assert d.bytes_route == rd.bytes_route and d.bytes_fp32 == rd.bytes_fp32
         assert np.float32(d.scale) == np.float32(rd.scale)
+
+
+def test_ternary_threshold_host_matches_oracle():
+    rng = np.random.default_rng(6)
+    for trial in range(500):
+        W = int(rng.integers(1, 40))
+        st = np.zeros(W, dtype=nf.STATS_DTYPE)
+        st["sum_abs_elig"] = rng.random(W) * 10.0 ** float(rng.integers(-9, 3))
+        st["sum_abs_elig"][rng.random(W) < 0.1] = np.nan
+        ne = int(rng.integers(0, 10 ** 7))
+        tau = float(np.float32(rng.choice([0.0, 0.25, 0.5, 1.0, 3.0, rng.random() * 4])))
+        th = nf.nf_ternary_threshold(st, ne, tau)
+        want = np.array([nfo.ternary_threshold(st[w], ne, tau) for w in range(W)], dtype=np.float32)
+        na, nb = np.isnan(th), np.isnan(want)
+        assert np.array_equal(na, nb) and np.array_equal(th[~na].view(np.uint32), want[~nb].view(np.uint32)), trial
 
 
 def test_route_decide_worked_example():
@@ -119,6 +134,23 @@ def test_invalid_arguments_return_codes_without_launch():
     pol = nf.policy(decode_mode=5)
     assert lib.nf_route_bucket(fake, 640, 2, 640, fake, ctypes.byref(pol), fake, 10, None, fake, fake, fake,
                                ws, 1 << 24, None) == nf.NF_ERR_INVALID_ARG
+    pol = nf.policy(format=7)
+    assert lib.nf_route_bucket(fake, 640, 2, 640, fake, ctypes.byref(pol), fake, 10, None, fake, fake, fake,
+                               ws, 1 << 24, None) == nf.NF_ERR_INVALID_ARG
+    pol = nf.policy(format=nf.NF_FORMAT_TERNARY, tau=-1.0)
+    assert lib.nf_route_bucket(fake, 640, 2, 640, fake, ctypes.byref(pol), fake, 10, None, fake, fake, fake,
+                               ws, 1 << 24, None) == nf.NF_ERR_INVALID_ARG
+    pol = nf.policy(format=nf.NF_FORMAT_TERNARY, tau=float("nan"))
+    assert lib.nf_route_bucket(fake, 640, 2, 640, fake, ctypes.byref(pol), fake, 10, None, fake, fake, fake,
+                               ws, 1 << 24, None) == nf.NF_ERR_INVALID_ARG
+    # ternary components
+    assert lib.nf_pack_ternary(fake, 640, 2, 640, fake, None, fake, 10, None) == nf.NF_ERR_INVALID_ARG
+    assert lib.nf_pack_ternary(fake, 640, 2, 640, fake, P(0x1002), fake, 10, None) == nf.NF_ERR_ALIGNMENT
+    assert lib.nf_ternary_reduce(fake, 10, 2, 640, fake, None, 0, None, fake, None) == nf.NF_ERR_INVALID_ARG
+    assert lib.nf_ternary_reduce(fake, 10, 2, 640, fake, fake, 4, None, fake, None) == nf.NF_ERR_INVALID_ARG
+    th = (ctypes.c_float * 2)()
+    assert lib.nf_ternary_threshold(st_fake := (nf.nf_worker_stats * 2)(), 2, 10, ctypes.c_float(-0.5), th) == \
+        nf.NF_ERR_INVALID_ARG
     # bucket size not a multiple of 64
     pol = nf.policy()
     assert lib.nf_route_buckets(fake, 6400, 2, 6400, 100, fake, ctypes.byref(pol), fake, 100, None, fake,
