@@ -45,6 +45,9 @@ def parse():
                     choices=["tiny", "resnet50", "vitb16", "gpt1p3b", "stress"])
     ap.add_argument("--force-lowbit", action="store_true", help="guard disabled (forced low-bit)")
     ap.add_argument("--no-counts", action="store_true", help="do not write the uint8 counts")
+    ap.add_argument("--format", default="binary", choices=["binary", "ternary"],
+                    help="low-bit payload: G-Binary sign counts or G-Ternary two-plane counts")
+    ap.add_argument("--tau", type=float, default=0.5, help="G-Ternary gate (units of mean |g|)")
     ap.add_argument("--cpu-buckets", type=int, default=None,
                     help="buckets of the oracle's CPU sample (default: about 12 s of work)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -161,13 +164,15 @@ def main():
     off, ln, el = synth.mask_segments(lay)
     mask_h = nf.nf_mask_from_segments(off, ln, el, n)
     mask = torch.from_numpy(mask_h.view(np.int64)).to(dev)
-    bits = torch.empty((W, nw), dtype=torch.int64, device=dev)
-    counts = None if args.no_counts else torch.empty(n, dtype=torch.uint8, device=dev)
+    ternary = args.format == "ternary"
+    planes = 2 if ternary else 1  # G-Ternary: positive and negative plane per worker
+    bits = torch.empty((planes * W, nw), dtype=torch.int64, device=dev)
+    counts = None if args.no_counts else torch.empty(planes * n, dtype=torch.uint8, device=dev)
     out = torch.empty(n, dtype=torch.float32, device=dev)
     stats = torch.empty(nb * W * nf.STATS_BYTES, dtype=torch.uint8, device=dev)
     dec = torch.empty(nb * nf.DECISION_BYTES, dtype=torch.uint8, device=dev)
     ws = nf.empty_workspace(nf.nf_workspace_bytes_buckets(W, n, bn), dev)
-    pol = nf.policy(force_lowbit=int(args.force_lowbit))
+    pol = nf.policy(force_lowbit=int(args.force_lowbit), format=int(ternary), tau=args.tau)
     launches = nf.nf_pass1_launches(W, n, bn)
     torch.cuda.synchronize()
     print("[bench] inputs resident", file=sys.stderr, flush=True)
@@ -209,11 +214,17 @@ def main():
     nbs = np.array([min(bn, n - b * bn) for b in range(nb)], dtype=np.int64)
     ne = d["n_eligible"].astype(np.int64)
     nwb = (nbs + 63) // 64
-    # pass 1: gradients once, mask once, sign words out, FP32 sums at routed positions out
-    pass1_bytes = float((4 * W * nbs + 8 * nwb + 8 * W * nwb + 4 * (nbs - ne)).sum())
+    # pass 1: gradients once, mask once, sign words out (G-Binary only), FP32 sums at routed
+    # positions out
+    pass1_bytes = float((4 * W * nbs + 8 * nwb + (0 if ternary else 8 * W * nwb) + 4 * (nbs - ne)).sum())
     is_l, is_f = d["route"] == 0, d["route"] == 1
-    pass2_bytes = float(((8 * W * nwb + 8 * nwb + (0 if args.no_counts else nbs) + 4 * ne) * is_l).sum()
-                        + ((4 * W * ne + 8 * nwb + 4 * ne) * is_f).sum())
+    cbytes = 0 if args.no_counts else planes * nbs
+    if ternary:
+        # second read of the eligible elements, two planes out and back in, counts, decode
+        l_bytes = 4 * W * ne + 8 * nwb + 16 * W * nwb + 16 * W * nwb + 8 * nwb + cbytes + 4 * ne
+    else:
+        l_bytes = 8 * W * nwb + 8 * nwb + cbytes + 4 * ne
+    pass2_bytes = float((l_bytes * is_l).sum() + ((4 * W * ne + 8 * nwb + 4 * ne) * is_f).sum())
     value = lay.input_bytes() / (ms_per_step * 1e-3) / 1e9
     achieved = pass1_bytes / (pass1_ms * 1e-3) / 1e9
 
@@ -236,7 +247,7 @@ def main():
     if not args.no_cpu_baseline:
         import oracle as nfo
         k = args.cpu_buckets or max(1, min(nb, int(12e9 * 0.35 / (4 * W * min(bn, n)))))
-        opol = nfo.policy(force_lowbit=int(args.force_lowbit))
+        opol = nfo.policy(force_lowbit=int(args.force_lowbit), format=int(ternary), tau=args.tau)
         model, ncpu = host_cpu()
         old_aff = os.sched_getaffinity(0)
         core = min(old_aff)
@@ -248,13 +259,15 @@ def main():
                 gh = grads[:, a:e].contiguous().cpu().numpy()
                 mh = np.ascontiguousarray(mask_h[a // 64:(e + 63) // 64])
                 c0 = time.perf_counter()
-                ref = nfo.reduce_bucket(gh, mh, opol)
+                ref = (nfo.reduce_bucket_ternary if ternary else nfo.reduce_bucket)(gh, mh, opol)
                 t_cpu += time.perf_counter() - c0
                 nbytes += 4 * W * (e - a)
                 rd = ref["decision"]
                 ok &= int(d["route"][b]) == rd.route and int(d["reasons"][b]) == rd.reasons
-                ok &= bool(np.array_equal(bits[:, a // 64:(e + 63) // 64].cpu().numpy().view(np.uint64),
-                                          ref["bits"]))
+                if rd.route == 0 or not ternary:  # G-Ternary planes are built on route L only
+                    got = bits[:, a // 64:(e + 63) // 64].cpu().numpy().view(np.uint64)
+                    want = np.concatenate([ref["pos"], ref["neg"]]) if ternary else ref["bits"]
+                    ok &= bool(np.array_equal(got, want))
         finally:
             os.sched_setaffinity(0, old_aff)
         cpu = {"value": round(nbytes / t_cpu / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
@@ -281,7 +294,7 @@ def main():
         "config": {"workload": lay.name, "W": W, "n_total": n, "buckets": nb, "bucket_n": bn,
                    "eligible_frac": round(float(ne.sum()) / n, 4),
                    "policy": "forced low-bit" if args.force_lowbit else "admitted, guard ok",
-                   "counts_written": not args.no_counts},
+                   "format": args.format, "counts_written": not args.no_counts},
         "device_ms": {"mean": round(device_ms, 4), "median": round(dev_med, 4), "min": round(dev_min, 4)},
         "roofline": {"kernel": "k_pass1", "bound": "hbm", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),

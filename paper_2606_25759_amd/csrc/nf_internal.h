@@ -25,9 +25,12 @@ namespace nf {
 // takes one chunk and keeps the chunk's sign words in LDS until it ends.
 // Pass 1 runs as a sequence of launches of kEpochBlocks chunks each, so the
 // bitmap stores of a launch reach memory together at its end rather than
-// spread thinly through the gradient read stream (measured on MI355X: the
-// spread-out stores cost about 40% of the scan's time; launch-end bursts,
-// about 15%).
+// spread thinly through the gradient read stream.  Measured on MI355X:
+// writes mixed into a streaming read cost far more than their own bytes (a
+// 1/32 share of writes slows a plain 84 GB read by 35-45%); spread-out
+// stores cost about 40% of the scan's time, launch-end bursts about 15-20%.
+// One chunk per compute unit (256 on MI355X) per launch is the best epoch
+// measured (128: -30%, 192 and 384: -7%, 512: -4%, 1024: -7%).
 constexpr int kWaves = 16;
 constexpr int kThreads1 = kWaves * 64;
 constexpr int kStageFloats = 16384;      // 64 KiB of LDS
@@ -35,7 +38,7 @@ constexpr int kStageFloats = 16384;      // 64 KiB of LDS
 #define NF_BITS_WORDS 4096
 #endif
 #ifndef NF_EPOCH_BLOCKS
-#define NF_EPOCH_BLOCKS 512
+#define NF_EPOCH_BLOCKS 256
 #endif
 #ifndef NF_MAX_G
 #define NF_MAX_G 32
@@ -174,6 +177,9 @@ struct TernArgs {
   float tau;
   int64_t n_total, bucket_n;
   int32_t W, decode_mode, bpb2;
+  // pack geometry (filled by the pack launcher from the Geometry)
+  int64_t chunks_full, total_chunks;
+  int32_t nb, wg, eg, T, G;
 };
 
 struct Pass2Args {

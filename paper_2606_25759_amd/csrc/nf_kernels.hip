@@ -17,6 +17,9 @@
 
 namespace nf {
 
+// Four floats as one 16-byte vector (for vector nontemporal stores).
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
 __device__ __forceinline__ bool finite32(float x) {
   return (__float_as_uint(x) & 0x7f800000u) != 0x7f800000u;
 }
@@ -92,6 +95,13 @@ __device__ __forceinline__ void lanes_from_ballots(const uint64_t (&bb)[NW], uin
         : "=v"(lo), "=v"(hi)
         : "s"(l[0]), "s"(h[0]));
   }
+}
+
+// A wavefront-uniform 64-bit value held in a vector register, as a scalar.
+__device__ __forceinline__ uint64_t uniform64(uint64_t x) {
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(x >> 32));
+  return ((uint64_t)hi << 32) | lo;
 }
 
 // c + bit `lane` of the wavefront-uniform word (the word read as a lane mask).
@@ -679,9 +689,12 @@ __global__ __launch_bounds__(256) void k_decide(DecideArgs a) {
 // tree of full adders (Harley-Seal), the rest ripple in.  The planes are then
 // transposed through LDS so that lane j decodes element j of each word: its
 // count selects fl32(scale * q[c]) from an LDS table, and every store is a
-// coalesced 64- or 256-byte row.  Fallback (route F) and the standalone FP32
-// reduction add the workers in order at the selected positions instead.
+// coalesced 64- or 256-byte row, nontemporal (they are not read again here;
+// measured 4% faster than cached stores).  Fallback (route F) and the
+// standalone FP32 reduction add the workers in order at the selected
+// positions instead.
 constexpr int kRec = 12;  // dwords per (word, half) record: 8 planes, mask half, pad
+constexpr int kFp32Rows = 8;  // worker rows in flight in the FP32 sums
 
 struct FullAdd {
   uint64_t sum, carry;
@@ -827,19 +840,16 @@ __global__ __launch_bounds__(kThreads2) void k_pass2(
         if (kk >= nk || i0 >= nbe) continue;
         if (i0 + 3 < nbe) {
           if (c4) {
-            *reinterpret_cast<uint32_t*>(counts + base + i0) = cw4;
+            __builtin_nontemporal_store(cw4, reinterpret_cast<uint32_t*>(counts + base + i0));
           } else if (counts) {
 #pragma unroll
             for (int e = 0; e < 4; ++e) counts[base + i0 + e] = (uint8_t)(cw4 >> (8 * e));
           }
           if (out) {
             if (o16 && mnib == 15u) {
-              float4 y;
-              y.x = tab[cw4 & 255u];
-              y.y = tab[(cw4 >> 8) & 255u];
-              y.z = tab[(cw4 >> 16) & 255u];
-              y.w = tab[cw4 >> 24];
-              *reinterpret_cast<float4*>(out + base + i0) = y;
+              const f32x4 y = {tab[cw4 & 255u], tab[(cw4 >> 8) & 255u], tab[(cw4 >> 16) & 255u],
+                               tab[cw4 >> 24]};
+              __builtin_nontemporal_store(y, reinterpret_cast<f32x4*>(out + base + i0));
             } else {
 #pragma unroll
               for (int e = 0; e < 4; ++e)
@@ -860,39 +870,52 @@ __global__ __launch_bounds__(kThreads2) void k_pass2(
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     } else {
-      constexpr int K = 16;
-      for (int s0 = 0; s0 < nk; s0 += K) {
-        const int64_t kb = k0 + s0;
-        const int nks = (nk - s0) < K ? (nk - s0) : K;
-        float sacc[K];
-        uint64_t selw[K];
-#pragma unroll
-        for (int k = 0; k < K; ++k) {
-          uint64_t m = 0;
-          if (k < nks) {
-            const uint64_t mw = mask ? mask[wbase + kb + k] : ~0ull;
-            m = sel == NF_SEL_ALL ? ~0ull : (sel == NF_SEL_ELIGIBLE ? mw : ~mw);
-            m &= low_bits(nbe - (kb + k) * 64);
-          }
-          selw[k] = m;
-          sacc[k] = 0.0f;
+      // ---- FP32 sums: 256 elements (four words) per step; lane l takes
+      // elements 4l .. 4l + 3 with one 16-byte load per worker row, eight
+      // rows in flight at a time, and loads nothing when none of its four
+      // elements is selected.  Rows are 16-byte aligned and buckets start on
+      // 64-element boundaries, so every full group of four is aligned.
+      const bool o16 = (reinterpret_cast<uintptr_t>(out + base) & 15) == 0;
+      for (int grp = 0; grp * 4 < nk; ++grp) {
+        const int64_t e = (k0 + grp * 4) * 64 + 4 * lane;  // my first element in the bucket
+        const int64_t left = nbe - e;
+        const int cnt = left <= 0 ? 0 : (left >= 4 ? 4 : (int)left);
+        uint32_t pick = cnt ? (1u << cnt) - 1u : 0u;
+        if (sel != NF_SEL_ALL && cnt) {
+          const uint32_t nib = (uint32_t)(mask[wbase + e / 64] >> (e & 63)) & 15u;
+          pick &= sel == NF_SEL_ELIGIBLE ? nib : ~nib;
         }
-        for (int w = 0; w < a.W; ++w) {
-          const float* row = g + (int64_t)w * a.wstride + base + kb * 64 + lane;
+        if (!pick) continue;
+        const float* p = g + base + e;
+        if (cnt == 4) {
+          f32x4 acc = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p));
+          int w = 1;
+          for (; w + kFp32Rows <= a.W; w += kFp32Rows) {
+            f32x4 x[kFp32Rows];
 #pragma unroll
-          for (int k = 0; k < K; ++k) {
-            if ((selw[k] >> lane) & 1ull) {
-              const float x = __builtin_nontemporal_load(row + 64 * k);
-              sacc[k] = w == 0 ? x : sacc[k] + x;
-            }
+            for (int u = 0; u < kFp32Rows; ++u)
+              x[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p + (int64_t)(w + u) * a.wstride));
+#pragma unroll
+            for (int u = 0; u < kFp32Rows; ++u) acc = acc + x[u];
           }
-        }
+          for (; w < a.W; ++w)
+            acc = acc + __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p + (int64_t)w * a.wstride));
+          if (a.mean) acc = acc / (float)a.W;
+          if (pick == 15u && o16) {
+            __builtin_nontemporal_store(acc, reinterpret_cast<f32x4*>(out + base + e));
+          } else {
 #pragma unroll
-        for (int k = 0; k < K; ++k) {
-          if ((selw[k] >> lane) & 1ull) {
-            float y = sacc[k];
+            for (int c = 0; c < 4; ++c)
+              if ((pick >> c) & 1u) out[base + e + c] = acc[c];
+          }
+        } else {
+          // the bucket's last, partial group of four
+          for (int c = 0; c < cnt; ++c) {
+            if (!((pick >> c) & 1u)) continue;
+            float y = p[c];
+            for (int w = 1; w < a.W; ++w) y = y + p[(int64_t)w * a.wstride + c];
             if (a.mean) y = y / (float)a.W;
-            out[base + (kb + k) * 64 + lane] = y;
+            out[base + e + c] = y;
           }
         }
       }
@@ -902,69 +925,169 @@ __global__ __launch_bounds__(kThreads2) void k_pass2(
 
 // ---------------------------------------------------------------- G-Ternary
 //
-// Pack (write side): a wavefront takes 64 consecutive words of one worker
-// row.  Lane l loads element 64k + l of word k where it is eligible (256-byte
-// coalesced loads; words without an eligible element are not read); two
-// ballots give the word of each plane, which lane 0 parks in LDS, and the
-// 64 words of a plane leave in one coalesced 512-byte store.
-__global__ __launch_bounds__(kThreads2) void k_tpack(TernArgs a) {
-  __shared__ uint64_t park[4][2][64];
-  const int b = blockIdx.y;
-  if (a.dec && a.dec[b].route != NF_ROUTE_LOWBIT) return;  // whole block
+// Pack (write side), laid out as pass 1: a block takes one chunk (G tiles of
+// one bucket) and wavefront v serves worker group v % WG and element group
+// v / WG; lane l loads element 64k + l of word k, so the ballots of
+// "eligible, not gated, g > 0" and "eligible, not gated, g < 0" are the
+// two planes' words.  The next tile's loads (and mask words) are in flight
+// while one tile is examined.  The chunk's words of both planes stay in LDS
+// and leave at its end as coalesced rows; launches of kEpochBlocks chunks
+// bring the plane stores of a launch together, as in pass 1.
+template <int WPW>
+__global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <= 2 ? 8 : 4, WPW <= 2 ? 8 : 4))) void k_tpack(
+    TernArgs a, int64_t q0) {
+  constexpr int NW = pass1_words(WPW);
+  constexpr int NX = WPW * NW;
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int64_t q = q0 + blockIdx.x;  // this block's chunk
+  if (q >= a.total_chunks) return;     // whole block
+  int b;
+  int64_t c;
+  if (q < (int64_t)(a.nb - 1) * a.chunks_full) {
+    b = (int)(q / a.chunks_full);
+    c = q - (int64_t)b * a.chunks_full;
+  } else {
+    b = a.nb - 1;
+    c = q - (int64_t)b * a.chunks_full;
+  }
+  if (a.dec && a.dec[b].route != NF_ROUTE_LOWBIT) return;  // whole block: no planes
   const int64_t base = (int64_t)b * a.bucket_n;
   const int64_t nbe = bucket_len(a.n_total, a.bucket_n, b);
-  const int64_t nwords = (nbe + 63) / 64;
-  const int64_t wbase = base / 64;
-  const int64_t items = (nwords + 63) / 64 * a.W;  // (64-word group, worker) pairs
   const int v = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wavefront index, uniform
   const int lane = threadIdx.x & 63;
-  uint64_t* ppos = park[v][0];
-  uint64_t* pneg = park[v][1];
-  for (int64_t it = (int64_t)blockIdx.x * 4 + v; it < items; it += (int64_t)a.bpb2 * 4) {
-    const int64_t grp = it / a.W;
-    const int w = (int)(it - grp * a.W);
-    const float th = a.dec ? ternary_threshold(a.stats[(int64_t)b * a.W + w], a.dec[b].n_eligible, a.tau)
-                           : a.theta[w];
-    const int64_t k0 = grp * 64;
-    const int nk = (int)((nwords - k0) < 64 ? (nwords - k0) : 64);
-    const float* row = a.g + (int64_t)w * a.wstride + base + k0 * 64 + lane;
-    for (int kb = 0; kb < nk; kb += 8) {
-      uint64_t mk[8];
-      float x[8];
+  const int wg = v % a.wg;
+  const int eg = v / a.wg;
+  const bool active = eg < a.eg;
+  const int T = a.T;
+  const int tile = a.eg * T;
+  const int64_t ntiles = (nbe + tile - 1) / tile;
+  const int64_t tb = c * a.G;
+  const int64_t te = (tb + a.G < ntiles) ? tb + a.G : ntiles;
+  const int64_t te_full = (te * tile <= nbe) ? te : te - 1;  // tiles [tb, te_full) are full
+  const int cw = a.G * a.eg * NW;                             // words per worker row and chunk
+  uint64_t* ppos = reinterpret_cast<uint64_t*>(smem);
+  uint64_t* pneg = ppos + (size_t)a.W * cw;
+
+  float th[WPW];
+  const float* rp[WPW];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int64_t k = k0 + kb + j;
-        uint64_t m = 0;
-        if (kb + j < nk) {
-          m = a.mask[wbase + k];
-          if (k == nwords - 1) m &= low_bits(nbe - k * 64);
-        }
-        mk[j] = m;
-      }
+  for (int j = 0; j < WPW; ++j) {
+    const int w = wg + j * a.wg;
+    const int wl = w < a.W ? w : wg;
+    th[j] = a.dec ? ternary_threshold(a.stats[(int64_t)b * a.W + wl], a.dec[b].n_eligible, a.tau)
+                  : a.theta[wl];
+    rp[j] = a.g + (int64_t)wl * a.wstride + base + (int64_t)eg * T + lane;
+  }
+  const uint64_t* mbase = a.mask + base / 64 + (int64_t)eg * (T / 64);
+  // The first NW words of the bucket's first tile (full whenever any tile of
+  // this chunk is): read by loads whose values are not needed.
+  const float* dp = a.g + (int64_t)wg * a.wstride + base + lane;
+  const uint64_t* dm = a.mask + base / 64;
+
+  // Loads of a full tile (or, for an idle wavefront or a tile past the full
+  // ones, of the bucket's first words).
+  auto issue = [&](int64_t tt, float (&X)[NX], uint64_t (&M)[NW]) {
+    const bool ok = active && tt < te_full;
+    const int64_t o = tt * tile;
 #pragma unroll
-      for (int j = 0; j < 8; ++j)
-        x[j] = ((mk[j] >> lane) & 1ull) ? __builtin_nontemporal_load(row + 64 * (kb + j)) : 0.0f;
+    for (int j = 0; j < WPW; ++j) {
+      const float* row = ok ? rp[j] + o : dp;
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const bool keep = !(__builtin_fabsf(x[j]) < th);  // gated to 0 below the threshold
-        const uint64_t pw = __ballot(keep && x[j] > 0.0f) & mk[j];
-        const uint64_t nw = __ballot(keep && x[j] < 0.0f) & mk[j];
-        if (lane == 0 && kb + j < nk) {
-          ppos[kb + j] = pw;
-          pneg[kb + j] = nw;
-        }
-      }
+      for (int k = 0; k < NW; ++k) X[j * NW + k] = __builtin_nontemporal_load(row + 64 * k);
     }
+    const uint64_t* mrow = ok ? mbase + o / 64 : dm;
+#pragma unroll
+    for (int k = 0; k < NW; ++k) M[k] = uniform64(mrow[k]);
+  };
+  auto body = [&](int64_t t, const float (&X)[NX], const uint64_t (&M)[NW]) {
+    const int ti = (int)(t - tb);
+#pragma unroll
+    for (int j = 0; j < WPW; ++j) {
+      const int w = wg + j * a.wg;
+      if (j > 0 && w >= a.W) continue;
+      uint64_t pb[NW], nb[NW];
+#pragma unroll
+      for (int k = 0; k < NW; ++k) {
+        const float x = X[j * NW + k];
+        const bool keep = !(__builtin_fabsf(x) < th[j]);  // gated to 0 below the threshold
+        pb[k] = __ballot(keep && x > 0.0f) & M[k];
+        nb[k] = __ballot(keep && x < 0.0f) & M[k];
+      }
+      uint32_t lo, hi;
+      const int at = w * cw + (ti * a.eg + eg) * NW + lane;
+      lanes_from_ballots<NW>(pb, lo, hi);
+      if (lane < NW) ppos[at] = ((uint64_t)hi << 32) | lo;
+      lanes_from_ballots<NW>(nb, lo, hi);
+      if (lane < NW) pneg[at] = ((uint64_t)hi << 32) | lo;
+    }
+  };
+  auto consume = [&](const float (&X)[NX]) {
+#pragma unroll
+    for (int k = 0; k < NX; ++k) asm volatile("" ::"v"(X[k]));
+  };
+
+  float xa[NX], xb[NX];
+  uint64_t ma[NW], mb[NW];
+  int64_t t = tb;
+  if (te_full > tb) {
+    issue(tb, xa, ma);
+    // Pairs of full tiles with the next one in flight, then the odd one.
+    for (int64_t p = (te_full - tb) >> 1; p > 0; --p, t += 2) {
+      issue(t + 1, xb, mb);
+      if (active) body(t, xa, ma);
+      issue(t + 2, xa, ma);
+      if (active) body(t + 1, xb, mb);
+    }
+    if ((te_full - tb) & 1) {
+      if (active) body(t, xa, ma);
+      ++t;
+    } else {
+      consume(xa);
+    }
+  }
+  if (t < te && active) {
+    // The bucket's last, partial tile: loads and mask bits stop at its end.
+    const int64_t e0 = t * tile + (int64_t)eg * T;
+    const int64_t c64 = nbe - e0;
+    const int cnt = (int)(c64 < 0 ? 0 : (c64 > T ? T : c64));
+#pragma unroll
+    for (int j = 0; j < WPW; ++j)
+#pragma unroll
+      for (int k = 0; k < NW; ++k)
+        xb[j * NW + k] = (64 * k + lane < cnt) ? __builtin_nontemporal_load(rp[j] + t * tile + 64 * k) : 0.0f;
+#pragma unroll
+    for (int k = 0; k < NW; ++k)
+      mb[k] = 64 * k < cnt ? uniform64(mbase[t * (tile / 64) + k] & low_bits(cnt - 64 * k)) : 0ull;
+    body(t, xb, mb);
+  }
+
+  // The chunk's words of both planes, row by row.
+  const int64_t e_beg = tb * tile;
+  const int64_t e_end = (te * tile < nbe) ? te * tile : nbe;
+  const int valid = te > tb ? (int)((e_end - e_beg + 63) / 64) : 0;
+  const int64_t gw0 = (base + e_beg) / 64;
+  if (a.eg == 1) {
+    // each worker's words were written by its own wavefront only
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    if (lane < nk) {
-      a.bits[(int64_t)w * a.bstride + wbase + k0 + lane] = ppos[lane];
-      a.bits[(int64_t)(a.W + w) * a.bstride + wbase + k0 + lane] = pneg[lane];
+#pragma unroll
+    for (int j = 0; j < WPW; ++j) {
+      const int w = wg + j * a.wg;
+      if (w >= a.W) break;
+      for (int o = lane; o < valid; o += 64) {
+        a.bits[(int64_t)w * a.bstride + gw0 + o] = ppos[w * cw + o];
+        a.bits[(int64_t)(a.W + w) * a.bstride + gw0 + o] = pneg[w * cw + o];
+      }
     }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    return;
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < a.W * valid; i += kThreads1) {
+    const int w = i / valid;
+    const int o = i - w * valid;
+    a.bits[(int64_t)w * a.bstride + gw0 + o] = ppos[w * cw + o];
+    a.bits[(int64_t)(a.W + w) * a.bstride + gw0 + o] = pneg[w * cw + o];
   }
 }
 
@@ -1050,8 +1173,8 @@ __global__ __launch_bounds__(kThreads2) void k_tpass2(TernArgs a) {
       };
       if (i0 + 3 < nbe) {
         if (c4) {
-          *reinterpret_cast<uint32_t*>(a.cpos + base + i0) = cp4;
-          *reinterpret_cast<uint32_t*>(a.cneg + base + i0) = cn4;
+          __builtin_nontemporal_store(cp4, reinterpret_cast<uint32_t*>(a.cpos + base + i0));
+          __builtin_nontemporal_store(cn4, reinterpret_cast<uint32_t*>(a.cneg + base + i0));
         } else if (a.cpos && a.cneg) {
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
@@ -1061,12 +1184,8 @@ __global__ __launch_bounds__(kThreads2) void k_tpass2(TernArgs a) {
         }
         if (a.out) {
           if (o16 && mnib == 15u) {
-            float4 y;
-            y.x = value(0);
-            y.y = value(1);
-            y.z = value(2);
-            y.w = value(3);
-            *reinterpret_cast<float4*>(a.out + base + i0) = y;
+            const f32x4 y = {value(0), value(1), value(2), value(3)};
+            __builtin_nontemporal_store(y, reinterpret_cast<f32x4*>(a.out + base + i0));
           } else {
 #pragma unroll
             for (int e = 0; e < 4; ++e)
@@ -1148,9 +1267,36 @@ hipError_t launch_decide(const Geometry& geo, const DecideArgs& a, hipStream_t s
   return hipGetLastError();
 }
 
-hipError_t launch_ternary_pack(const Geometry& geo, const TernArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(k_tpack, dim3((unsigned)geo.bpb2, (unsigned)geo.nb), dim3(kThreads2), 0, s, a);
-  return hipGetLastError();
+hipError_t launch_ternary_pack(const Geometry& geo, const TernArgs& a0, hipStream_t s) {
+  TernArgs a = a0;
+  a.chunks_full = geo.chunks_full;
+  a.total_chunks = geo.total_chunks;
+  a.nb = (int32_t)geo.nb;
+  a.wg = geo.wg;
+  a.eg = geo.eg;
+  a.T = geo.T;
+  a.G = geo.G;
+  // Both planes of a chunk: 2 * W * G * EG * (T / 64) words, at most 64 KiB.
+  const size_t smem = 2 * (size_t)geo.W * geo.G * geo.eg * pass1_words(geo.wpw) * sizeof(uint64_t);
+  if (smem > 65536) return hipErrorInvalidValue;
+  // No chunk shares state with another, so every launch after the first may
+  // start while the one before drains.
+  for (int64_t q0 = 0; q0 < geo.total_chunks; q0 += kEpochBlocks) {
+    const int64_t left = geo.total_chunks - q0;
+    const dim3 grid((unsigned)(left < kEpochBlocks ? left : kEpochBlocks));
+    const uint32_t fl = q0 > 0 ? hipExtAnyOrderLaunch : 0u;
+    switch (geo.wpw) {
+      case 1: hipExtLaunchKernelGGL((k_tpack<1>), grid, dim3(kThreads1), smem, s, nullptr, nullptr, fl, a, q0); break;
+      case 2: hipExtLaunchKernelGGL((k_tpack<2>), grid, dim3(kThreads1), smem, s, nullptr, nullptr, fl, a, q0); break;
+      case 4: hipExtLaunchKernelGGL((k_tpack<4>), grid, dim3(kThreads1), smem, s, nullptr, nullptr, fl, a, q0); break;
+      case 8: hipExtLaunchKernelGGL((k_tpack<8>), grid, dim3(kThreads1), smem, s, nullptr, nullptr, fl, a, q0); break;
+      case 16: hipExtLaunchKernelGGL((k_tpack<16>), grid, dim3(kThreads1), smem, s, nullptr, nullptr, fl, a, q0); break;
+      default: return hipErrorInvalidValue;
+    }
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 hipError_t launch_ternary_reduce(const Geometry& geo, const TernArgs& a, hipStream_t s) {
