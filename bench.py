@@ -54,6 +54,8 @@ def parse():
     ap.add_argument("--no-probe", action="store_true", help="skip the streaming-read reference")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run the copy kernel of known traffic (counter calibration)")
+    ap.add_argument("--contrast", action="store_true",
+                    help="only time hierarchical vs stock vs direct sign counting (one JSON line per shape)")
     return ap.parse_args()
 
 
@@ -133,6 +135,70 @@ def calibrate_copy():
     return 0
 
 
+# (nodes, GPUs per node, elements): the paper's local-count logical buckets (8 workers x 131K and
+# x 524K elements, 2 nodes x 4 GPUs), and one 25 MiB bucket at 4 x 4 and 8 x 8 workers.
+CONTRAST_SHAPES = [(2, 4, 131_072), (2, 4, 524_288), (4, 4, 6_553_600), (8, 8, 6_553_600)]
+# Context only (another machine): mean local-count route times of the paper's reducer check on
+# 2 nodes x 4 A100 (its Table 9): 8 x 131K -> 260 us, 8 x 524K -> 570 us.
+PAPER_LOCAL_COUNT_US = {131_072: 260.0, 524_288: 570.0}
+
+
+def contrast(reps=50):
+    """Kernel time of three ways to turn W sign bitmaps into counts and the decoded aggregate:
+    direct (one bit-sliced count over all W rows), hierarchical (node-local partial counts over
+    each node's P rows, then the partial-count sum and decode), and stock (every one of the W
+    workers counts all W rows and decodes itself: W replicas)."""
+    import torch
+    import paper_2606_25759_amd as nf
+
+    dev = torch.device("cuda:0")
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(11)
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) * 1e3 / reps  # us per call
+
+    for nodes, per, n in CONTRAST_SHAPES:
+        W = nodes * per
+        nw = (n + 63) // 64
+        bits = torch.randint(-2 ** 62, 2 ** 62, (W, nw), dtype=torch.int64, device=dev, generator=gen)
+        mask = torch.full((nw,), -1, dtype=torch.int64, device=dev)
+        scale = torch.full((1,), 1e-3, dtype=torch.float32, device=dev)
+        counts = torch.empty(n, dtype=torch.uint8, device=dev)
+        out = torch.empty(n, dtype=torch.float32, device=dev)
+        stride = (n + 15) // 16 * 16
+        partial = torch.empty((nodes, stride), dtype=torch.uint8, device=dev)
+        sc = torch.empty(W * stride, dtype=torch.uint8, device=dev)
+        so = torch.empty(W * stride, dtype=torch.float32, device=dev)
+        t_direct = timed(lambda: nf.nf_signcount_reduce(bits, W, n, mask, scale, 0, counts, out))
+        t_local = timed(lambda: nf.nf_partial_counts(bits, W, per, n, partial))
+        t_exch = timed(lambda: nf.nf_partial_count_reduce(partial, W, n, mask, scale, 0, counts, out))
+        t_hier = timed(lambda: (nf.nf_partial_counts(bits, W, per, n, partial),
+                                nf.nf_partial_count_reduce(partial, W, n, mask, scale, 0, counts, out)))
+        t_stock = timed(lambda: nf.nf_stock_signcount(bits, W, n, mask, scale, 0, W, sc, so, stride))
+        torch.cuda.synchronize()
+        ok = bool(torch.equal(sc[:n], counts))
+        rec = {"metric": "sign-count kernel time, hierarchical vs stock (one GPU)", "unit": "us",
+               "config": {"nodes": nodes, "gpus_per_node": per, "W": W, "n": n},
+               "direct_us": round(t_direct, 2), "hier_local_us": round(t_local, 2),
+               "hier_exchange_return_us": round(t_exch, 2), "hier_total_us": round(t_hier, 2),
+               "stock_total_us": round(t_stock, 2), "stock_per_worker_us": round(t_stock / W, 2),
+               "stock_over_hier": round(t_stock / t_hier, 2), "replica_parity": "ok" if ok else "MISMATCH",
+               "bits_read_gb_direct": round(8 * W * nw / 1e9, 4),
+               "paper_local_count_us_a100": PAPER_LOCAL_COUNT_US.get(n) if W == 8 else None}
+        print(json.dumps(rec), flush=True)
+        del bits, sc, so, partial
+    return 0
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -148,6 +214,8 @@ def main():
     torch.cuda.init()
     if args.calibrate_copy:
         return calibrate_copy()
+    if args.contrast:
+        return contrast()
 
     import paper_2606_25759_amd as nf
     import synth

@@ -190,6 +190,49 @@ nf_status nf_signcount_reduce(const uint64_t* bits, int64_t bits_stride_words, i
                               int32_t decode_mode, uint8_t* counts, float* out, void* stream);
 
 /*
+ * Node-local counting of the hierarchical sign-count reducer (§6.1: counting
+ * at the node, then an exchange of partial counts between nodes, then the
+ * aggregate's return; §6.3 contrasts this with stock packed-sign transport,
+ * where every worker counts every stream itself).  The W rows of bits form
+ * G = W / P groups of P consecutive workers, a group standing for one node's
+ * P GPUs.  partial[g][i] = the number of rows of group g whose bit i is set,
+ * in [0, P]: G rows of n bytes, row g at partial + g * partial_stride
+ * (device).  Requires 1 <= P <= W, W a multiple of P, partial_stride >= n.
+ * The sum over g of partial[g][i] is the count c_i of nf_signcount_reduce.
+ * No workspace.
+ */
+nf_status nf_partial_counts(const uint64_t* bits, int64_t bits_stride_words, int32_t W, int32_t P,
+                            int64_t n, uint8_t* partial, int64_t partial_stride, void* stream);
+
+/*
+ * Partial-count exchange and aggregate return of the hierarchical reducer
+ * (§6.1), on one device: c_i = sum of the G rows of partial (row g at
+ * partial + g * partial_stride; G divides W), then counts (nullable, n
+ * bytes) and out (nullable, at mask = 1) exactly as nf_signcount_reduce with
+ * W workers, scale *scale_dev and decode_mode.  partial must be 16-byte
+ * aligned and partial_stride a multiple of 16 (NF_ERR_ALIGNMENT).  No
+ * workspace.
+ */
+nf_status nf_partial_count_reduce(const uint8_t* partial, int64_t partial_stride, int32_t G,
+                                  int32_t W, int64_t n, const uint64_t* mask,
+                                  const float* scale_dev, int32_t decode_mode, uint8_t* counts,
+                                  float* out, void* stream);
+
+/*
+ * Stock packed-sign baseline (§6.3): after an all-gather of the packed signs,
+ * every worker counts all W rows and decodes the aggregate itself.  On one
+ * device: `replicas` (1..65535) independent count-and-decode passes of
+ * nf_signcount_reduce, replica r writing counts + r * replica_stride
+ * (nullable) and out + r * replica_stride (nullable; at mask = 1);
+ * replica_stride >= n elements.  Every replica equals nf_signcount_reduce's
+ * result.  No workspace.
+ */
+nf_status nf_stock_signcount(const uint64_t* bits, int64_t bits_stride_words, int32_t W, int64_t n,
+                             const uint64_t* mask, const float* scale_dev, int32_t decode_mode,
+                             int32_t replicas, uint8_t* counts, float* out, int64_t replica_stride,
+                             void* stream);
+
+/*
  * G-Ternary write-side threshold (§2.2's zero gating, applied before
  * aggregation; host, pure function): for each worker w,
  * theta[w] = fl32(tau * fl32(stats[w].sum_abs_elig / n_eligible)), i.e. tau

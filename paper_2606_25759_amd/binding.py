@@ -33,7 +33,7 @@ EXPORTS = ["nf_abi_version", "nf_last_error", "nf_mask_from_segments", "nf_works
            "nf_bucket_health", "nf_pack_signs", "nf_fp32_reduce", "nf_signcount_reduce",
            "nf_route_decide", "nf_route_bucket", "nf_workspace_bytes_buckets", "nf_route_buckets",
            "nf_set_phase_events", "nf_pass1_launches", "nf_ternary_threshold", "nf_pack_ternary",
-           "nf_ternary_reduce"]
+           "nf_ternary_reduce", "nf_partial_counts", "nf_partial_count_reduce", "nf_stock_signcount"]
 
 
 class nf_worker_stats(ctypes.Structure):
@@ -106,6 +106,9 @@ def load(path=None):
         "nf_ternary_threshold": (ctypes.c_int, [_P, _I32, _I64, ctypes.c_float, _P]),
         "nf_pack_ternary": (ctypes.c_int, [_P, _I64, _I32, _I64, _P, _P, _P, _I64, _P]),
         "nf_ternary_reduce": (ctypes.c_int, [_P, _I64, _I32, _I64, _P, _P, _I32, _P, _P, _P]),
+        "nf_partial_counts": (ctypes.c_int, [_P, _I64, _I32, _I32, _I64, _P, _I64, _P]),
+        "nf_partial_count_reduce": (ctypes.c_int, [_P, _I64, _I32, _I32, _I64, _P, _P, _I32, _P, _P, _P]),
+        "nf_stock_signcount": (ctypes.c_int, [_P, _I64, _I32, _I64, _P, _P, _I32, _I32, _P, _P, _I64, _P]),
     }
     for name, (res, args) in sigs.items():
         fn = getattr(lib, name)
@@ -241,6 +244,35 @@ def nf_signcount_reduce(bits, W, n, mask, scale, decode_mode, counts, out, strea
                                       _dev_ptr(scale, torch.float32, "scale"), decode_mode,
                                       _dev_ptr(counts, torch.uint8, "counts"),
                                       _dev_ptr(out, torch.float32, "out"), _stream(stream)))
+
+
+def nf_partial_counts(bits, W, P, n, partial, stream=None):
+    """Node-local counts: partial is a uint8 device tensor [W // P, stride >= n]."""
+    b, bstride = _bits_rows(bits)
+    if partial is not None and (partial.dim() != 2 or partial.stride(1) != 1):
+        raise ValueError("partial must be a 2-D row-major uint8 tensor")
+    _check(load().nf_partial_counts(b, bstride, W, P, n, _dev_ptr(partial, torch.uint8, "partial"),
+                                    partial.stride(0) if partial is not None else 0, _stream(stream)))
+
+
+def nf_partial_count_reduce(partial, W, n, mask, scale, decode_mode, counts, out, stream=None):
+    """Sum of the G partial-count rows of partial ([G, stride] uint8) and decode."""
+    if partial.dim() != 2 or partial.stride(1) != 1:
+        raise ValueError("partial must be a 2-D row-major uint8 tensor")
+    _check(load().nf_partial_count_reduce(_dev_ptr(partial, torch.uint8, "partial"), partial.stride(0),
+                                          partial.shape[0], W, n, _words(mask),
+                                          _dev_ptr(scale, torch.float32, "scale"), decode_mode,
+                                          _dev_ptr(counts, torch.uint8, "counts"),
+                                          _dev_ptr(out, torch.float32, "out"), _stream(stream)))
+
+
+def nf_stock_signcount(bits, W, n, mask, scale, decode_mode, replicas, counts, out, replica_stride,
+                       stream=None):
+    """Replicated count and decode: replica r at counts/out + r * replica_stride."""
+    b, bstride = _bits_rows(bits)
+    _check(load().nf_stock_signcount(b, bstride, W, n, _words(mask), _dev_ptr(scale, torch.float32, "scale"),
+                                     decode_mode, replicas, _dev_ptr(counts, torch.uint8, "counts"),
+                                     _dev_ptr(out, torch.float32, "out"), replica_stride, _stream(stream)))
 
 
 def nf_ternary_threshold(stats, n_eligible, tau):

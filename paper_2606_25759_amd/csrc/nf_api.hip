@@ -402,6 +402,99 @@ nf_status nf_signcount_reduce(const uint64_t* bits, int64_t bits_stride_words, i
   return ok();
 }
 
+nf_status nf_partial_counts(const uint64_t* bits, int64_t bits_stride_words, int32_t W, int32_t P,
+                            int64_t n, uint8_t* partial, int64_t partial_stride, void* stream) {
+  if (W < 1 || W > 255) return fail(NF_ERR_INVALID_ARG, "W=%d outside [1, 255]", W);
+  if (P < 1 || P > W || W % P) return fail(NF_ERR_INVALID_ARG, "P=%d must divide W=%d", P, W);
+  if (n < 0) return fail(NF_ERR_INVALID_ARG, "n < 0");
+  NF_TRY(check_bits(bits, bits_stride_words, n, W));
+  if (n > 0 && !partial) return fail(NF_ERR_INVALID_ARG, "partial is NULL");
+  if (partial_stride < n) return fail(NF_ERR_INVALID_ARG, "partial_stride < n");
+  if (n == 0) return ok();
+  const nf::Geometry geo = nf::make_geometry(P, n, n);
+  nf::Pass2Args p = pass2_args(geo);
+  p.bits = bits;
+  p.bstride = bits_stride_words;
+  p.counts = partial;
+  p.op = nf::kOpCountDecode;
+  p.nz = W / P;
+  p.z_rows = P;
+  p.z_counts = partial_stride;
+  hipError_t e = nf::launch_pass2(geo, p, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "partial-count launch");
+  return ok();
+}
+
+nf_status nf_partial_count_reduce(const uint8_t* partial, int64_t partial_stride, int32_t G, int32_t W,
+                                  int64_t n, const uint64_t* mask, const float* scale_dev,
+                                  int32_t decode_mode, uint8_t* counts, float* out, void* stream) {
+  if (W < 1 || W > 255) return fail(NF_ERR_INVALID_ARG, "W=%d outside [1, 255]", W);
+  if (G < 1 || G > W || W % G) return fail(NF_ERR_INVALID_ARG, "G=%d must divide W=%d", G, W);
+  if (n < 0) return fail(NF_ERR_INVALID_ARG, "n < 0");
+  if (n > 0 && !partial) return fail(NF_ERR_INVALID_ARG, "partial is NULL");
+  if (partial_stride < n) return fail(NF_ERR_INVALID_ARG, "partial_stride < n");
+  if (!aligned(partial, 16) || partial_stride % 16)
+    return fail(NF_ERR_ALIGNMENT, "partial must be 16-byte aligned with a stride that is a multiple of 16");
+  if (decode_mode != NF_DECODE_SOFT && decode_mode != NF_DECODE_MAJORITY)
+    return fail(NF_ERR_INVALID_ARG, "decode_mode=%d", decode_mode);
+  if (out) {
+    NF_TRY(check_mask(mask, n));
+    if (!scale_dev) return fail(NF_ERR_INVALID_ARG, "scale_dev is NULL");
+    if (!aligned(out, 4) || !aligned(scale_dev, 4)) return fail(NF_ERR_ALIGNMENT, "out/scale not 4-byte aligned");
+  }
+  if (n == 0 || (!out && !counts)) return ok();
+  nf::PsumArgs a;
+  a.partial = partial;
+  a.pstride = partial_stride;
+  a.mask = mask;
+  a.scale = scale_dev;
+  a.counts = counts;
+  a.out = out;
+  a.n = n;
+  a.G = G;
+  a.W = W;
+  a.decode_mode = decode_mode;
+  hipError_t e = nf::launch_psum(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "partial-count reduce launch");
+  return ok();
+}
+
+nf_status nf_stock_signcount(const uint64_t* bits, int64_t bits_stride_words, int32_t W, int64_t n,
+                             const uint64_t* mask, const float* scale_dev, int32_t decode_mode,
+                             int32_t replicas, uint8_t* counts, float* out, int64_t replica_stride,
+                             void* stream) {
+  if (replicas < 1 || replicas > 65535) return fail(NF_ERR_INVALID_ARG, "replicas=%d outside [1, 65535]", replicas);
+  if (replica_stride < n) return fail(NF_ERR_INVALID_ARG, "replica_stride < n");
+  if (W < 1 || W > 255) return fail(NF_ERR_INVALID_ARG, "W=%d outside [1, 255]", W);
+  if (n < 0) return fail(NF_ERR_INVALID_ARG, "n < 0");
+  NF_TRY(check_bits(bits, bits_stride_words, n, W));
+  if (decode_mode != NF_DECODE_SOFT && decode_mode != NF_DECODE_MAJORITY)
+    return fail(NF_ERR_INVALID_ARG, "decode_mode=%d", decode_mode);
+  if (out) {
+    NF_TRY(check_mask(mask, n));
+    if (!scale_dev) return fail(NF_ERR_INVALID_ARG, "scale_dev is NULL");
+    if (!aligned(out, 4) || !aligned(scale_dev, 4)) return fail(NF_ERR_ALIGNMENT, "out/scale not 4-byte aligned");
+  }
+  if (n == 0 || (!out && !counts)) return ok();
+  const nf::Geometry geo = nf::make_geometry(W, n, n);
+  nf::Pass2Args p = pass2_args(geo);
+  p.bits = bits;
+  p.bstride = bits_stride_words;
+  p.mask = mask;
+  p.scale = scale_dev;
+  p.counts = counts;
+  p.out = out;
+  p.op = nf::kOpCountDecode;
+  p.decode_mode = decode_mode;
+  p.nz = replicas;
+  p.z_rows = 0;
+  p.z_counts = replica_stride;
+  p.z_out = replica_stride;
+  hipError_t e = nf::launch_pass2(geo, p, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "stock signcount launch");
+  return ok();
+}
+
 nf_status nf_ternary_threshold(const nf_worker_stats* stats_host, int32_t W, int64_t n_eligible,
                                float tau, float* theta_host) {
   if (W < 1 || W > 255) return fail(NF_ERR_INVALID_ARG, "W=%d outside [1, 255]", W);

@@ -194,6 +194,22 @@ struct Pass2Args {
   float* out;
   int64_t n_total, bucket_n;
   int32_t W, op, select, decode_mode, mean, bpb2;
+  // grid z (0 or 1: one count): count z reads rows from z * z_rows and
+  // writes counts + z * z_counts, out + z * z_out
+  int32_t nz, z_rows;
+  int64_t z_counts, z_out;
+};
+
+// Partial-count reduction (inter-node sum of node-local counts + decode).
+struct PsumArgs {
+  const uint8_t* partial;  // G rows of n bytes, row g at partial + g * pstride
+  int64_t pstride;
+  const uint64_t* mask;    // required when out != NULL
+  const float* scale;      // device, one float; required when out != NULL
+  uint8_t* counts;         // nullable: n bytes
+  float* out;              // nullable: written at mask = 1
+  int64_t n;
+  int32_t G, W, decode_mode;
 };
 
 // ------------------------------------------------------------ route rules
@@ -295,5 +311,6 @@ hipError_t launch_decide(const Geometry& geo, const DecideArgs& a, hipStream_t s
 hipError_t launch_pass2(const Geometry& geo, const Pass2Args& a, hipStream_t s);
 hipError_t launch_ternary_pack(const Geometry& geo, const TernArgs& a, hipStream_t s);
 hipError_t launch_ternary_reduce(const Geometry& geo, const TernArgs& a, hipStream_t s);
+hipError_t launch_psum(const PsumArgs& a, hipStream_t s);
 
 }  // namespace nf

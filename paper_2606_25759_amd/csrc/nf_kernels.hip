@@ -17,8 +17,10 @@
 
 namespace nf {
 
-// Four floats as one 16-byte vector (for vector nontemporal stores).
+// Four floats / four dwords as one 16-byte vector (for vector nontemporal
+// loads and stores).
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ bool finite32(float x) {
   return (__float_as_uint(x) & 0x7f800000u) != 0x7f800000u;
@@ -752,11 +754,18 @@ __device__ __forceinline__ void count_column(const uint64_t* col, int64_t bstrid
 }
 
 __global__ __launch_bounds__(kThreads2) void k_pass2(
-    const uint64_t* __restrict__ bits, const float* __restrict__ g, const uint64_t* __restrict__ mask,
+    const uint64_t* __restrict__ bits0, const float* __restrict__ g, const uint64_t* __restrict__ mask,
     const nf_route_decision* __restrict__ dec, const float* __restrict__ scale_p,
-    uint8_t* __restrict__ counts, float* __restrict__ out, Pass2Args a) {
+    uint8_t* __restrict__ counts0, float* __restrict__ out0, Pass2Args a) {
   __shared__ float tab[256];
   __shared__ __align__(16) uint32_t rec[4][64 * 2 * kRec];
+  // Grid z: independent counts over rows z * z_rows .. z * z_rows + W - 1,
+  // written z * z_counts / z * z_out further on (node-local partial counts,
+  // replicated stock counting); z = 0 for every other call.
+  const int z = blockIdx.z;
+  const uint64_t* bits = bits0 ? bits0 + (int64_t)z * a.z_rows * a.bstride : nullptr;
+  uint8_t* counts = counts0 ? counts0 + (int64_t)z * a.z_counts : nullptr;
+  float* out = out0 ? out0 + (int64_t)z * a.z_out : nullptr;
   const int b = blockIdx.y;
   const int64_t base = (int64_t)b * a.bucket_n;
   const int64_t nbe = bucket_len(a.n_total, a.bucket_n, b);
@@ -1305,8 +1314,79 @@ hipError_t launch_ternary_reduce(const Geometry& geo, const TernArgs& a, hipStre
 }
 
 hipError_t launch_pass2(const Geometry& geo, const Pass2Args& a, hipStream_t s) {
-  hipLaunchKernelGGL(k_pass2, dim3((unsigned)geo.bpb2, (unsigned)geo.nb), dim3(kThreads2), 0, s,
+  const unsigned nz = a.nz > 0 ? (unsigned)a.nz : 1u;
+  hipLaunchKernelGGL(k_pass2, dim3((unsigned)geo.bpb2, (unsigned)geo.nb, nz), dim3(kThreads2), 0, s,
                      a.bits, a.g, a.mask, a.dec, a.scale, a.counts, a.out, a);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------- partial-count reduction
+//
+// Inter-node step of the hierarchical reducer: c_i = sum over the G rows of
+// uint8 partial counts, then the aggregate return (decode) as in pass 2.  A
+// thread takes 16 consecutive elements: one 16-byte load per partial row,
+// summed as packed bytes in 32-bit adds (every byte's sum is at most W <=
+// 255, so no carry crosses a byte), one 16-byte store of counts, and the
+// 16 decoded values through an LDS table of fl32(scale * q[c]).
+__global__ __launch_bounds__(kThreads2) void k_psum(PsumArgs a) {
+  __shared__ float tab[256];
+  if (a.out) {
+    const float scale = *a.scale;
+    for (int c = threadIdx.x; c <= a.W; c += kThreads2) tab[c] = scale * decode_q(c, a.W, a.decode_mode);
+    __syncthreads();
+  }
+  const int64_t ngroups = (a.n + 15) / 16;
+  const bool c16 = a.counts && ((reinterpret_cast<uintptr_t>(a.counts) & 15) == 0);
+  const bool o16 = a.out && ((reinterpret_cast<uintptr_t>(a.out) & 15) == 0);
+  for (int64_t t = (int64_t)blockIdx.x * kThreads2 + threadIdx.x; t < ngroups; t += (int64_t)gridDim.x * kThreads2) {
+    const int64_t i0 = t * 16;
+    const int cnt = (a.n - i0) < 16 ? (int)(a.n - i0) : 16;
+    uint32_t c[4] = {0u, 0u, 0u, 0u};
+    if (cnt == 16) {
+      for (int gr = 0; gr < a.G; ++gr) {
+        const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(a.partial + (int64_t)gr * a.pstride + i0));
+        c[0] += v[0];
+        c[1] += v[1];
+        c[2] += v[2];
+        c[3] += v[3];
+      }
+    } else {
+      for (int gr = 0; gr < a.G; ++gr)
+        for (int e = 0; e < cnt; ++e) c[e / 4] += (uint32_t)a.partial[(int64_t)gr * a.pstride + i0 + e] << (8 * (e % 4));
+    }
+    if (a.counts) {
+      if (cnt == 16 && c16) {
+        const u32x4 cv = {c[0], c[1], c[2], c[3]};
+        __builtin_nontemporal_store(cv, reinterpret_cast<u32x4*>(a.counts + i0));
+      } else {
+        for (int e = 0; e < cnt; ++e) a.counts[i0 + e] = (uint8_t)(c[e / 4] >> (8 * (e % 4)));
+      }
+    }
+    if (a.out) {
+      const uint32_t m16 = (uint32_t)(a.mask[i0 / 64] >> (i0 & 63)) & 0xffffu;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const uint32_t cw = c[q];
+        const uint32_t mq = (m16 >> (4 * q)) & 15u;
+        const int64_t j = i0 + 4 * q;
+        if (cnt == 16 && o16 && mq == 15u) {
+          const f32x4 y = {tab[cw & 255u], tab[(cw >> 8) & 255u], tab[(cw >> 16) & 255u], tab[cw >> 24]};
+          __builtin_nontemporal_store(y, reinterpret_cast<f32x4*>(a.out + j));
+        } else {
+          for (int e = 0; e < 4; ++e)
+            if (4 * q + e < cnt && ((mq >> e) & 1u)) a.out[j + e] = tab[(cw >> (8 * e)) & 255u];
+        }
+      }
+    }
+  }
+}
+
+hipError_t launch_psum(const PsumArgs& a, hipStream_t s) {
+  const int64_t ngroups = (a.n + 15) / 16;
+  int64_t blocks = (ngroups + kThreads2 - 1) / kThreads2;
+  if (blocks > 4096) blocks = 4096;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(k_psum, dim3((unsigned)blocks), dim3(kThreads2), 0, s, a);
   return hipGetLastError();
 }
 

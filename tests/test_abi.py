@@ -157,6 +157,24 @@ def test_invalid_arguments_return_codes_without_launch():
                                 fake, fake, ws, 1 << 24, None) == nf.NF_ERR_INVALID_ARG
     # decode counts: W out of range
     assert lib.nf_signcount_reduce(fake, 10, 0, 640, fake, fake, 0, fake, fake, None) == nf.NF_ERR_INVALID_ARG
+    # hierarchical counting: group size must divide W; partial stride; alignment of partial rows
+    assert lib.nf_partial_counts(fake, 10, 8, 3, 640, fake, 640, None) == nf.NF_ERR_INVALID_ARG
+    assert lib.nf_partial_counts(fake, 10, 8, 0, 640, fake, 640, None) == nf.NF_ERR_INVALID_ARG
+    assert lib.nf_partial_counts(fake, 10, 8, 4, 640, fake, 639, None) == nf.NF_ERR_INVALID_ARG
+    assert lib.nf_partial_counts(fake, 9, 8, 4, 640, fake, 640, None) == nf.NF_ERR_INVALID_ARG
+    assert lib.nf_partial_count_reduce(fake, 640, 3, 8, 640, fake, fake, 0, fake, fake, None) == \
+        nf.NF_ERR_INVALID_ARG
+    assert lib.nf_partial_count_reduce(P(0x1008), 640, 2, 8, 640, fake, fake, 0, fake, fake, None) == \
+        nf.NF_ERR_ALIGNMENT
+    assert lib.nf_partial_count_reduce(fake, 648, 2, 8, 640, fake, fake, 0, fake, fake, None) == \
+        nf.NF_ERR_ALIGNMENT
+    assert lib.nf_partial_count_reduce(fake, 640, 2, 8, 640, fake, None, 0, fake, fake, None) == \
+        nf.NF_ERR_INVALID_ARG
+    # stock replicas: count and stride
+    assert lib.nf_stock_signcount(fake, 10, 8, 640, fake, fake, 0, 0, fake, fake, 640, None) == \
+        nf.NF_ERR_INVALID_ARG
+    assert lib.nf_stock_signcount(fake, 10, 8, 640, fake, fake, 0, 2, fake, fake, 639, None) == \
+        nf.NF_ERR_INVALID_ARG
     # decision: n_eligible > n
     st = (nf.nf_worker_stats * 2)()
     d = nf.nf_route_decision()
