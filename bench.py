@@ -56,6 +56,9 @@ def parse():
                     help="only run the copy kernel of known traffic (counter calibration)")
     ap.add_argument("--contrast", action="store_true",
                     help="only time hierarchical vs stock vs direct sign counting (one JSON line per shape)")
+    ap.add_argument("--controller", type=int, default=0, metavar="STEPS",
+                    help="only run STEPS controller-driven reducer steps (Supervisor + endpoint guard feeding "
+                         "the route policy) on the chosen workload and report route evidence")
     return ap.parse_args()
 
 
@@ -199,6 +202,77 @@ def contrast(reps=50):
     return 0
 
 
+def controller_run(args):
+    """A synthetic training run in which the host controller supplies each step's route policy:
+    Commander admission, Supervisor CUSUM recovery and the route-use budget from a loss trace,
+    and the endpoint-capacity guard from a cost model.  Every step runs the reducer on the GPU;
+    its route decisions go back to the controller (L/F/P events, MGTR)."""
+    import numpy as np
+    import torch
+    import paper_2606_25759_amd as nf
+    import synth
+
+    dev = torch.device("cuda:0")
+    lay = synth.CONFIGS[args.workload]()
+    W, n, bn, nb = lay.W, lay.n_total, lay.bucket_n, lay.nb
+    nw = (n + 63) // 64
+    grads = torch.empty((W, lay.stride), dtype=torch.float32, device=dev)
+    synth.generate_device(lay, grads)
+    off, ln, el = synth.mask_segments(lay)
+    mask_h = nf.nf_mask_from_segments(off, ln, el, n)
+    mask = torch.from_numpy(mask_h.view(np.int64)).to(dev)
+    ternary = args.format == "ternary"
+    planes = 2 if ternary else 1
+    bits = torch.empty((planes * W, nw), dtype=torch.int64, device=dev)
+    out = torch.empty(n, dtype=torch.float32, device=dev)
+    stats = torch.empty(nb * W * nf.STATS_BYTES, dtype=torch.uint8, device=dev)
+    dec = torch.empty(nb * nf.DECISION_BYTES, dtype=torch.uint8, device=dev)
+    ws = nf.empty_workspace(nf.nf_workspace_bytes_buckets(W, n, bn), dev)
+
+    # Operating profile in the style of the paper's Transformer row (Table 2: slack 2.11e-4, threshold
+    # 1.01e-2, one-epoch cooldown, a post-recovery guard); an epoch is 50 steps here, the guard lasts
+    # two cooldowns with the threshold halved, admission after a 40-step warm-up, a 0.8 route-use target.
+    T = args.controller
+    prof = nf.supervisor_profile(admit_step=40, cooldown_steps=50, guard_steps=100, short_cooldown_steps=5,
+                                 ema_alpha=0.1, slack=2.11e-4, threshold=1.01e-2, guard_scale=0.5,
+                                 near_band=0.25, small_move=5e-3, target_share=0.8, share_margin=0.03)
+    state = nf.nf_supervisor_init(prof)
+    # Endpoint guard for a full bucket: 2 nodes x (W/2) GPUs, 25 GB/s links, 100 GB/s endpoint counting.
+    elig = np.unpackbits(mask_h[: bn // 64].view(np.uint8), bitorder="little").sum()
+    model = nf.nf_endpoint_model(2, max(1, W // 2), planes, 0, 25e9, 100e9, 20e-6, 30e-6)
+    t_fp32, t_low, guard_ok = nf.nf_endpoint_guard(model, min(bn, n), int(elig))
+    # Synthetic loss: a decaying curve with noise and two degradation episodes.
+    rng = np.random.default_rng(17)
+    t = np.arange(T)
+    loss = 0.7 * np.exp(-t / 300.0) + 0.3 + rng.normal(0, 2e-3, T)
+    for a in (T // 3, (2 * T) // 3):
+        loss[a:a + 30] += np.linspace(0.0, 0.05, 30)[: len(loss[a:a + 30])]
+    routes_per_step = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(T):
+        pol = nf.nf_supervisor_policy(prof, state, nf.policy(guard_ok=int(guard_ok), format=int(ternary)))
+        nf.nf_route_buckets(grads, n, bn, mask, pol, bits, None, out, stats, dec, ws)
+        d = nf.decisions_host(dec, nb)  # synchronises the stream
+        nf.nf_supervisor_update(prof, state, d, float(loss[k]))
+        routes_per_step.append((int((d["route"] == 0).sum()), int((d["route"] == 1).sum()),
+                                int((d["route"] == 2).sum())))
+    wall = time.perf_counter() - t0
+    rec = {"metric": "controller-driven reducer run (route evidence)", "config": {
+               "workload": lay.name, "W": W, "buckets": nb, "steps": T, "format": args.format},
+           "endpoint_guard": {"t_fp32_us": round(t_fp32 * 1e6, 2), "t_lowbit_us": round(t_low * 1e6, 2),
+                              "guard_ok": guard_ok},
+           "events": {"L": state.events_l, "F": state.events_f, "P": state.events_p},
+           "lowbit_share": round(state.events_l / max(1, state.events_l + state.events_f + state.events_p), 4),
+           "mgtr": round(state.bytes_route / state.bytes_fp32, 4),
+           "alarms": state.alarms, "short_recoveries": state.short_recoveries,
+           "readmissions": state.readmissions, "budget_vetoes": state.budget_vetoes,
+           "ms_per_step_wall": round(wall * 1e3 / T, 3),
+           "first_lowbit_step": next((i for i, r in enumerate(routes_per_step) if r[0]), None)}
+    print(json.dumps(rec), flush=True)
+    return 0
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -216,6 +290,8 @@ def main():
         return calibrate_copy()
     if args.contrast:
         return contrast()
+    if args.controller:
+        return controller_run(args)
 
     import paper_2606_25759_amd as nf
     import synth

@@ -323,6 +323,106 @@ nf_status nf_route_buckets(const float* grads, int64_t worker_stride, int32_t W,
                            nf_worker_stats* stats, nf_route_decision* decisions, void* ws,
                            size_t ws_bytes, void* stream);
 
+/* ------------------------------------------------------------------------
+ * Controller inputs on the host (§4.3 Supervisor recovery, §4.4 online
+ * control, §6.4 endpoint-capacity guard).  These functions produce the
+ * admitted / veto / guard_ok fields of nf_route_policy from an operating
+ * profile, the training loss and the route decisions of earlier steps.
+ * Pure host functions; every pointer is host memory.
+ *
+ * Supervisor per step t (the paper gives the mechanisms, not formulas; the
+ * readings are stated here):
+ *   - health signal: s_0 = loss_0, s_t = s_{t-1} + ema_alpha (loss_t - s_{t-1});
+ *   - detector, Page's one-sided CUSUM on the per-step increase of s with the
+ *     profile's slack and threshold (§4.1): S_t = max(0, S_{t-1} + (s_t -
+ *     s_{t-1}) - slack), on steps run with low-bit admitted and not vetoed
+ *     only; alarm when S_t > threshold (threshold * guard_scale during a
+ *     readmission guard);
+ *   - an alarm starts an FP32 cooldown (veto) of cooldown_steps steps and
+ *     resets S; a near-threshold alarm (S_t <= threshold_eff * (1 +
+ *     near_band)) with a small loss movement (|loss_t - loss_{t-1}| <=
+ *     small_move) gets short_cooldown_steps instead when that is > 0 (the
+ *     noise-aware short recovery);
+ *   - after the cooldown low-bit is readmitted under a guard of guard_steps
+ *     low-bit steps with the stricter threshold (0: readmitted directly);
+ *   - Commander admits low-bit from step admit_step on (earlier steps: plain
+ *     FP32, not admitted);
+ *   - route-use budget guard: when the realized low-bit share L / (L + F + P)
+ *     of the route events recorded so far exceeds target_share + share_margin,
+ *     the next step is vetoed (target_share >= 1 disables it).
+ * ------------------------------------------------------------------------ */
+enum { NF_SUP_WARMUP = 0, NF_SUP_LOWBIT = 1, NF_SUP_COOLDOWN = 2, NF_SUP_GUARD = 3 };
+
+/* Operating-profile settings of Commander and Supervisor (§4.1, Table 2). */
+typedef struct {
+  int32_t admit_step;            /* first step with low-bit admitted, >= 0         */
+  int32_t cooldown_steps;        /* FP32 fallback length after an alarm, >= 0     */
+  int32_t guard_steps;           /* readmission guard length, >= 0                 */
+  int32_t short_cooldown_steps;  /* noise-aware short recovery, >= 0 (0: off)      */
+  double ema_alpha;              /* smoothing of the loss, in (0, 1]               */
+  double slack;                  /* CUSUM slack (tolerated increase per step)      */
+  double threshold;              /* CUSUM threshold, > 0                           */
+  double guard_scale;            /* threshold factor in the guard, in (0, 1]       */
+  double near_band;              /* near-threshold band, >= 0                      */
+  double small_move;             /* small loss movement, >= 0                      */
+  double target_share;           /* route-use budget: target low-bit share         */
+  double share_margin;           /* guard band over the target, >= 0               */
+} nf_supervisor_profile;
+
+/* Supervisor state and the run's route evidence (caller-owned, host). */
+typedef struct {
+  int64_t step;                  /* steps recorded so far                           */
+  int32_t state;                 /* NF_SUP_*                                        */
+  int32_t has_prev;              /* a loss has been recorded                        */
+  int32_t cooldown_left, guard_left;
+  double smoothed, cusum, prev_loss;
+  int64_t alarms, short_recoveries, readmissions, budget_vetoes;
+  int64_t events_l, events_f, events_p;  /* route events (buckets) by route (§3.2) */
+  double bytes_route, bytes_fp32;        /* MGTR = bytes_route / bytes_fp32 (§3.2)  */
+} nf_supervisor_state;
+
+/* Validates the profile and starts a run (state WARMUP, or LOWBIT when
+ * admit_step is 0).  NF_ERR_INVALID_ARG on an invalid profile. */
+nf_status nf_supervisor_init(const nf_supervisor_profile* profile_host, nf_supervisor_state* state_host);
+
+/* Controller inputs for the next step: sets policy->admitted and
+ * policy->veto (cooldown or route-use budget); other fields untouched. */
+nf_status nf_supervisor_policy(const nf_supervisor_profile* profile_host,
+                               const nf_supervisor_state* state_host, nf_route_policy* policy_host);
+
+/* Records the step just run: its nb route decisions (events and modeled
+ * bytes) and its loss (finite), then advances the detector and the state.
+ * The decisions are those made under nf_supervisor_policy for this step. */
+nf_status nf_supervisor_update(const nf_supervisor_profile* profile_host,
+                               nf_supervisor_state* state_host,
+                               const nf_route_decision* decisions_host, int64_t nb, double loss);
+
+/* Endpoint-capacity guard (§6.4): reducer-path measurements and topology. */
+typedef struct {
+  int32_t nodes, gpus_per_node;  /* N nodes x P GPUs, W = N P workers, >= 1        */
+  int32_t bits_per_element;      /* payload bits per eligible element: 1 (G-Binary)
+                                    or 2 (G-Ternary)                                */
+  int32_t reserved;
+  double net_bytes_per_s;        /* per-link network bandwidth B, > 0               */
+  double endpoint_bytes_per_s;   /* endpoint counting service rate R (payload bytes
+                                    per second), > 0                                */
+  double latency_fp32_s, latency_lowbit_s;  /* fixed costs, >= 0                     */
+} nf_endpoint_model;
+
+/*
+ * Estimated bucket communication time of the hierarchical low-bit reducer
+ * and of the matched FP32 ring all-reduce, for a bucket of n elements of
+ * which n_eligible are eligible; *guard_ok = (t_lowbit < t_fp32):
+ *   t_fp32   = latency_fp32 + 2 (W-1)/W * 4 n / B
+ *   t_lowbit = latency_lowbit + b n_E/8 / B       payload to the node endpoint
+ *            + P b n_E/8 / R                      node-local counting
+ *            + 2 (N-1)/N * n_E / B                uint8 partial-count exchange
+ *            + n_E / B                            aggregate return
+ *            + 2 (W-1)/W * 4 (n - n_E) / B        routed elements in FP32
+ */
+nf_status nf_endpoint_guard(const nf_endpoint_model* model_host, int64_t n, int64_t n_eligible,
+                            double* t_fp32_host, double* t_lowbit_host, int32_t* guard_ok_host);
+
 /*
  * Profiling hook (no paper counterpart).  When set on the calling thread,
  * nf_route_bucket and nf_route_buckets record these hipEvent_t handles (each

@@ -33,7 +33,9 @@ EXPORTS = ["nf_abi_version", "nf_last_error", "nf_mask_from_segments", "nf_works
            "nf_bucket_health", "nf_pack_signs", "nf_fp32_reduce", "nf_signcount_reduce",
            "nf_route_decide", "nf_route_bucket", "nf_workspace_bytes_buckets", "nf_route_buckets",
            "nf_set_phase_events", "nf_pass1_launches", "nf_ternary_threshold", "nf_pack_ternary",
-           "nf_ternary_reduce", "nf_partial_counts", "nf_partial_count_reduce", "nf_stock_signcount"]
+           "nf_ternary_reduce", "nf_partial_counts", "nf_partial_count_reduce", "nf_stock_signcount",
+           "nf_supervisor_init", "nf_supervisor_policy", "nf_supervisor_update", "nf_endpoint_guard"]
+NF_SUP_WARMUP, NF_SUP_LOWBIT, NF_SUP_COOLDOWN, NF_SUP_GUARD = 0, 1, 2, 3
 
 
 class nf_worker_stats(ctypes.Structure):
@@ -53,6 +55,32 @@ class nf_route_decision(ctypes.Structure):
                 ("scale", ctypes.c_float), ("reserved", ctypes.c_uint32),
                 ("n_eligible", ctypes.c_int64), ("bytes_route", ctypes.c_double),
                 ("bytes_fp32", ctypes.c_double)]
+
+
+class nf_supervisor_profile(ctypes.Structure):
+    _fields_ = [("admit_step", ctypes.c_int32), ("cooldown_steps", ctypes.c_int32),
+                ("guard_steps", ctypes.c_int32), ("short_cooldown_steps", ctypes.c_int32),
+                ("ema_alpha", ctypes.c_double), ("slack", ctypes.c_double), ("threshold", ctypes.c_double),
+                ("guard_scale", ctypes.c_double), ("near_band", ctypes.c_double),
+                ("small_move", ctypes.c_double), ("target_share", ctypes.c_double),
+                ("share_margin", ctypes.c_double)]
+
+
+class nf_supervisor_state(ctypes.Structure):
+    _fields_ = [("step", ctypes.c_int64), ("state", ctypes.c_int32), ("has_prev", ctypes.c_int32),
+                ("cooldown_left", ctypes.c_int32), ("guard_left", ctypes.c_int32),
+                ("smoothed", ctypes.c_double), ("cusum", ctypes.c_double), ("prev_loss", ctypes.c_double),
+                ("alarms", ctypes.c_int64), ("short_recoveries", ctypes.c_int64),
+                ("readmissions", ctypes.c_int64), ("budget_vetoes", ctypes.c_int64),
+                ("events_l", ctypes.c_int64), ("events_f", ctypes.c_int64), ("events_p", ctypes.c_int64),
+                ("bytes_route", ctypes.c_double), ("bytes_fp32", ctypes.c_double)]
+
+
+class nf_endpoint_model(ctypes.Structure):
+    _fields_ = [("nodes", ctypes.c_int32), ("gpus_per_node", ctypes.c_int32),
+                ("bits_per_element", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("net_bytes_per_s", ctypes.c_double), ("endpoint_bytes_per_s", ctypes.c_double),
+                ("latency_fp32_s", ctypes.c_double), ("latency_lowbit_s", ctypes.c_double)]
 
 
 STATS_DTYPE = np.dtype([("nonfinite", "<u8"), ("sum_abs_elig", "<f8"), ("sum_sq", "<f8")])
@@ -109,6 +137,10 @@ def load(path=None):
         "nf_partial_counts": (ctypes.c_int, [_P, _I64, _I32, _I32, _I64, _P, _I64, _P]),
         "nf_partial_count_reduce": (ctypes.c_int, [_P, _I64, _I32, _I32, _I64, _P, _P, _I32, _P, _P, _P]),
         "nf_stock_signcount": (ctypes.c_int, [_P, _I64, _I32, _I64, _P, _P, _I32, _I32, _P, _P, _I64, _P]),
+        "nf_supervisor_init": (ctypes.c_int, [_P, _P]),
+        "nf_supervisor_policy": (ctypes.c_int, [_P, _P, _P]),
+        "nf_supervisor_update": (ctypes.c_int, [_P, _P, _P, _I64, ctypes.c_double]),
+        "nf_endpoint_guard": (ctypes.c_int, [_P, _I64, _I64, _P, _P, _P]),
     }
     for name, (res, args) in sigs.items():
         fn = getattr(lib, name)
@@ -209,6 +241,44 @@ def nf_route_decide(stats, n, n_eligible, pol=None):
     _check(load().nf_route_decide(st.ctypes.data, len(st), n, n_eligible, ctypes.byref(pol),
                                   ctypes.byref(d)))
     return d
+
+
+# ------------------------------------------------------- controller (host)
+
+def supervisor_profile(admit_step=0, cooldown_steps=10, guard_steps=0, short_cooldown_steps=0, ema_alpha=0.1,
+                       slack=0.0, threshold=1.0, guard_scale=1.0, near_band=0.0, small_move=0.0,
+                       target_share=1.0, share_margin=0.0):
+    return nf_supervisor_profile(admit_step, cooldown_steps, guard_steps, short_cooldown_steps, ema_alpha, slack,
+                                 threshold, guard_scale, near_band, small_move, target_share, share_margin)
+
+
+def nf_supervisor_init(profile):
+    st = nf_supervisor_state()
+    _check(load().nf_supervisor_init(ctypes.byref(profile), ctypes.byref(st)))
+    return st
+
+
+def nf_supervisor_policy(profile, state, pol=None):
+    """Sets admitted and veto of pol (a new default policy if None); returns it."""
+    pol = pol if pol is not None else policy()
+    _check(load().nf_supervisor_policy(ctypes.byref(profile), ctypes.byref(state), ctypes.byref(pol)))
+    return pol
+
+
+def nf_supervisor_update(profile, state, decisions, loss):
+    """decisions: numpy DECISION_DTYPE array of the step's buckets (host)."""
+    d = np.ascontiguousarray(decisions, dtype=DECISION_DTYPE)
+    _check(load().nf_supervisor_update(ctypes.byref(profile), ctypes.byref(state),
+                                       d.ctypes.data if len(d) else None, len(d), float(loss)))
+    return state
+
+
+def nf_endpoint_guard(model, n, n_eligible):
+    """Returns (t_fp32, t_lowbit, guard_ok)."""
+    tf, tl, ok = ctypes.c_double(), ctypes.c_double(), ctypes.c_int32()
+    _check(load().nf_endpoint_guard(ctypes.byref(model), n, n_eligible, ctypes.byref(tf), ctypes.byref(tl),
+                                    ctypes.byref(ok)))
+    return tf.value, tl.value, bool(ok.value)
 
 
 # ------------------------------------------------------------- device calls

@@ -241,6 +241,13 @@ nf_status route_flat(const float* g, int64_t stride, int32_t W, int64_t n_total,
 
 }  // namespace
 
+namespace nf {
+nf_status set_error(nf_status st, const char* msg) {
+  g_err = msg;
+  return st;
+}
+}  // namespace nf
+
 extern "C" {
 
 int nf_abi_version(void) { return NF_ABI_VERSION; }

@@ -305,6 +305,9 @@ NF_HD inline float decode_q(int c, int W, int mode) {
   return (float)margin / (float)W;
 }
 
+// Sets the thread-local message of nf_last_error (nf_api.hip) and returns st.
+nf_status set_error(nf_status st, const char* msg);
+
 // Launchers (nf_kernels.hip).
 hipError_t launch_pass1(const Geometry& geo, const Pass1Args& a, hipStream_t s);
 hipError_t launch_decide(const Geometry& geo, const DecideArgs& a, hipStream_t s);
