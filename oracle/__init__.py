@@ -72,6 +72,9 @@ def load(path=None):
         "nfo_pack_ternary": (None, [_P, _I64, _I32, _I64, _P, _P, _P, _P, _I64]),
         "nfo_ternary_decode_table": (None, [_I32, _I32, _P]),
         "nfo_ternary_output": (None, [_P, _I64, _P, _P, _P, _P, ctypes.c_float, _I32, _I32, _P]),
+        "nfo_pack_compact": (None, [_P, _I64, _I32, _I64, _P, _P, _I64]),
+        "nfo_slice_scales": (None, [_P, _I64, _I32, _P, _P, _I64, _P, _P]),
+        "nfo_sliced_output": (None, [_P, _I64, _P, _P, _P, _P, _P, _I64, _P, _I32, _P]),
         "nfo_reduce_bucket_ternary": (ctypes.c_int, [_P, _I64, _I32, _I64, _P, _P, _P, _P, _I64,
                                                      _P, _P, _P, _P, _P]),
     }
@@ -269,3 +272,45 @@ def reduce_bucket_ternary(g, mask, pol, lib=None):
         raise ValueError("invalid arguments")
     return dict(pos=pos[:, :nw], neg=neg[:, :nw], cpos=cp[:n], cneg=cn[:n], out=out[:n], stats=st,
                 decision=d)
+
+
+def pack_compact(g, mask, lib=None):
+    """Compacted sign payload [W, ceil(n_E/64)] (R30)."""
+    lib = lib or load()
+    g, stride = _grads(g)
+    W, n = g.shape
+    m = np.ascontiguousarray(mask, np.uint64)
+    ne = count_eligible(m, n, lib=lib) if n else 0
+    cw = (ne + 63) // 64
+    cb = np.zeros((W, max(cw, 1)), dtype=np.uint64)
+    lib.nfo_pack_compact(_ptr(g), stride, W, n, _ptr(m if m.size else np.zeros(1, np.uint64)), _ptr(cb),
+                         cb.shape[1])
+    return cb[:, :cw]
+
+
+def slice_scales(g, off, length, lib=None):
+    """(sums [S, W] float64, scales [S] float32) of the slices (R31)."""
+    lib = lib or load()
+    g, stride = _grads(g)
+    W = g.shape[0]
+    off = np.ascontiguousarray(off, dtype=np.int64)
+    length = np.ascontiguousarray(length, dtype=np.int64)
+    S = len(off)
+    sums = np.zeros((max(S, 1), W), dtype=np.float64)
+    sc = np.zeros(max(S, 1), dtype=np.float32)
+    lib.nfo_slice_scales(_ptr(g), stride, W, _ptr(off), _ptr(length), S, _ptr(sums), _ptr(sc))
+    return sums[:S], sc[:S]
+
+
+def sliced_output(mask, counts, y, q, off, length, scales, route=ROUTE_L, lib=None):
+    """Positional output with per-slice scales (R32)."""
+    lib = lib or load()
+    n = len(y)
+    out = np.zeros(max(n, 1), dtype=np.float32)
+    m = np.ascontiguousarray(mask, np.uint64)
+    lib.nfo_sliced_output(_ptr(m if m.size else np.zeros(1, np.uint64)), n,
+                          _ptr(np.ascontiguousarray(counts, np.uint8)), _ptr(np.ascontiguousarray(y, np.float32)),
+                          _ptr(np.ascontiguousarray(q, np.float32)), _ptr(np.ascontiguousarray(off, np.int64)),
+                          _ptr(np.ascontiguousarray(length, np.int64)), len(off),
+                          _ptr(np.ascontiguousarray(scales, np.float32)), route, _ptr(out))
+    return out[:n]

@@ -58,6 +58,22 @@
  *       MAJORITY q_d = sign(d) (0 at d = 0); the output is fl32(scale * q_d)
  *       with the scale of R5.  Routes, reasons and FP32 positions as above.
  *   R21 MGTR for the ternary L route: 2 n_E / 8 + 4 + 4 n_F bytes per worker.
+ *
+ * Per-slice scales and a compacted payload (§5.2 records a mean-absolute
+ * scale per eligible slice; §6.1 counts bit-packed updates; the paper fixes
+ * neither the scale's granularity nor the payload's layout):
+ *   R29 The eligible slices of a bucket are S intervals [off_s, off_s +
+ *       len_s), sorted, disjoint, len_s >= 1; the mask is their union.
+ *   R30 Compacted payload: bit r of worker w's row is (g > 0) of the r-th
+ *       eligible element in element order (r = 0 .. n_E - 1), LSB-first
+ *       uint64 words, ceil(n_E / 64) words, padding bits 0.
+ *   R31 Slice scale: scale_s = fl32((sum_w S_sw / len_s) / W), S_sw the FP64
+ *       sum of |g| over the slice in element order, workers in order (R5 on
+ *       one slice).
+ *   R32 Sliced decode: out_i = fl32(scale_s(i) * q[c_i]) at eligible i (c_i
+ *       the count over the compacted rows at i's rank, equal to the
+ *       positional count), the FP32 path elsewhere.
+ *   R33 MGTR for this route: n_E / 8 + 4 S + 4 n_F bytes per worker.
  */
 #include "nfo.h"
 
@@ -359,4 +375,55 @@ int nfo_reduce_bucket_ternary(const float* g, int64_t stride, int32_t W,
                        W, d->route, out + i0);
   }
   return 0;
+}
+
+/* ---- compacted payload (R30) --------------------------------------------- */
+void nfo_pack_compact(const float* g, int64_t stride, int32_t W, int64_t n,
+                      const uint64_t* mask, uint64_t* cbits, int64_t cstride) {
+  int64_t n_eligible = nfo_count_eligible(mask, n);
+  int64_t cwords = (n_eligible + 63) / 64;
+  for (int32_t w = 0; w < W; ++w) {
+    const float* row = g + (int64_t)w * stride;
+    uint64_t* crow = cbits + (int64_t)w * cstride;
+    for (int64_t k = 0; k < cwords; ++k) crow[k] = 0;
+    int64_t r = 0; /* rank of the next eligible element */
+    for (int64_t i = 0; i < n; ++i) {
+      if (!mask_bit(mask, i)) continue;
+      if (row[i] > 0.0f) crow[r / 64] |= (uint64_t)1 << (r % 64);
+      ++r;
+    }
+  }
+}
+
+/* ---- per-slice scales (R29, R31) ----------------------------------------- */
+void nfo_slice_scales(const float* g, int64_t stride, int32_t W,
+                      const int64_t* off, const int64_t* len, int64_t S,
+                      double* sums /* [S][W] */, float* scales /* [S] */) {
+  for (int64_t s = 0; s < S; ++s) {
+    double acc = 0.0;
+    for (int32_t w = 0; w < W; ++w) {
+      const float* row = g + (int64_t)w * stride + off[s];
+      double t = 0.0;
+      for (int64_t j = 0; j < len[s]; ++j) t += fabs((double)row[j]);
+      sums[s * W + w] = t;
+      acc += t / (double)len[s];
+    }
+    scales[s] = (float)(acc / (double)W);
+  }
+}
+
+/* ---- sliced decode (R32) ------------------------------------------------- */
+void nfo_sliced_output(const uint64_t* mask, int64_t n, const uint8_t* counts,
+                       const float* y, const float* q, const int64_t* off,
+                       const int64_t* len, int64_t S, const float* scales,
+                       int32_t route, float* out) {
+  int64_t s = 0;
+  for (int64_t i = 0; i < n; ++i) {
+    if (route == NFO_ROUTE_L && mask_bit(mask, i)) {
+      while (s < S && i >= off[s] + len[s]) ++s; /* the slice holding i */
+      out[i] = scales[s] * q[counts[i]];
+    } else {
+      out[i] = y[i];
+    }
+  }
 }

@@ -152,6 +152,17 @@ int nfo_reduce_bucket_ternary(const float* g, int64_t stride, int32_t W,
                               int64_t bits_stride, uint8_t* cpos, uint8_t* cneg,
                               float* out, nfo_stats* stats, nfo_decision* d);
 
+/* Per-slice scales and the compacted payload (R29-R33). */
+void nfo_pack_compact(const float* g, int64_t stride, int32_t W, int64_t n,
+                      const uint64_t* mask, uint64_t* cbits, int64_t cstride);
+void nfo_slice_scales(const float* g, int64_t stride, int32_t W,
+                      const int64_t* off, const int64_t* len, int64_t S,
+                      double* sums, float* scales);
+void nfo_sliced_output(const uint64_t* mask, int64_t n, const uint8_t* counts,
+                       const float* y, const float* q, const int64_t* off,
+                       const int64_t* len, int64_t S, const float* scales,
+                       int32_t route, float* out);
+
 #ifdef __cplusplus
 }
 #endif

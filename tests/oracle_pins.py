@@ -803,6 +803,104 @@ def pin_ternary_negation(lib):
     assert np.array_equal(a["out"][e], -b["out"][e]), "negation decoded values"
 
 
+# ------------------------------------- compacted payload, per-slice scales
+
+def np_compact(g, mask_bool_row):
+    """Reference compacted rows from numpy: the (g > 0) bits at eligible positions, repacked LSB-first."""
+    W = g.shape[0]
+    rows = []
+    for w in range(W):
+        b = (g[w] > 0) & mask_bool_row
+        sel = b[mask_bool_row].astype(np.uint8)
+        nE = len(sel)
+        padded = np.zeros(((nE + 63) // 64) * 64, dtype=np.uint8)
+        padded[:nE] = sel
+        rows.append(np.packbits(padded, bitorder="little").view(np.uint64))
+    return np.array(rows).reshape(W, -1)
+
+
+def pin_pack_compact(lib):
+    # hand example: mask bits 1, 2, 4, 5, 7; signs there - + - + -  -> ranks 1 and 3 set
+    g = np.array([[1.0, -1.0, 2.0, 3.0, -4.0, 5.0, 6.0, -7.0]], dtype=np.float32)
+    m = np.array([0b10110110], dtype=np.uint64)
+    assert nfo.pack_compact(g, m, lib=lib)[0, 0] == 0b01010, "hand example"
+    rng = np.random.default_rng(21)
+    for W, n, dens in [(1, 1, 1.0), (3, 63, 0.5), (5, 64, 0.9), (2, 65, 0.3), (7, 1000, 0.7), (4, 4097, 0.95),
+                       (3, 3000, 0.02)]:
+        g = rng.normal(size=(W, n)).astype(np.float32)
+        g[rng.random((W, n)) < 0.05] = 0.0
+        mb = rng.random(n) < dens
+        words = np.packbits(np.concatenate([mb, np.zeros((-n) % 64, bool)]).astype(np.uint8),
+                            bitorder="little").view(np.uint64)
+        got = nfo.pack_compact(g, words, lib=lib)
+        assert np.array_equal(got, np_compact(g, mb)), f"compact W={W} n={n}"
+        if dens == 1.0 or mb.all():
+            assert np.array_equal(got, nfo.pack(g, words, lib=lib)), "all eligible: compact = positional"
+    assert nfo.pack_compact(np.ones((2, 10), np.float32), np.zeros(1, np.uint64), lib=lib).shape == (2, 0)
+
+
+def pin_slice_scales(lib):
+    rng = np.random.default_rng(22)
+    # one slice over the whole eligible region: the bucket scale of R5
+    W, n = 5, 3000
+    g = rng.normal(0, 1e-3, (W, n)).astype(np.float32)
+    off, ln = np.array([700]), np.array([1800])
+    mb = np.zeros(n, bool)
+    mb[700:2500] = True
+    words = np.packbits(np.concatenate([mb, np.zeros((-n) % 64, bool)]).astype(np.uint8),
+                        bitorder="little").view(np.uint64)
+    st = nfo.health(g, words, lib=lib)
+    _, sc = nfo.slice_scales(g, off, ln, lib=lib)
+    assert sc[0] == nfo.scale(st, 1800, lib=lib), "one slice = bucket scale"
+    # constant |g| = a on a slice: scale a exactly
+    g2 = np.where(rng.random((W, n)) < 0.5, 0.375, -0.375).astype(np.float32)
+    _, sc = nfo.slice_scales(g2, [0, 100, 2999], [50, 900, 1], lib=lib)
+    assert np.all(sc == np.float32(0.375)), "constant magnitude"
+    # dyadic values: FP64 sums exact; the scale is the exact rational rounded once
+    g3 = (rng.integers(-64, 65, (3, 200)) / 64.0).astype(np.float32)
+    offs, lens = np.array([0, 10, 150]), np.array([7, 120, 50])
+    sums, sc = nfo.slice_scales(g3, offs, lens, lib=lib)
+    for s_ in range(3):
+        exact = [sum(Fraction(abs(float(x))) for x in g3[w, offs[s_]:offs[s_] + lens[s_]]) for w in range(3)]
+        assert all(sums[s_, w] == float(exact[w]) for w in range(3)), "exact slice sums"
+        want = f32_round(sum(e / lens[s_] for e in exact) / 3)
+        got = sc[s_]
+        # the oracle divides and adds in FP64 (R31): within one FP32 rounding of the exact value
+        assert got == want or abs(float(got) - float(want)) <= np.spacing(np.float32(want)), "slice scale"
+
+
+def pin_sliced_output(lib):
+    rng = np.random.default_rng(23)
+    W, n = 6, 5000
+    g = rng.normal(0, 1e-3, (W, n)).astype(np.float32)
+    offs, lens = np.array([100, 900, 4000]), np.array([800, 2500, 999])  # slices 0 and 1 adjacent
+    mb = np.zeros(n, bool)
+    for o, l in zip(offs, lens):
+        mb[o:o + l] = True
+    words = np.packbits(np.concatenate([mb, np.zeros((-n) % 64, bool)]).astype(np.uint8),
+                        bitorder="little").view(np.uint64)
+    bits = nfo.pack(g, words, lib=lib)
+    c = nfo.counts(bits, n, lib=lib)
+    y = nfo.fp32_path(g, lib=lib)
+    q = nfo.decode_table(W, lib=lib)
+    scales = np.array([1.5e-4, 2.5e-3, 7.0e-1], dtype=np.float32)
+    out = nfo.sliced_output(words, c, y, q, offs, lens, scales, lib=lib)
+    for o, l, sc in zip(offs, lens, scales):
+        assert np.array_equal(out[o:o + l], (sc * q[c[o:o + l]]).astype(np.float32)), "slice decode"
+    assert np.array_equal(out[~mb], y[~mb]), "routed positions carry the FP32 path"
+    # one slice with the bucket scale reproduces the G-Binary bucket output
+    r = nfo.reduce_bucket(g[:, 1000:3500], np.packbits(np.ones(2500 + (-2500) % 64, np.uint8)[:2560],
+                                                      bitorder="little").view(np.uint64), lib=lib)
+    gs = g[:, 1000:3500]
+    m1 = np.packbits(np.concatenate([np.ones(2500, bool), np.zeros(60, bool)]).astype(np.uint8),
+                     bitorder="little").view(np.uint64)
+    _, sc1 = nfo.slice_scales(gs, [0], [2500], lib=lib)
+    o1 = nfo.sliced_output(m1, r["counts"], nfo.fp32_path(gs, lib=lib), q, [0], [2500], sc1, lib=lib)
+    assert sc1[0] == np.float32(r["decision"].scale) and np.array_equal(o1, r["out"]), "one slice = G-Binary"
+    # a route other than L gives the FP32 path everywhere
+    assert np.array_equal(nfo.sliced_output(words, c, y, q, offs, lens, scales, route=nfo.ROUTE_F, lib=lib), y)
+
+
 ALL_PINS = [pin_mask_from_segments, pin_pack_bruteforce, pin_counts_invariants, pin_fp32_path,
             pin_health, pin_scale, pin_decode_table, pin_whole_bucket_bruteforce,
             pin_appendix_example, pin_w1, pin_negation, pin_scaling, pin_all_fp32_mask,
@@ -810,7 +908,7 @@ ALL_PINS = [pin_mask_from_segments, pin_pack_bruteforce, pin_counts_invariants, 
             pin_route_correctness, pin_health_routes,
             pin_ternary_threshold, pin_pack_ternary_bruteforce, pin_ternary_decode_table,
             pin_ternary_tau0_is_binary, pin_ternary_gate_all, pin_ternary_whole_bucket,
-            pin_ternary_negation]
+            pin_ternary_negation, pin_pack_compact, pin_slice_scales, pin_sliced_output]
 
 
 def run_all(lib):

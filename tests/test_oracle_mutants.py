@@ -93,6 +93,18 @@ MUTANTS = [
     ("tern_majority_tie", "q[d + W] = d > 0 ? 1.0f", "q[d + W] = d >= 0 ? 1.0f"),
     ("tern_counts_neg_from_pos", "nfo_counts(neg, bits_stride, W, n, cneg);", "nfo_counts(pos, bits_stride, W, n, cneg);"),
     ("tern_decode_by_reciprocal", "q[d + W] = (float)d / (float)W;", "q[d + W] = (float)d * (1.0f / (float)W);"),
+    # compacted payload and per-slice scales (R29-R33)
+    ("compact_positional_rank", "      if (!mask_bit(mask, i)) continue;\n      if (row[i] > 0.0f) crow[r / 64]",
+     "      if (row[i] > 0.0f && mask_bit(mask, i)) crow[r / 64]"),
+    ("compact_sign_ge", "if (row[i] > 0.0f) crow[r / 64]", "if (row[i] >= 0.0f) crow[r / 64]"),
+    ("compact_msb_first", "crow[r / 64] |= (uint64_t)1 << (r % 64);", "crow[r / 64] |= (uint64_t)1 << (63 - r % 64);"),
+    ("slice_sum_signed", "for (int64_t j = 0; j < len[s]; ++j) t += fabs((double)row[j]);",
+     "for (int64_t j = 0; j < len[s]; ++j) t += (double)row[j];"),
+    ("slice_mean_missing", "acc += t / (double)len[s];", "acc += t;"),
+    ("slice_workers_not_averaged", "scales[s] = (float)(acc / (double)W);", "scales[s] = (float)acc;"),
+    ("slice_skips_last", "for (int64_t j = 0; j < len[s]; ++j) t +=", "for (int64_t j = 0; j + 1 < len[s]; ++j) t +="),
+    ("sliced_boundary_off_by_one", "while (s < S && i >= off[s] + len[s]) ++s;", "while (s < S && i > off[s] + len[s]) ++s;"),
+    ("sliced_first_scale_only", "out[i] = scales[s] * q[counts[i]];", "out[i] = scales[0] * q[counts[i]];"),
 ]
 
 
