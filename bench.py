@@ -56,6 +56,8 @@ def parse():
                     help="only run the copy kernel of known traffic (counter calibration)")
     ap.add_argument("--contrast", action="store_true",
                     help="only time hierarchical vs stock vs direct sign counting (one JSON line per shape)")
+    ap.add_argument("--sliced", action="store_true",
+                    help="only time the compacted payload and per-slice scale kernels on the workload")
     ap.add_argument("--controller", type=int, default=0, metavar="STEPS",
                     help="only run STEPS controller-driven reducer steps (Supervisor + endpoint guard feeding "
                          "the route policy) on the chosen workload and report route evidence")
@@ -273,6 +275,69 @@ def controller_run(args):
     return 0
 
 
+def sliced_run(args, reps=5):
+    """Kernel times of the compacted eligible-only payload and per-slice scales over the whole
+    workload (every eligible tensor of the binding is one slice): compaction of the positional sign
+    rows, the per-slice statistics and scales, and the count + decode from the compacted rows."""
+    import numpy as np
+    import torch
+    import paper_2606_25759_amd as nf
+    import synth
+
+    dev = torch.device("cuda:0")
+    lay = synth.CONFIGS[args.workload]()
+    W, n, bn, nb = lay.W, lay.n_total, lay.bucket_n, lay.nb
+    nw = (n + 63) // 64
+    grads = torch.empty((W, lay.stride), dtype=torch.float32, device=dev)
+    synth.generate_device(lay, grads)
+    off, ln, el = synth.mask_segments(lay)
+    e = np.asarray(el, bool)
+    sl = nf.SlicedLayout(np.asarray(off)[e], np.asarray(ln)[e], n, device=dev)
+    mask = sl.d_mask
+    bits = torch.empty((W, nw), dtype=torch.int64, device=dev)
+    out = torch.empty(n, dtype=torch.float32, device=dev)
+    stats = torch.empty(nb * W * nf.STATS_BYTES, dtype=torch.uint8, device=dev)
+    dec = torch.empty(nb * nf.DECISION_BYTES, dtype=torch.uint8, device=dev)
+    ws = nf.empty_workspace(nf.nf_workspace_bytes_buckets(W, n, bn), dev)
+    nf.nf_route_buckets(grads, n, bn, mask, nf.policy(force_lowbit=1), bits, None, out, stats, dec, ws)
+    nwc = (sl.n_eligible + 63) // 64
+    cbits = torch.empty((W, nwc), dtype=torch.int64, device=dev)
+    sums = torch.empty((sl.S, W), dtype=torch.float64, device=dev)
+    scales = torch.empty(sl.S, dtype=torch.float32, device=dev)
+    ws2 = nf.empty_workspace(nf.nf_slice_workspace_bytes(W, sl.segments), dev)
+    counts_c = torch.empty(sl.n_eligible, dtype=torch.uint8, device=dev)
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps  # ms per call
+
+    t_compact = timed(lambda: nf.nf_compact_signs(bits, W, n, sl, cbits))
+    t_scales = timed(lambda: nf.nf_slice_scales(grads, sl, sums, scales, ws2))
+    t_reduce = timed(lambda: nf.nf_compact_signcount_reduce(cbits, W, sl, scales, 0, counts_c, out))
+    nE, S = sl.n_eligible, sl.S
+    b_compact = 8 * W * nw + 16 * nw + 8 * W * nwc          # positional rows, mask + prefix, compacted rows
+    b_scales = 4 * W * nE                                  # the eligible gradients once
+    b_reduce = 8 * W * nwc + nE + nE + 20 * nw + 4 * nE    # rows, counts out and in, tables, decoded values
+    gbs = lambda b, t: round(b / (t * 1e-3) / 1e9, 1)
+    rec = {"metric": "compacted payload and per-slice scales, kernel times", "unit": "ms",
+           "config": {"workload": lay.name, "W": W, "n": n, "n_eligible": nE, "slices": S},
+           "compact_ms": round(t_compact, 4), "compact_gbs": gbs(b_compact, t_compact),
+           "slice_scales_ms": round(t_scales, 4), "slice_scales_gbs": gbs(b_scales, t_scales),
+           "compact_reduce_ms": round(t_reduce, 4), "compact_reduce_gbs": gbs(b_reduce, t_reduce),
+           "payload_bytes_per_worker": {"positional": 8 * nw, "compacted": 8 * nwc},
+           "mgtr_sliced_compacted": round((nE / 8 + 4 * S + 4 * (n - nE)) / (4 * n), 5),
+           "mgtr_bucket_scale_positional_bits": round((nw * 8 + 4 * nb + 4 * (n - nE)) / (4 * n), 5)}
+    print(json.dumps(rec), flush=True)
+    return 0
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -292,6 +357,8 @@ def main():
         return contrast()
     if args.controller:
         return controller_run(args)
+    if args.sliced:
+        return sliced_run(args)
 
     import paper_2606_25759_amd as nf
     import synth

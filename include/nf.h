@@ -232,6 +232,87 @@ nf_status nf_stock_signcount(const uint64_t* bits, int64_t bits_stride_words, in
                              int32_t replicas, uint8_t* counts, float* out, int64_t replica_stride,
                              void* stream);
 
+/* ------------------------------------------------------------------------
+ * Per-slice scales and the compacted eligible-only payload.  §5.2 records a
+ * mean-absolute scale for the eligible slices and §6.1 counts bit-packed
+ * updates; the paper fixes neither the scale's granularity nor the
+ * payload's layout.  Here:
+ *   - the bucket's eligible slices are S intervals [off[s], off[s] +
+ *     len[s]), sorted, disjoint and non-empty (one per eligible parameter
+ *     slice of the binding, §5.1); the mask is their union;
+ *   - the compacted payload of worker w holds bit r = (g > 0) of the r-th
+ *     eligible element in element order, r = 0 .. n_E - 1 (ceil(n_E / 64)
+ *     LSB-first words, padding 0): exactly n_E payload bits per worker;
+ *   - scale_s = fl32((sum over workers, in order, of S_sw / len[s]) / W),
+ *     S_sw the FP64 sum of |g| of worker w over slice s (the bucket scale's
+ *     rule on one slice); the decoded value at an eligible element i of
+ *     slice s is fl32(scale_s * q[c_i]).
+ * ------------------------------------------------------------------------ */
+
+/* Sizes of a slice table (host): n_E = sum of len[s]; segments = the number
+ * of statistics segments, sum of ceil(len[s] / 65536). */
+nf_status nf_sliced_layout_sizes(const int64_t* len_host, int64_t S, int64_t* n_eligible_host,
+                                 int64_t* segments_host);
+
+/*
+ * Layout tables of a slice table over n elements (host; built once per
+ * binding, like the mask).  Slices outside [0, n), unsorted, overlapping or
+ * empty give NF_ERR_INVALID_ARG.  Writes, into caller-allocated host arrays
+ * (nw = ceil(n / 64), nwc = ceil(n_E / 64)):
+ *   mask_host[nw]       the eligibility mask, the union of the slices
+ *   prefix_host[nw + 1] eligible elements before word k (prefix[nw] = n_E)
+ *   start_host[nwc]     the word holding compacted rank 64 o
+ *   wslice_host[nw]     the slice holding word k's first eligible element
+ *                       (S when the word has none)
+ *   rstart_host[S + 1]  compacted rank of slice s's first element
+ *                       (rstart[S] = n_E)
+ *   segp_host[S + 1]    first statistics segment of slice s
+ */
+nf_status nf_sliced_layout(const int64_t* off_host, const int64_t* len_host, int64_t S, int64_t n,
+                           uint64_t* mask_host, uint64_t* prefix_host, int64_t* start_host,
+                           int32_t* wslice_host, int64_t* rstart_host, int64_t* segp_host);
+
+/*
+ * Compaction of the positional sign payload (rows of nf_pack_signs) into
+ * the compacted payload: for each of the W rows, cbits row w (at cbits + w *
+ * cbits_stride_words, cbits_stride_words >= ceil(n_E / 64)) receives the
+ * bits of the eligible positions in order.  mask, prefix and start: device
+ * copies of the layout tables; n_eligible = prefix[nw].  No workspace.
+ */
+nf_status nf_compact_signs(const uint64_t* bits, int64_t bits_stride_words, int32_t W, int64_t n,
+                           const uint64_t* mask, const uint64_t* prefix, const int64_t* start,
+                           int64_t n_eligible, uint64_t* cbits, int64_t cbits_stride_words,
+                           void* stream);
+
+/* Workspace bytes of nf_slice_scales for W workers and `segments`. */
+size_t nf_slice_workspace_bytes(int32_t W, int64_t segments);
+
+/*
+ * Per-slice statistics and scales: sums[s * W + w] = S_sw (FP64, in a fixed
+ * order: per 65,536-element segment, then the segments in order; within
+ * 1e-12 relative of a sequential sum) and scales[s] = scale_s (device
+ * arrays).  off, len, segp: device copies of the slice table and of
+ * segp_host; grads as for nf_bucket_health (4-byte alignment suffices).
+ * Reads the eligible elements once.
+ */
+nf_status nf_slice_scales(const float* grads, int64_t worker_stride, int32_t W, const int64_t* off,
+                          const int64_t* len, const int64_t* segp, int64_t S, int64_t segments,
+                          double* sums, float* scales, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Read side over the compacted payload (§3.3 step 7 with per-slice scales):
+ * counts_c[r] = sum over the W compacted rows of bit r (n_E bytes, in
+ * compacted order; required), then, when out is not NULL, out[i] =
+ * fl32(scales[s] * q[c]) at every eligible element i (slice s, count c of
+ * its rank), other positions untouched; q as nf_signcount_reduce's.  mask,
+ * prefix, wslice, rstart: device copies of the layout tables.  No workspace.
+ */
+nf_status nf_compact_signcount_reduce(const uint64_t* cbits, int64_t cbits_stride_words, int32_t W,
+                                      int64_t n, const uint64_t* mask, const uint64_t* prefix,
+                                      const int32_t* wslice, const int64_t* rstart, int64_t S,
+                                      int64_t n_eligible, const float* scales, int32_t decode_mode,
+                                      uint8_t* counts_c, float* out, void* stream);
+
 /*
  * G-Ternary write-side threshold (§2.2's zero gating, applied before
  * aggregation; host, pure function): for each worker w,

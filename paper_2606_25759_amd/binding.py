@@ -34,7 +34,9 @@ EXPORTS = ["nf_abi_version", "nf_last_error", "nf_mask_from_segments", "nf_works
            "nf_route_decide", "nf_route_bucket", "nf_workspace_bytes_buckets", "nf_route_buckets",
            "nf_set_phase_events", "nf_pass1_launches", "nf_ternary_threshold", "nf_pack_ternary",
            "nf_ternary_reduce", "nf_partial_counts", "nf_partial_count_reduce", "nf_stock_signcount",
-           "nf_supervisor_init", "nf_supervisor_policy", "nf_supervisor_update", "nf_endpoint_guard"]
+           "nf_supervisor_init", "nf_supervisor_policy", "nf_supervisor_update", "nf_endpoint_guard",
+           "nf_sliced_layout_sizes", "nf_sliced_layout", "nf_compact_signs", "nf_slice_workspace_bytes",
+           "nf_slice_scales", "nf_compact_signcount_reduce"]
 NF_SUP_WARMUP, NF_SUP_LOWBIT, NF_SUP_COOLDOWN, NF_SUP_GUARD = 0, 1, 2, 3
 
 
@@ -141,6 +143,13 @@ def load(path=None):
         "nf_supervisor_policy": (ctypes.c_int, [_P, _P, _P]),
         "nf_supervisor_update": (ctypes.c_int, [_P, _P, _P, _I64, ctypes.c_double]),
         "nf_endpoint_guard": (ctypes.c_int, [_P, _I64, _I64, _P, _P, _P]),
+        "nf_sliced_layout_sizes": (ctypes.c_int, [_P, _I64, _P, _P]),
+        "nf_sliced_layout": (ctypes.c_int, [_P, _P, _I64, _I64, _P, _P, _P, _P, _P, _P]),
+        "nf_compact_signs": (ctypes.c_int, [_P, _I64, _I32, _I64, _P, _P, _P, _I64, _P, _I64, _P]),
+        "nf_slice_workspace_bytes": (_SZ, [_I32, _I64]),
+        "nf_slice_scales": (ctypes.c_int, [_P, _I64, _I32, _P, _P, _P, _I64, _I64, _P, _P, _P, _SZ, _P]),
+        "nf_compact_signcount_reduce": (ctypes.c_int, [_P, _I64, _I32, _I64, _P, _P, _P, _P, _I64, _I64, _P,
+                                                        _I32, _P, _P, _P]),
     }
     for name, (res, args) in sigs.items():
         fn = getattr(lib, name)
@@ -343,6 +352,73 @@ def nf_stock_signcount(bits, W, n, mask, scale, decode_mode, replicas, counts, o
     _check(load().nf_stock_signcount(b, bstride, W, n, _words(mask), _dev_ptr(scale, torch.float32, "scale"),
                                      decode_mode, replicas, _dev_ptr(counts, torch.uint8, "counts"),
                                      _dev_ptr(out, torch.float32, "out"), replica_stride, _stream(stream)))
+
+
+class SlicedLayout:
+    """Host layout tables of a slice table (nf_sliced_layout) and their device copies."""
+
+    def __init__(self, off, length, n, device=None):
+        self.off = np.ascontiguousarray(off, dtype=np.int64)
+        self.len = np.ascontiguousarray(length, dtype=np.int64)
+        self.S, self.n = len(self.off), int(n)
+        ne, seg = ctypes.c_int64(), ctypes.c_int64()
+        _check(load().nf_sliced_layout_sizes(self.len.ctypes.data if self.S else None, self.S, ctypes.byref(ne),
+                                             ctypes.byref(seg)))
+        self.n_eligible, self.segments = ne.value, seg.value
+        nw = (self.n + 63) // 64
+        self.mask = np.zeros(max(nw, 1), np.uint64)
+        self.prefix = np.zeros(nw + 1, np.uint64)
+        self.start = np.zeros(max((self.n_eligible + 63) // 64, 1), np.int64)
+        self.wslice = np.zeros(max(nw, 1), np.int32)
+        self.rstart = np.zeros(self.S + 1, np.int64)
+        self.segp = np.zeros(self.S + 1, np.int64)
+        _check(load().nf_sliced_layout(self.off.ctypes.data if self.S else None,
+                                       self.len.ctypes.data if self.S else None, self.S, self.n,
+                                       self.mask.ctypes.data, self.prefix.ctypes.data, self.start.ctypes.data,
+                                       self.wslice.ctypes.data, self.rstart.ctypes.data, self.segp.ctypes.data))
+        self.mask = self.mask[:nw]
+        if device is not None:
+            self.to(device)
+
+    def to(self, device):
+        t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(device)
+        self.d_mask = t(self.mask.view(np.int64)) if len(self.mask) else torch.zeros(1, dtype=torch.int64, device=device)
+        self.d_prefix = t(self.prefix.view(np.int64))
+        self.d_start = t(self.start)
+        self.d_wslice = t(self.wslice)
+        self.d_rstart = t(self.rstart)
+        self.d_segp = t(self.segp)
+        self.d_off = t(self.off) if self.S else torch.zeros(1, dtype=torch.int64, device=device)
+        self.d_len = t(self.len) if self.S else torch.zeros(1, dtype=torch.int64, device=device)
+        return self
+
+
+def nf_compact_signs(bits, W, n, lay, cbits, stream=None):
+    b, bstride = _bits_rows(bits)
+    c, cstride = _bits_rows(cbits)
+    _check(load().nf_compact_signs(b, bstride, W, n, _words(lay.d_mask), lay.d_prefix.data_ptr(),
+                                   lay.d_start.data_ptr(), lay.n_eligible, c, cstride, _stream(stream)))
+
+
+def nf_slice_workspace_bytes(W, segments):
+    return int(load().nf_slice_workspace_bytes(W, segments))
+
+
+def nf_slice_scales(grads, lay, sums, scales, ws, stream=None):
+    g, stride, W = _rows(grads)
+    _check(load().nf_slice_scales(g, stride, W, lay.d_off.data_ptr(), lay.d_len.data_ptr(), lay.d_segp.data_ptr(),
+                                  lay.S, lay.segments, _dev_ptr(sums, torch.float64, "sums"),
+                                  _dev_ptr(scales, torch.float32, "scales"), _dev_ptr(ws, torch.uint8, "ws"),
+                                  ws.numel(), _stream(stream)))
+
+
+def nf_compact_signcount_reduce(cbits, W, lay, scales, decode_mode, counts_c, out, stream=None):
+    c, cstride = _bits_rows(cbits)
+    _check(load().nf_compact_signcount_reduce(c, cstride, W, lay.n, _words(lay.d_mask), lay.d_prefix.data_ptr(),
+                                              lay.d_wslice.data_ptr(), lay.d_rstart.data_ptr(), lay.S,
+                                              lay.n_eligible, _dev_ptr(scales, torch.float32, "scales"),
+                                              decode_mode, _dev_ptr(counts_c, torch.uint8, "counts_c"),
+                                              _dev_ptr(out, torch.float32, "out"), _stream(stream)))
 
 
 def nf_ternary_threshold(stats, n_eligible, tau):

@@ -502,6 +502,177 @@ nf_status nf_stock_signcount(const uint64_t* bits, int64_t bits_stride_words, in
   return ok();
 }
 
+nf_status nf_sliced_layout_sizes(const int64_t* len_host, int64_t S, int64_t* n_eligible_host,
+                                 int64_t* segments_host) {
+  if (S < 0 || (S > 0 && !len_host) || !n_eligible_host || !segments_host)
+    return fail(NF_ERR_INVALID_ARG, "S < 0 or NULL arrays");
+  int64_t ne = 0, seg = 0;
+  for (int64_t s = 0; s < S; ++s) {
+    if (len_host[s] < 1) return fail(NF_ERR_INVALID_ARG, "slice %lld has length < 1", (long long)s);
+    ne += len_host[s];
+    seg += nf::ceil_div(len_host[s], nf::kSliceSeg);
+  }
+  *n_eligible_host = ne;
+  *segments_host = seg;
+  return ok();
+}
+
+nf_status nf_sliced_layout(const int64_t* off_host, const int64_t* len_host, int64_t S, int64_t n,
+                           uint64_t* mask_host, uint64_t* prefix_host, int64_t* start_host,
+                           int32_t* wslice_host, int64_t* rstart_host, int64_t* segp_host) {
+  if (S < 0 || n < 0) return fail(NF_ERR_INVALID_ARG, "negative S or n");
+  if (S > 0 && (!off_host || !len_host)) return fail(NF_ERR_INVALID_ARG, "slice arrays are NULL");
+  if (S >= (int64_t)1 << 31) return fail(NF_ERR_INVALID_ARG, "too many slices");
+  const int64_t nw = (n + 63) / 64;
+  if (!prefix_host || !rstart_host || !segp_host || (nw > 0 && (!mask_host || !wslice_host)) ||
+      (S > 0 && !start_host))
+    return fail(NF_ERR_INVALID_ARG, "output arrays are NULL");
+  int64_t end = 0;
+  for (int64_t s = 0; s < S; ++s) {
+    if (len_host[s] < 1 || off_host[s] < end || off_host[s] > n - len_host[s])
+      return fail(NF_ERR_INVALID_ARG, "slice %lld [%lld, +%lld): slices must be sorted, disjoint, non-empty, inside [0, %lld)",
+                  (long long)s, (long long)off_host[s], (long long)len_host[s], (long long)n);
+    end = off_host[s] + len_host[s];
+  }
+  // mask: the union of the slices
+  memset(mask_host, 0, (size_t)nw * sizeof(uint64_t));
+  for (int64_t s = 0; s < S; ++s)
+    for (int64_t i = off_host[s]; i < off_host[s] + len_host[s];) {
+      const int64_t k = i / 64, b = i % 64;
+      const int64_t take = (64 - b) < (off_host[s] + len_host[s] - i) ? (64 - b) : (off_host[s] + len_host[s] - i);
+      mask_host[k] |= (take == 64 ? ~0ull : ((1ull << take) - 1ull)) << b;
+      i += take;
+    }
+  // eligible elements before each word, and the word holding every 64th rank
+  uint64_t acc = 0;
+  int64_t o = 0;
+  for (int64_t k = 0; k < nw; ++k) {
+    prefix_host[k] = acc;
+    const uint64_t next = acc + (uint64_t)__builtin_popcountll(mask_host[k]);
+    for (; (uint64_t)(64 * o) < next; ++o) start_host[o] = k;
+    acc = next;
+  }
+  prefix_host[nw] = acc;
+  // slice of each word's first eligible element
+  int64_t s = 0;
+  for (int64_t k = 0; k < nw; ++k) {
+    while (s < S && off_host[s] + len_host[s] <= 64 * k) ++s;
+    wslice_host[k] = (int32_t)((s < S && off_host[s] < 64 * (k + 1)) ? s : S);
+  }
+  // compacted start of each slice and its first statistics segment
+  rstart_host[0] = 0;
+  segp_host[0] = 0;
+  for (int64_t t = 0; t < S; ++t) {
+    rstart_host[t + 1] = rstart_host[t] + len_host[t];
+    segp_host[t + 1] = segp_host[t] + nf::ceil_div(len_host[t], nf::kSliceSeg);
+  }
+  return ok();
+}
+
+nf_status nf_compact_signs(const uint64_t* bits, int64_t bits_stride_words, int32_t W, int64_t n,
+                           const uint64_t* mask, const uint64_t* prefix, const int64_t* start,
+                           int64_t n_eligible, uint64_t* cbits, int64_t cbits_stride_words,
+                           void* stream) {
+  if (W < 1 || W > 255) return fail(NF_ERR_INVALID_ARG, "W=%d outside [1, 255]", W);
+  if (n < 0 || n_eligible < 0 || n_eligible > n) return fail(NF_ERR_INVALID_ARG, "need 0 <= n_eligible <= n");
+  NF_TRY(check_bits(bits, bits_stride_words, n, W));
+  NF_TRY(check_mask(mask, n));
+  if (n_eligible > 0 && (!prefix || !start || !cbits)) return fail(NF_ERR_INVALID_ARG, "NULL layout table or output");
+  if (!aligned(cbits, 8) || !aligned(prefix, 8) || !aligned(start, 8)) return fail(NF_ERR_ALIGNMENT, "8-byte alignment");
+  if (cbits_stride_words < (n_eligible + 63) / 64) return fail(NF_ERR_INVALID_ARG, "cbits_stride_words < ceil(n_E/64)");
+  if (n_eligible == 0) return ok();
+  nf::CompactArgs a;
+  a.bits = bits;
+  a.bstride = bits_stride_words;
+  a.mask = mask;
+  a.prefix = prefix;
+  a.start = start;
+  a.cbits = cbits;
+  a.cstride = cbits_stride_words;
+  a.n = n;
+  a.n_eligible = n_eligible;
+  hipError_t e = nf::launch_compact(a, W, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "compact launch");
+  return ok();
+}
+
+size_t nf_slice_workspace_bytes(int32_t W, int64_t segments) {
+  if (W < 1 || W > 255 || segments < 0) return 0;
+  return nf::align256((size_t)segments * (size_t)W * sizeof(double));
+}
+
+nf_status nf_slice_scales(const float* grads, int64_t worker_stride, int32_t W, const int64_t* off,
+                          const int64_t* len, const int64_t* segp, int64_t S, int64_t segments,
+                          double* sums, float* scales, void* ws, size_t ws_bytes, void* stream) {
+  if (W < 1 || W > 255) return fail(NF_ERR_INVALID_ARG, "W=%d outside [1, 255]", W);
+  if (S < 0 || segments < S || segments > 0x7fffffff) return fail(NF_ERR_INVALID_ARG, "need 0 <= S <= segments < 2^31");
+  if (S == 0) return ok();
+  if (!grads || !off || !len || !segp || !sums || !scales) return fail(NF_ERR_INVALID_ARG, "NULL argument");
+  if (!aligned(grads, 4) || !aligned(sums, 8) || !aligned(scales, 4) || !aligned(off, 8) || !aligned(len, 8) ||
+      !aligned(segp, 8))
+    return fail(NF_ERR_ALIGNMENT, "misaligned argument");
+  NF_TRY(check_ws(ws, ws_bytes, nf_slice_workspace_bytes(W, segments)));
+  nf::SliceArgs a;
+  a.g = grads;
+  a.wstride = worker_stride;
+  a.off = off;
+  a.len = len;
+  a.segp = segp;
+  a.part = static_cast<double*>(ws);
+  a.sums = sums;
+  a.scales = scales;
+  a.S = S;
+  a.W = W;
+  hipError_t e = nf::launch_slice_scales(a, segments, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "slice scale launch");
+  return ok();
+}
+
+nf_status nf_compact_signcount_reduce(const uint64_t* cbits, int64_t cbits_stride_words, int32_t W,
+                                      int64_t n, const uint64_t* mask, const uint64_t* prefix,
+                                      const int32_t* wslice, const int64_t* rstart, int64_t S,
+                                      int64_t n_eligible, const float* scales, int32_t decode_mode,
+                                      uint8_t* counts_c, float* out, void* stream) {
+  if (W < 1 || W > 255) return fail(NF_ERR_INVALID_ARG, "W=%d outside [1, 255]", W);
+  if (n < 0 || n_eligible < 0 || n_eligible > n || S < 0) return fail(NF_ERR_INVALID_ARG, "need 0 <= n_eligible <= n, S >= 0");
+  if (decode_mode != NF_DECODE_SOFT && decode_mode != NF_DECODE_MAJORITY)
+    return fail(NF_ERR_INVALID_ARG, "decode_mode=%d", decode_mode);
+  if (n_eligible == 0) return ok();
+  NF_TRY(check_bits(cbits, cbits_stride_words, n_eligible, W));
+  if (!counts_c) return fail(NF_ERR_INVALID_ARG, "counts_c is NULL");
+  if (out) {
+    NF_TRY(check_mask(mask, n));
+    if (S < 1 || !prefix || !wslice || !rstart || !scales) return fail(NF_ERR_INVALID_ARG, "NULL layout table or scales");
+    if (!aligned(out, 4) || !aligned(prefix, 8) || !aligned(rstart, 8) || !aligned(wslice, 4) || !aligned(scales, 4))
+      return fail(NF_ERR_ALIGNMENT, "misaligned argument");
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const nf::Geometry geo = nf::make_geometry(W, n_eligible, n_eligible);
+  nf::Pass2Args p = pass2_args(geo);
+  p.bits = cbits;
+  p.bstride = cbits_stride_words;
+  p.counts = counts_c;
+  p.op = nf::kOpCountDecode;
+  hipError_t e = nf::launch_pass2(geo, p, s);
+  if (e != hipSuccess) return hip_fail(e, "compacted count launch");
+  if (!out) return ok();
+  nf::ExpandArgs x;
+  x.mask = mask;
+  x.prefix = prefix;
+  x.wslice = wslice;
+  x.rstart = rstart;
+  x.scales = scales;
+  x.counts_c = counts_c;
+  x.out = out;
+  x.n = n;
+  x.S = S;
+  x.W = W;
+  x.decode_mode = decode_mode;
+  e = nf::launch_cexpand(x, s);
+  if (e != hipSuccess) return hip_fail(e, "sliced decode launch");
+  return ok();
+}
+
 nf_status nf_ternary_threshold(const nf_worker_stats* stats_host, int32_t W, int64_t n_eligible,
                                float tau, float* theta_host) {
   if (W < 1 || W > 255) return fail(NF_ERR_INVALID_ARG, "W=%d outside [1, 255]", W);

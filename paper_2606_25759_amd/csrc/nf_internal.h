@@ -305,6 +305,49 @@ NF_HD inline float decode_q(int c, int W, int mode) {
   return (float)margin / (float)W;
 }
 
+// Per-slice scales and the compacted payload (nf_sliced.hip).
+constexpr int64_t kSliceSeg = 65536;  // elements per statistics segment of a slice
+
+struct CompactArgs {
+  const uint64_t* bits;     // positional rows
+  int64_t bstride;
+  const uint64_t* mask;
+  const uint64_t* prefix;   // [nw + 1] eligible elements before word k
+  const int64_t* start;     // [ceil(n_E / 64)] word holding rank 64 o
+  uint64_t* cbits;          // compacted rows
+  int64_t cstride;
+  int64_t n, n_eligible;
+};
+
+struct SliceArgs {
+  const float* g;
+  int64_t wstride;
+  const int64_t* off;       // [S]
+  const int64_t* len;       // [S]
+  const int64_t* segp;      // [S + 1] first segment of slice s
+  double* part;             // [segments][W] workspace
+  double* sums;             // [S][W]
+  float* scales;            // [S]
+  int64_t S;
+  int32_t W;
+};
+
+struct ExpandArgs {
+  const uint64_t* mask;
+  const uint64_t* prefix;   // [nw + 1]
+  const int32_t* wslice;    // [nw]
+  const int64_t* rstart;    // [S + 1]
+  const float* scales;      // [S]
+  const uint8_t* counts_c;  // [n_E] counts in compacted order
+  float* out;
+  int64_t n, S;
+  int32_t W, decode_mode;
+};
+
+hipError_t launch_compact(const CompactArgs& a, int W, hipStream_t s);
+hipError_t launch_slice_scales(const SliceArgs& a, int64_t segments, hipStream_t s);
+hipError_t launch_cexpand(const ExpandArgs& a, hipStream_t s);
+
 // Sets the thread-local message of nf_last_error (nf_api.hip) and returns st.
 nf_status set_error(nf_status st, const char* msg);
 
