@@ -940,7 +940,7 @@ __global__ __launch_bounds__(kThreads2) void k_pass2(
 // "eligible, not gated, g > 0" and "eligible, not gated, g < 0" are the
 // two planes' words.  The next tile's loads (and mask words) are in flight
 // while one tile is examined.  The chunk's words of both planes stay in LDS
-// and leave at its end as coalesced rows; launches of kEpochBlocks chunks
+// and leave at its end as coalesced rows; launches of pass 1's epochs
 // bring the plane stores of a launch together, as in pass 1.
 template <int WPW>
 __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <= 2 ? 8 : 4, WPW <= 2 ? 8 : 4))) void k_tpack(
@@ -1243,15 +1243,16 @@ static hipError_t pass1_dispatch(const Geometry& geo, const Pass1Args& a, hipStr
     }
     if (e != hipSuccess) return e;
   }
-  // One launch per kEpochBlocks chunks (see the geometry notes).  The first
+  // One launch per epoch of chunks (see the geometry notes).  The first
   // launch is ordered after earlier work on the stream; later ones may
   // start while the one before drains, which is safe when no two chunks of
   // a bucket share a partial slot (every chunk then writes only its own
   // slot and sign words).  The next ordered launch (decide) waits for all.
   const uint32_t overlap = geo.chunks_full <= kMaxSlots ? hipExtAnyOrderLaunch : 0u;
-  for (int64_t q0 = 0; q0 < geo.total_chunks; q0 += kEpochBlocks) {
+  const int64_t epoch = pass1_epoch(geo);
+  for (int64_t q0 = 0; q0 < geo.total_chunks; q0 += epoch) {
     const int64_t left = geo.total_chunks - q0;
-    const dim3 grid((unsigned)(left < kEpochBlocks ? left : kEpochBlocks));
+    const dim3 grid((unsigned)(left < epoch ? left : epoch));
     const uint32_t fl = q0 > 0 ? overlap : 0u;
     switch (geo.wpw) {
       case 1: hipExtLaunchKernelGGL((k_pass1<1, PACK>), grid, block, smem, s, nullptr, nullptr, fl, a.g, a.mask, a.bits, a.out, a.part, a.part_ne, a, q0); break;
@@ -1290,9 +1291,10 @@ hipError_t launch_ternary_pack(const Geometry& geo, const TernArgs& a0, hipStrea
   if (smem > 65536) return hipErrorInvalidValue;
   // No chunk shares state with another, so every launch after the first may
   // start while the one before drains.
-  for (int64_t q0 = 0; q0 < geo.total_chunks; q0 += kEpochBlocks) {
+  const int64_t epoch = one_launch_epoch(geo.total_chunks);  // chunks share no state here
+  for (int64_t q0 = 0; q0 < geo.total_chunks; q0 += epoch) {
     const int64_t left = geo.total_chunks - q0;
-    const dim3 grid((unsigned)(left < kEpochBlocks ? left : kEpochBlocks));
+    const dim3 grid((unsigned)(left < epoch ? left : epoch));
     const uint32_t fl = q0 > 0 ? hipExtAnyOrderLaunch : 0u;
     switch (geo.wpw) {
       case 1: hipExtLaunchKernelGGL((k_tpack<1>), grid, dim3(kThreads1), smem, s, nullptr, nullptr, fl, a, q0); break;
