@@ -170,6 +170,23 @@ def test_invalid_arguments_return_codes_without_launch():
         nf.NF_ERR_ALIGNMENT
     assert lib.nf_partial_count_reduce(fake, 640, 2, 8, 640, fake, None, 0, fake, fake, None) == \
         nf.NF_ERR_INVALID_ARG
+    # compacted payload and per-slice scales
+    assert lib.nf_compact_signs(fake, 10, 2, 640, fake, fake, fake, 641, fake, 11, None) == nf.NF_ERR_INVALID_ARG
+    assert lib.nf_compact_signs(fake, 10, 2, 640, fake, fake, fake, 600, fake, 9, None) == nf.NF_ERR_INVALID_ARG
+    assert lib.nf_compact_signs(fake, 10, 2, 640, fake, P(0x1004), fake, 600, fake, 10, None) == nf.NF_ERR_ALIGNMENT
+    assert lib.nf_slice_scales(fake, 640, 0, fake, fake, fake, 3, 3, fake, fake, ws, 1 << 20, None) == \
+        nf.NF_ERR_INVALID_ARG
+    assert lib.nf_slice_scales(fake, 640, 2, fake, fake, fake, 3, 2, fake, fake, ws, 1 << 20, None) == \
+        nf.NF_ERR_INVALID_ARG
+    need = nf.nf_slice_workspace_bytes(2, 3)
+    assert lib.nf_slice_scales(fake, 640, 2, fake, fake, fake, 3, 3, fake, fake, ws, need - 1, None) == \
+        nf.NF_ERR_WORKSPACE
+    assert lib.nf_compact_signcount_reduce(fake, 10, 2, 640, fake, fake, fake, fake, 2, 600, fake, 0, None, fake,
+                                           None) == nf.NF_ERR_INVALID_ARG
+    assert lib.nf_compact_signcount_reduce(fake, 10, 2, 640, fake, fake, fake, fake, 0, 600, fake, 0, fake, fake,
+                                           None) == nf.NF_ERR_INVALID_ARG
+    assert lib.nf_compact_signcount_reduce(fake, 10, 2, 640, fake, fake, fake, fake, 2, 600, fake, 7, fake, fake,
+                                           None) == nf.NF_ERR_INVALID_ARG
     # stock replicas: count and stride
     assert lib.nf_stock_signcount(fake, 10, 8, 640, fake, fake, 0, 0, fake, fake, 640, None) == \
         nf.NF_ERR_INVALID_ARG
@@ -179,6 +196,14 @@ def test_invalid_arguments_return_codes_without_launch():
     st = (nf.nf_worker_stats * 2)()
     d = nf.nf_route_decision()
     assert lib.nf_route_decide(st, 2, 10, 11, ctypes.byref(pol), ctypes.byref(d)) == nf.NF_ERR_INVALID_ARG
+
+
+def test_sliced_sizes():
+    ne, seg = ctypes.c_int64(), ctypes.c_int64()
+    ln = np.array([1, 65536, 65537, 200_000], dtype=np.int64)
+    assert nf.load().nf_sliced_layout_sizes(ln.ctypes.data, 4, ctypes.byref(ne), ctypes.byref(seg)) == nf.NF_OK
+    assert ne.value == int(ln.sum()) and seg.value == 1 + 1 + 2 + 4
+    assert nf.nf_slice_workspace_bytes(16, 8) == 1024 and nf.nf_slice_workspace_bytes(0, 8) == 0
 
 
 def test_workspace_sizes():
