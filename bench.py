@@ -321,6 +321,7 @@ def sliced_run(args, reps=5):
     t_compact = timed(lambda: nf.nf_compact_signs(bits, W, n, sl, cbits))
     t_scales = timed(lambda: nf.nf_slice_scales(grads, sl, sums, scales, ws2))
     t_reduce = timed(lambda: nf.nf_compact_signcount_reduce(cbits, W, sl, scales, 0, counts_c, out))
+    t_count = timed(lambda: nf.nf_compact_signcount_reduce(cbits, W, sl, scales, 0, counts_c, None))
     nE, S = sl.n_eligible, sl.S
     b_compact = 8 * W * nw + 16 * nw + 8 * W * nwc          # positional rows, mask + prefix, compacted rows
     b_scales = 4 * W * nE                                  # the eligible gradients once
@@ -331,6 +332,7 @@ def sliced_run(args, reps=5):
            "compact_ms": round(t_compact, 4), "compact_gbs": gbs(b_compact, t_compact),
            "slice_scales_ms": round(t_scales, 4), "slice_scales_gbs": gbs(b_scales, t_scales),
            "compact_reduce_ms": round(t_reduce, 4), "compact_reduce_gbs": gbs(b_reduce, t_reduce),
+           "of_which_count_ms": round(t_count, 4),
            "payload_bytes_per_worker": {"positional": 8 * nw, "compacted": 8 * nwc},
            "mgtr_sliced_compacted": round((nE / 8 + 4 * S + 4 * (n - nE)) / (4 * n), 5),
            "mgtr_bucket_scale_positional_bits": round((nw * 8 + 4 * nb + 4 * (n - nE)) / (4 * n), 5)}

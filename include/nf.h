@@ -302,7 +302,7 @@ nf_status nf_slice_scales(const float* grads, int64_t worker_stride, int32_t W, 
 /*
  * Read side over the compacted payload (§3.3 step 7 with per-slice scales):
  * counts_c[r] = sum over the W compacted rows of bit r (n_E bytes, in
- * compacted order; required), then, when out is not NULL, out[i] =
+ * compacted order; required, 4-byte aligned), then, when out is not NULL, out[i] =
  * fl32(scales[s] * q[c]) at every eligible element i (slice s, count c of
  * its rank), other positions untouched; q as nf_signcount_reduce's.  mask,
  * prefix, wslice, rstart: device copies of the layout tables.  No workspace.

@@ -640,6 +640,7 @@ nf_status nf_compact_signcount_reduce(const uint64_t* cbits, int64_t cbits_strid
   if (n_eligible == 0) return ok();
   NF_TRY(check_bits(cbits, cbits_stride_words, n_eligible, W));
   if (!counts_c) return fail(NF_ERR_INVALID_ARG, "counts_c is NULL");
+  if (!aligned(counts_c, 4)) return fail(NF_ERR_ALIGNMENT, "counts_c not 4-byte aligned");
   if (out) {
     NF_TRY(check_mask(mask, n));
     if (S < 1 || !prefix || !wslice || !rstart || !scales) return fail(NF_ERR_INVALID_ARG, "NULL layout table or scales");
@@ -666,6 +667,7 @@ nf_status nf_compact_signcount_reduce(const uint64_t* cbits, int64_t cbits_strid
   x.out = out;
   x.n = n;
   x.S = S;
+  x.n_eligible = n_eligible;
   x.W = W;
   x.decode_mode = decode_mode;
   e = nf::launch_cexpand(x, s);

@@ -332,6 +332,7 @@ struct CompactArgs {
   uint64_t* cbits;          // compacted rows
   int64_t cstride;
   int64_t n, n_eligible;
+  int32_t W;                // rows (filled by the launcher)
 };
 
 struct SliceArgs {
@@ -353,9 +354,9 @@ struct ExpandArgs {
   const int32_t* wslice;    // [nw]
   const int64_t* rstart;    // [S + 1]
   const float* scales;      // [S]
-  const uint8_t* counts_c;  // [n_E] counts in compacted order
+  const uint8_t* counts_c;  // [n_E] counts in compacted order, 4-byte aligned
   float* out;
-  int64_t n, S;
+  int64_t n, S, n_eligible;
   int32_t W, decode_mode;
 };
 

@@ -55,61 +55,73 @@ __device__ __forceinline__ uint64_t compress64(uint64_t x, uint64_t m) {
   return x;
 }
 
-// Compacted word o of row w = blockIdx.y gathers ranks 64o .. 64o + 63: it
-// starts at the positional word holding rank 64o (start[o]), skips the
-// ranks of that word below 64o, and appends the compressed words that
-// follow until 64 ranks (or n_E) are covered.  A lane takes four compacted
-// words, so that their table and payload loads are in flight together.
-constexpr int kCompactPerLane = 4;
+// Lane o (compacted word o, every row) gathers ranks 64o .. 64o + 63: it
+// starts at the positional word holding rank 64o (start[o]), skips the ranks
+// of that word below 64o, and appends the compressed words that follow until
+// 64 ranks (or n_E) are covered.  The layout tables are read once per
+// compacted word and serve all W rows.  When two positional words cover the
+// 64 ranks (every word but those in sparse stretches of the mask), the rows
+// go four at a time with both of their words in flight; otherwise each row
+// walks the words one by one.
+constexpr int kCompactRows = 4;
 
 __global__ __launch_bounds__(kThreadsS) void k_compact(CompactArgs a) {
-  const int w = blockIdx.y;
-  const uint64_t* row = a.bits + (int64_t)w * a.bstride;
-  uint64_t* crow = a.cbits + (int64_t)w * a.cstride;
   const int64_t nwc = (a.n_eligible + 63) / 64;
   const int64_t nw = (a.n + 63) / 64;
-  // a wavefront takes 64 * kCompactPerLane consecutive compacted words; lane l
-  // takes words l, l + 64, ... of them, so each batch of loads is contiguous
-  const int lane = threadIdx.x & 63;
-  const int64_t wave = (int64_t)blockIdx.x * (kThreadsS / 64) + (threadIdx.x >> 6);
-  const int64_t waves = (int64_t)gridDim.x * (kThreadsS / 64);
-  for (int64_t t0 = wave * 64 * kCompactPerLane; t0 < nwc; t0 += waves * 64 * kCompactPerLane) {
-    const int64_t o0 = t0 + lane;
-    int64_t k[kCompactPerLane];
-    uint64_t pk[kCompactPerLane], m0[kCompactPerLane], x0[kCompactPerLane];
-#pragma unroll
-    for (int j = 0; j < kCompactPerLane; ++j) k[j] = o0 + 64 * j < nwc ? a.start[o0 + 64 * j] : 0;
-#pragma unroll
-    for (int j = 0; j < kCompactPerLane; ++j) {
-      pk[j] = a.prefix[k[j]];
-      m0[j] = a.mask[k[j]];
-      x0[j] = row[k[j]];
+  const int W = a.W;
+  for (int64_t o = (int64_t)blockIdx.x * kThreadsS + threadIdx.x; o < nwc; o += (int64_t)gridDim.x * kThreadsS) {
+    const int64_t r0 = o * 64;
+    const int need = (int)((a.n_eligible - r0) < 64 ? (a.n_eligible - r0) : 64);
+    const int64_t k = a.start[o];
+    const int skip = (int)(r0 - (int64_t)a.prefix[k]);
+    uint64_t m0 = a.mask[k];
+    if (k == nw - 1) m0 &= low_mask(a.n - 64 * k);
+    const int c0 = __popcll(m0) - skip;  // ranks of word k at or above 64o (>= 1)
+    uint64_t m1 = 0;
+    if (c0 < need && k + 1 < nw) {
+      m1 = a.mask[k + 1];
+      if (k + 1 == nw - 1) m1 &= low_mask(a.n - 64 * (k + 1));
     }
+    const bool two = c0 >= need || c0 + __popcll(m1) >= need;
+    const uint64_t keep = low_mask(need);
+    if (two) {
+      for (int w0 = 0; w0 < W; w0 += kCompactRows) {
+        uint64_t x0[kCompactRows], x1[kCompactRows];
 #pragma unroll
-    for (int j = 0; j < kCompactPerLane; ++j) {
-      const int64_t o = o0 + 64 * j;
-      if (o >= nwc) break;
-      const int64_t r0 = o * 64;
-      const int need = (int)((a.n_eligible - r0) < 64 ? (a.n_eligible - r0) : 64);
-      int64_t kk = k[j];
-      int skip = (int)(r0 - (int64_t)pk[j]);
-      uint64_t m = m0[j], x = x0[j];
-      uint64_t acc = 0;
+        for (int u = 0; u < kCompactRows; ++u) {
+          const int w = w0 + u < W ? w0 + u : W - 1;
+          x0[u] = a.bits[(int64_t)w * a.bstride + k];
+          x1[u] = c0 < need ? a.bits[(int64_t)w * a.bstride + k + 1] : 0ull;
+        }
+#pragma unroll
+        for (int u = 0; u < kCompactRows; ++u) {
+          if (w0 + u >= W) break;
+          uint64_t e = compress64(x0[u], m0) >> skip;
+          if (c0 < need) e |= compress64(x1[u], m1) << c0;
+          a.cbits[(int64_t)(w0 + u) * a.cstride + o] = e & keep;
+        }
+      }
+      continue;
+    }
+    for (int w = 0; w < W; ++w) {
+      const uint64_t* row = a.bits + (int64_t)w * a.bstride;
+      int64_t kk = k;
+      int sk = skip;
+      uint64_t m = m0, acc = 0;
       int got = 0;
       while (true) {
-        if (kk == nw - 1) m &= low_mask(a.n - 64 * kk);
-        const int cnt = __popcll(m) - skip;
+        const int cnt = __popcll(m) - sk;
         if (cnt > 0) {
-          const uint64_t e = compress64(x, m) >> skip;
+          const uint64_t e = compress64(row[kk], m) >> sk;
           acc |= got < 64 ? e << got : 0ull;
           got += cnt;
         }
-        skip = 0;
+        sk = 0;
         if (got >= need || ++kk >= nw) break;
         m = a.mask[kk];
-        x = row[kk];
+        if (kk == nw - 1) m &= low_mask(a.n - 64 * kk);
       }
-      crow[o] = acc & low_mask(need);
+      a.cbits[(int64_t)w * a.cstride + o] = acc & keep;
     }
   }
 }
@@ -172,15 +184,19 @@ __global__ __launch_bounds__(kThreadsS) void k_slice_scale(SliceArgs a) {
 
 // A wavefront takes 64 consecutive positional words per task.  Lane t loads
 // mask word k0 + t; a scan of the popcounts gives each word's first rank
-// (prefix[k0] + the eligible elements of the task's earlier words), so the
-// task loads one prefix entry.  Then, word by word, lane j decodes element j:
-// its rank is the word's first rank + the eligible bits below j, its count
-// counts_c[rank], its slice the one whose compacted range holds the rank
-// (walked forward per lane, ranks only grow).  Counts are loaded eight
-// words at a time.  Slice starts and scales sit in LDS when the table has at
-// most kExpandLdsSlices slices.
-constexpr int kExpandBatch = 8;
+// (prefix[k0] + the eligible elements of the task's earlier words).  The
+// task's counts, at most 4096 consecutive bytes of counts_c from rank
+// prefix[k0] on, are brought into LDS with coalesced dword loads.  Then,
+// word by word, lane j decodes element j: its count sits at (the word's
+// first rank - prefix[k0] + the eligible bits below j) in LDS, its slice is
+// the one whose compacted range holds its rank (walked forward per lane,
+// ranks only grow).  The task's mask words and first ranks are read back
+// from LDS as broadcasts, four words at a time.  Slice starts and scales sit
+// in LDS when the table has at most kExpandLdsSlices slices.
 constexpr int kExpandLdsSlices = 1024;
+constexpr int kExpandStageWords = 4096 / 4 + 2;  // dwords per wavefront: 4096 counts + alignment
+constexpr int kExpandUnroll = 4;                 // words decoded together
+constexpr int kExpandStageLoads = (kExpandStageWords + 63) / 64;  // dword loads per lane per task
 
 __device__ __forceinline__ int64_t slice_of_rank(const int64_t* rstart, int64_t S, int64_t r) {
   int64_t lo = 0, hi = S - 1;  // last s with rstart[s] <= r
@@ -196,6 +212,9 @@ __global__ __launch_bounds__(kThreadsS) void k_cexpand(ExpandArgs a) {
   __shared__ float tab[256];
   __shared__ int64_t rs[kExpandLdsSlices + 1];
   __shared__ float sc[kExpandLdsSlices];
+  __shared__ uint32_t stage[kThreadsS / 64][kExpandStageWords];
+  __shared__ uint64_t tmask[kThreadsS / 64][64];
+  __shared__ int tex[kThreadsS / 64][64];
   const bool lds = a.S <= kExpandLdsSlices;
   for (int c = threadIdx.x; c <= a.W; c += kThreadsS) tab[c] = decode_q(c, a.W, a.decode_mode);
   if (lds) {
@@ -206,7 +225,13 @@ __global__ __launch_bounds__(kThreadsS) void k_cexpand(ExpandArgs a) {
   const int64_t* rstart = lds ? rs : a.rstart;
   const float* scales = lds ? sc : a.scales;
   const int lane = threadIdx.x & 63;
+  uint32_t* st = stage[threadIdx.x >> 6];
+  uint64_t* tw = tmask[threadIdx.x >> 6];
+  int* te = tex[threadIdx.x >> 6];
+  const uint8_t* stb = reinterpret_cast<const uint8_t*>(st);
   const int64_t nw = (a.n + 63) / 64;
+  const int64_t ncw = a.n_eligible / 4;  // whole dwords of counts_c (the last 0-3 bytes go one by one)
+  const uint32_t* cw = reinterpret_cast<const uint32_t*>(a.counts_c);
   const int64_t wave = (int64_t)blockIdx.x * (kThreadsS / 64) + (threadIdx.x >> 6);
   const int64_t waves = (int64_t)gridDim.x * (kThreadsS / 64);
   for (int64_t k0 = wave * 64; k0 < nw; k0 += waves * 64) {
@@ -221,40 +246,75 @@ __global__ __launch_bounds__(kThreadsS) void k_cexpand(ExpandArgs a) {
       if (lane >= d) incl += v;
     }
     const int excl = incl - __popcll(mw);
+    const int total = __shfl(incl, 63, 64);
+    if (total == 0) continue;  // no eligible element in the task
     const int64_t base = (int64_t)a.prefix[k0];
-    if (__shfl(incl, 63, 64) == 0) continue;  // no eligible element in the task
-    int64_t s = slice_of_rank(rstart, a.S, base);  // every rank of the task is >= base
-    for (int t0 = 0; t0 < nk; t0 += kExpandBatch) {
-      uint8_t c[kExpandBatch];
-      int64_t r[kExpandBatch];
-      bool e[kExpandBatch];
+    // counts of ranks [base, base + total) into LDS, from the dword holding rank base
+    const int64_t d0 = base / 4;
+    const int off = (int)(base - 4 * d0);
+    const int nd = (off + total + 3) / 4;
+    // every load of the lane first, then the LDS stores (one round trip, not 17)
+    uint32_t v[kExpandStageLoads];
 #pragma unroll
-      for (int u = 0; u < kExpandBatch; ++u) {
-        const int t = t0 + u;
-        const uint64_t m = uniform64(__shfl(mw, t < 64 ? t : 63, 64));
-        const int ex = __shfl(excl, t < 64 ? t : 63, 64);
-        e[u] = t < nk && ((m >> lane) & 1ull);
-        r[u] = base + ex + __popcll(m & ((1ull << lane) - 1ull));
-        c[u] = e[u] ? a.counts_c[r[u]] : 0;
+    for (int j = 0; j < kExpandStageLoads; ++j) {
+      const int i = lane + 64 * j;
+      const int64_t d = d0 + i;
+      v[j] = (i < nd && d < ncw) ? __builtin_nontemporal_load(cw + d) : 0u;
+    }
+#pragma unroll
+    for (int j = 0; j < kExpandStageLoads; ++j) {
+      const int i = lane + 64 * j;
+      const int64_t d = d0 + i;
+      if (i < nd && d >= ncw)  // the last 1-3 counts of counts_c, byte by byte
+        for (int e = 0; e < 4 && 4 * d + e < a.n_eligible; ++e) v[j] |= (uint32_t)a.counts_c[4 * d + e] << (8 * e);
+      if (i < nd) st[i] = v[j];
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    tw[lane] = mw;    // the task's mask words and first ranks, read back as
+    te[lane] = excl;  // wavefront-wide broadcasts
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    int64_t s = slice_of_rank(rstart, a.S, base);  // every rank of the task is >= base
+    const uint64_t below = (1ull << lane) - 1ull;
+    for (int t = 0; t < nk; t += kExpandUnroll) {
+      bool el[kExpandUnroll];
+      int rel[kExpandUnroll];
+      uint8_t c[kExpandUnroll];
+#pragma unroll
+      for (int u = 0; u < kExpandUnroll; ++u) {
+        const int tt = t + u < nk ? t + u : nk - 1;
+        const uint64_t m = t + u < nk ? tw[tt] : 0ull;
+        el[u] = (m >> lane) & 1ull;
+        rel[u] = te[tt] + __popcll(m & below);  // rank - base
+        c[u] = el[u] ? stb[off + rel[u]] : 0;
       }
 #pragma unroll
-      for (int u = 0; u < kExpandBatch; ++u) {
-        if (!e[u]) continue;
-        while (s + 1 < a.S && r[u] >= rstart[s + 1]) ++s;
-        a.out[64 * (k0 + t0 + u) + lane] = scales[s] * tab[c[u]];
+      for (int u = 0; u < kExpandUnroll; ++u) {
+        if (!el[u]) continue;
+        const int64_t r = base + rel[u];
+        while (s + 1 < a.S && r >= rstart[s + 1]) ++s;
+        a.out[64 * (k0 + t + u) + lane] = scales[s] * tab[c[u]];
       }
     }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
 }
 
 }  // namespace
 
-hipError_t launch_compact(const CompactArgs& a, int W, hipStream_t s) {
+hipError_t launch_compact(const CompactArgs& a0, int W, hipStream_t s) {
+  CompactArgs a = a0;
+  a.W = W;
   const int64_t nwc = (a.n_eligible + 63) / 64;
-  int64_t blocks = (nwc + kThreadsS * kCompactPerLane - 1) / (kThreadsS * kCompactPerLane);
-  if (blocks > 2048) blocks = 2048;
+  int64_t blocks = (nwc + kThreadsS - 1) / kThreadsS;
+  if (blocks > 8192) blocks = 8192;
   if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(k_compact, dim3((unsigned)blocks, (unsigned)W), dim3(kThreadsS), 0, s, a);
+  hipLaunchKernelGGL(k_compact, dim3((unsigned)blocks), dim3(kThreadsS), 0, s, a);
   return hipGetLastError();
 }
 
