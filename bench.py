@@ -49,7 +49,7 @@ def parse():
                     help="low-bit payload: G-Binary sign counts or G-Ternary two-plane counts")
     ap.add_argument("--tau", type=float, default=0.5, help="G-Ternary gate (units of mean |g|)")
     ap.add_argument("--cpu-buckets", type=int, default=None,
-                    help="buckets of the oracle's CPU sample (default: about 12 s of work)")
+                    help="buckets of the oracle's CPU sample (default: about 15 s of work)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-probe", action="store_true", help="skip the streaming-read reference")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -459,7 +459,8 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         import oracle as nfo
-        k = args.cpu_buckets or max(1, min(nb, int(12e9 * 0.35 / (4 * W * min(bn, n)))))
+        # about 15 s of single-core oracle work at its ~0.55 GB/s
+        k = args.cpu_buckets or max(1, min(nb, int(8.4e9 / (4 * W * min(bn, n)))))
         opol = nfo.policy(force_lowbit=int(args.force_lowbit), format=int(ternary), tau=args.tau)
         model, ncpu = host_cpu()
         old_aff = os.sched_getaffinity(0)
