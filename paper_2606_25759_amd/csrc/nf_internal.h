@@ -54,6 +54,9 @@ constexpr int kMaxG = NF_MAX_G;                // tiles per chunk at most
 // that shares one adds to its predecessor's partial, which must then come
 // from an earlier, stream-ordered launch.
 constexpr int64_t kOneLaunchChunks = 4 * kEpochBlocks;
+// Chunks that keep every compute unit busy: two 16-wavefront blocks each.
+constexpr int64_t kFillChunks = 512;
+static_assert(kFillChunks <= kMaxSlots, "a filled small problem must not share partial slots");
 inline int64_t one_launch_epoch(int64_t total_chunks) {
   return total_chunks <= kOneLaunchChunks ? (total_chunks > 0 ? total_chunks : 1) : kEpochBlocks;
 }
@@ -107,11 +110,21 @@ inline Geometry make_geometry(int W, int64_t n_total, int64_t bucket_n) {
   g.nb = n_total <= 0 ? 1 : ceil_div(n_total, bucket_n);
   int64_t full = n_total < bucket_n ? n_total : bucket_n;
   if (full < 0) full = 0;
-  g.chunks_full = ceil_div(ceil_div(full, g.tile), g.G);
   int64_t last = n_total - (g.nb - 1) * bucket_n;
   if (last < 0) last = 0;
-  int64_t chunks_last = ceil_div(ceil_div(last, g.tile), g.G);
-  g.total_chunks = (g.nb - 1) * g.chunks_full + chunks_last;
+  const int64_t tiles_full = ceil_div(full, g.tile), tiles_last = ceil_div(last, g.tile);
+  auto total_for = [&](int G) { return (g.nb - 1) * ceil_div(tiles_full, G) + ceil_div(tiles_last, G); };
+  // A problem of fewer than kFillChunks chunks would leave compute units
+  // idle: it takes the smallest G that keeps it within kFillChunks chunks
+  // (so within one launch and with no shared partial slot).
+  if (total_for(g.G) < kFillChunks)
+    for (int G = 1; G < g.G; ++G)
+      if (total_for(G) <= kFillChunks) {
+        g.G = G;
+        break;
+      }
+  g.chunks_full = ceil_div(tiles_full, g.G);
+  g.total_chunks = total_for(g.G);
   g.slots = (int)(g.chunks_full < kMaxSlots ? g.chunks_full : kMaxSlots);
   if (g.slots < 1) g.slots = 1;
   int64_t words = (full + 63) / 64;
