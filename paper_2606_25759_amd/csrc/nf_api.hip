@@ -147,10 +147,14 @@ nf_status run_pass1_decide(const nf::Geometry& geo, const float* g, int64_t stri
   }
   d.n_total = geo.n_total;
   d.bucket_n = geo.bucket_n;
+  d.part2 = reinterpret_cast<nf::Partial*>(w + lay.part2);
+  d.part2_ne = reinterpret_cast<uint64_t*>(w + lay.ne2);
   d.W = geo.W;
   d.slots = geo.slots;
   d.tile = geo.tile;
   d.G = geo.G;
+  d.gs = geo.gs;
+  d.groups = geo.groups;
   e = nf::launch_decide(geo, d, s);
   if (e != hipSuccess) return hip_fail(e, "decide launch");
   if (phases) record_phase(2, s);

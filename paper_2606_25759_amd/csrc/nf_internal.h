@@ -44,19 +44,15 @@ constexpr int kStageFloats = 16384;      // 64 KiB of LDS
 #define NF_MAX_G 32
 #endif
 constexpr int kBitsWords = NF_BITS_WORDS;      // LDS words for a chunk's sign words (32 KiB)
-constexpr int kMaxSlots = 512;                 // partial-statistics slots per bucket
+constexpr int kMaxSlots = 512;                 // partials the decision reduces per bucket at most
 constexpr int kEpochBlocks = NF_EPOCH_BLOCKS;  // chunks per pass-1 launch
 constexpr int kMaxG = NF_MAX_G;                // tiles per chunk at most
 // Small problems (at most 4 epochs of chunks) run as one launch: their few
 // stores cost less than the launch tails (measured on the 0.82 GB
-// ResNet-50-scale workload: pass 1 0.28 -> 0.19 ms).  Pass 1 does so only
-// when no two chunks of a bucket share a partial-statistics slot: a chunk
-// that shares one adds to its predecessor's partial, which must then come
-// from an earlier, stream-ordered launch.
+// ResNet-50-scale workload: pass 1 0.28 -> 0.19 ms).
 constexpr int64_t kOneLaunchChunks = 4 * kEpochBlocks;
 // Chunks that keep every compute unit busy: two 16-wavefront blocks each.
 constexpr int64_t kFillChunks = 512;
-static_assert(kFillChunks <= kMaxSlots, "a filled small problem must not share partial slots");
 inline int64_t one_launch_epoch(int64_t total_chunks) {
   return total_chunks <= kOneLaunchChunks ? (total_chunks > 0 ? total_chunks : 1) : kEpochBlocks;
 }
@@ -77,16 +73,16 @@ struct Geometry {
   int64_t n_total, bucket_n, nb;
   int64_t chunks_full;   // chunks of a full bucket
   int64_t total_chunks;  // over all buckets
-  int slots;             // partial-statistics slots per bucket (<= kMaxSlots)
+  int slots;             // partial-statistics slots per bucket: one per chunk
+  int gs;                // slots per second-level group (0: no second level)
+  int groups;            // second-level groups per full bucket (<= kMaxSlots)
   int bpb2;              // pass-2 blocks per bucket
 };
 
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 // Chunks per pass-1 launch (see kOneLaunchChunks).
-inline int64_t pass1_epoch(const Geometry& g) {
-  return g.chunks_full <= kMaxSlots ? one_launch_epoch(g.total_chunks) : kEpochBlocks;
-}
+inline int64_t pass1_epoch(const Geometry& g) { return one_launch_epoch(g.total_chunks); }
 
 inline Geometry make_geometry(int W, int64_t n_total, int64_t bucket_n) {
   Geometry g;
@@ -125,8 +121,12 @@ inline Geometry make_geometry(int W, int64_t n_total, int64_t bucket_n) {
       }
   g.chunks_full = ceil_div(tiles_full, g.G);
   g.total_chunks = total_for(g.G);
-  g.slots = (int)(g.chunks_full < kMaxSlots ? g.chunks_full : kMaxSlots);
-  if (g.slots < 1) g.slots = 1;
+  // Every chunk owns a slot, so no two chunks ever touch the same partial.
+  // A bucket of more than kMaxSlots chunks is first summed in groups of gs
+  // consecutive slots (at most kMaxSlots groups), which the decision reads.
+  g.slots = (int)(g.chunks_full > 1 ? g.chunks_full : 1);
+  g.gs = g.chunks_full > kMaxSlots ? (int)ceil_div(g.chunks_full, kMaxSlots) : 0;
+  g.groups = g.gs ? (int)ceil_div(g.chunks_full, g.gs) : 0;
   int64_t words = (full + 63) / 64;
   int64_t chunks2 = ceil_div(words, kWordsPerWave2 * 4);
   if (chunks2 < 1) chunks2 = 1;
@@ -144,15 +144,20 @@ struct Partial {
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct WorkspaceLayout {
-  size_t partials, ne, total;
+  size_t partials, ne, part2, ne2, total;
 };
 
+// [bucket][slot][W] partials, [bucket][slot] eligible counts, then the
+// second-level [bucket][group][W] and [bucket][group] sums.
 inline WorkspaceLayout workspace_layout(const Geometry& g) {
   WorkspaceLayout l;
-  size_t slots = (size_t)g.nb * (size_t)g.slots;
+  const size_t slots = (size_t)g.nb * (size_t)g.slots;
+  const size_t groups = (size_t)g.nb * (size_t)g.groups;
   l.partials = 0;
   l.ne = align256(slots * (size_t)g.W * sizeof(Partial));
-  l.total = l.ne + align256(slots * sizeof(uint64_t));
+  l.part2 = l.ne + align256(slots * sizeof(uint64_t));
+  l.ne2 = l.part2 + align256(groups * (size_t)g.W * sizeof(Partial));
+  l.total = l.ne2 + align256(groups * sizeof(uint64_t));
   return l;
 }
 
@@ -176,11 +181,13 @@ struct Pass1Args {
 struct DecideArgs {
   const Partial* part;
   const uint64_t* part_ne;
+  Partial* part2;          // second-level sums (gs > 0)
+  uint64_t* part2_ne;
   nf_worker_stats* stats;
   nf_route_decision* dec;  // NULL: statistics only
   nf_route_policy pol;
   int64_t n_total, bucket_n;
-  int32_t W, slots, tile, G;
+  int32_t W, slots, tile, G, gs, groups;
 };
 
 // kOpFallbackOnly: route-driven, FP32 sums of the buckets routed F only.

@@ -300,8 +300,7 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
       }
     }
     __syncthreads();
-    const int64_t slot = (int64_t)b * a.slots + (c % kMaxSlots);
-    const bool first = c < kMaxSlots;
+    const int64_t slot = (int64_t)b * a.slots + c;
     if ((int)threadIdx.x < a.W) {
       const int w = threadIdx.x;
       Partial p = red[w];
@@ -310,15 +309,9 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
         p.ssq += q3.ssq;
         p.nonfinite += q3.nonfinite;
       }
-      if (!first) {
-        const Partial o = part[slot * a.W + w];
-        p.sabs = o.sabs + p.sabs;
-        p.ssq = o.ssq + p.ssq;
-        p.nonfinite = o.nonfinite + p.nonfinite;
-      }
       part[slot * a.W + w] = p;
     }
-    if (threadIdx.x == 0 && first) part_ne[slot] = 0;  // later chunks of the slot add nothing
+    if (threadIdx.x == 0) part_ne[slot] = 0;
     return;
   }
   auto fast_body = [&](int64_t t, float (&X)[NX], float (&Xn)[NX]) {
@@ -522,8 +515,7 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
     }
   }
 
-  const int64_t slot = (int64_t)b * a.slots + (c % kMaxSlots);
-  const bool first = c < kMaxSlots;
+  const int64_t slot = (int64_t)b * a.slots + c;  // the chunk's own partial slot
   if (a.eg == 1) {
     // One element group: each worker lives in exactly one wavefront, which
     // stores its own rows of sign words and its own partials, so the block
@@ -548,16 +540,10 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
         p.sabs = s1;
         p.ssq = s2;
         p.nonfinite = nonf[j];
-        if (!first) {
-          const Partial o = part[slot * a.W + w];
-          p.sabs = o.sabs + p.sabs;
-          p.ssq = o.ssq + p.ssq;
-          p.nonfinite = o.nonfinite + p.nonfinite;
-        }
         part[slot * a.W + w] = p;
       }
     }
-    if (wg == 0 && lane == 0) part_ne[slot] = first ? ne : part_ne[slot] + ne;
+    if (wg == 0 && lane == 0) part_ne[slot] = ne;
     return;
   }
 
@@ -576,9 +562,8 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
     __syncthreads();
   }
 
-  // Block partials: wavefront sums, then element groups in order.  Chunk c
-  // of bucket b goes to slot c % kMaxSlots; chunks beyond the first
-  // kMaxSlots add to it, always in launch order.
+  // Block partials: wavefront sums, then element groups in order, to the
+  // chunk's own slot.
   Partial* red = reinterpret_cast<Partial*>(smem);
   uint64_t* red_ne = reinterpret_cast<uint64_t*>(red + a.eg * a.W);
   if (active) {
@@ -607,22 +592,67 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
       p.ssq += q2.ssq;
       p.nonfinite += q2.nonfinite;
     }
-    if (!first) {
-      const Partial o = part[slot * a.W + w];
-      p.sabs = o.sabs + p.sabs;
-      p.ssq = o.ssq + p.ssq;
-      p.nonfinite = o.nonfinite + p.nonfinite;
-    }
     part[slot * a.W + w] = p;
   }
   if (threadIdx.x == 0) {
     uint64_t s = 0;
     for (int e = 0; e < a.eg; ++e) s += red_ne[e];
-    part_ne[slot] = first ? s : part_ne[slot] + s;
+    part_ne[slot] = s;
   }
 }
 
 // ------------------------------------------------------------------ decide
+// Second level for buckets of more than kMaxSlots chunks: block x sums
+// group x % groups (gs consecutive slots) of bucket x / groups.  Thread
+// t < parts * W takes worker t % W and every parts-th slot from t / W on;
+// the parts are then added in order, so the result does not depend on
+// timing.
+__global__ __launch_bounds__(256) void k_slotsum(DecideArgs a) {
+  __shared__ Partial red[256];
+  const int b = (int)(blockIdx.x / (unsigned)a.groups);
+  const int grp = (int)(blockIdx.x - (unsigned)b * (unsigned)a.groups);
+  const int64_t nbe = bucket_len(a.n_total, a.bucket_n, b);
+  const int64_t chunks = ((nbe + a.tile - 1) / a.tile + a.G - 1) / a.G;
+  const int64_t s0 = (int64_t)grp * a.gs;
+  if (s0 >= chunks) return;  // whole block: this bucket has fewer groups
+  const int cnt = (int)(chunks - s0 < a.gs ? chunks - s0 : a.gs);
+  const int parts = 256 / a.W;
+  const int t = threadIdx.x;
+  const Partial* P = a.part + ((int64_t)b * a.slots + s0) * a.W;
+  if (t < parts * a.W) {
+    const int w = t % a.W;
+    double s1 = 0.0, s2 = 0.0;
+    uint64_t nf = 0;
+#pragma unroll 8
+    for (int k = t / a.W; k < cnt; k += parts) {
+      const Partial q = P[(int64_t)k * a.W + w];
+      s1 += q.sabs;
+      s2 += q.ssq;
+      nf += q.nonfinite;
+    }
+    red[t].sabs = s1;
+    red[t].ssq = s2;
+    red[t].nonfinite = nf;
+  }
+  __syncthreads();
+  if (t < a.W) {
+    Partial r = red[t];
+    for (int p = 1; p < parts; ++p) {
+      r.sabs += red[p * a.W + t].sabs;
+      r.ssq += red[p * a.W + t].ssq;
+      r.nonfinite += red[p * a.W + t].nonfinite;
+    }
+    a.part2[((int64_t)b * a.groups + grp) * a.W + t] = r;
+  }
+  if (t < 64) {
+    const uint64_t* N = a.part_ne + (int64_t)b * a.slots + s0;
+    uint64_t ne = 0;
+    for (int k = t; k < cnt; k += 64) ne += N[k];
+    ne = wave_sum_u64(ne);
+    if (t == 0) a.part2_ne[(int64_t)b * a.groups + grp] = ne;
+  }
+}
+
 __global__ __launch_bounds__(256) void k_decide(DecideArgs a) {
   __shared__ nf_worker_stats st[256];
   __shared__ uint64_t ne_s;
@@ -631,14 +661,19 @@ __global__ __launch_bounds__(256) void k_decide(DecideArgs a) {
   const int b = blockIdx.x;
   const int v = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wavefront index, uniform
   const int lane = threadIdx.x & 63;
-  const Partial* P = a.part + (int64_t)b * a.slots * a.W;
-  // slots written for this bucket: one per chunk, at most kMaxSlots
+  // One slot per chunk of this bucket, or its second-level group sums.
   const int64_t nbe = bucket_len(a.n_total, a.bucket_n, b);
   const int64_t chunks = ((nbe + a.tile - 1) / a.tile + a.G - 1) / a.G;
-  const int used = (int)(chunks < a.slots ? chunks : a.slots);
+  const bool two = a.gs > 0;
+  const Partial* P = two ? a.part2 + (int64_t)b * a.groups * a.W : a.part + (int64_t)b * a.slots * a.W;
+  const uint64_t* PN = two ? a.part2_ne + (int64_t)b * a.groups : a.part_ne + (int64_t)b * a.slots;
+  const int used = (int)(two ? (chunks + a.gs - 1) / a.gs : chunks);
+  // The slot loops are unrolled so that their loads are in flight together;
+  // the adds keep their order.
   for (int w = v; w < a.W; w += 4) {
     double s1 = 0.0, s2 = 0.0;
     uint64_t nf = 0;
+#pragma unroll 8
     for (int k = lane; k < used; k += 64) {
       const Partial p = P[(int64_t)k * a.W + w];
       s1 += p.sabs;
@@ -656,7 +691,8 @@ __global__ __launch_bounds__(256) void k_decide(DecideArgs a) {
   }
   if (v == 0) {
     uint64_t s = 0;
-    for (int k = lane; k < used; k += 64) s += a.part_ne[(int64_t)b * a.slots + k];
+#pragma unroll 8
+    for (int k = lane; k < used; k += 64) s += PN[k];
     s = wave_sum_u64(s);
     if (lane == 0) ne_s = s;
   }
@@ -1245,10 +1281,10 @@ static hipError_t pass1_dispatch(const Geometry& geo, const Pass1Args& a, hipStr
   }
   // One launch per epoch of chunks (see the geometry notes).  The first
   // launch is ordered after earlier work on the stream; later ones may
-  // start while the one before drains, which is safe when no two chunks of
-  // a bucket share a partial slot (every chunk then writes only its own
-  // slot and sign words).  The next ordered launch (decide) waits for all.
-  const uint32_t overlap = geo.chunks_full <= kMaxSlots ? hipExtAnyOrderLaunch : 0u;
+  // start while the one before drains: every chunk writes only its own
+  // partial slot and sign words.  The next ordered launch (the decision)
+  // waits for all.
+  const uint32_t overlap = hipExtAnyOrderLaunch;
   const int64_t epoch = pass1_epoch(geo);
   for (int64_t q0 = 0; q0 < geo.total_chunks; q0 += epoch) {
     const int64_t left = geo.total_chunks - q0;
@@ -1273,6 +1309,11 @@ hipError_t launch_pass1(const Geometry& geo, const Pass1Args& a, hipStream_t s) 
 }
 
 hipError_t launch_decide(const Geometry& geo, const DecideArgs& a, hipStream_t s) {
+  if (geo.gs > 0) {
+    hipLaunchKernelGGL(k_slotsum, dim3((unsigned)(geo.nb * geo.groups)), dim3(256), 0, s, a);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   hipLaunchKernelGGL(k_decide, dim3((unsigned)geo.nb), dim3(256), 0, s, a);
   return hipGetLastError();
 }

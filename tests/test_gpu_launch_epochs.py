@@ -1,7 +1,7 @@
 """Pass-1 launch shapes against the oracle: a bucket small enough for one
-launch, a bucket whose chunks share partial-statistics slots (more than 512
-chunks: then chunk c adds to chunk c - 512's partial, which must come from an
-earlier launch), and a flat buffer of several buckets in one launch.  Every
+launch, buckets of more than 512 chunks (their per-chunk partials are summed
+in groups before the decision), in one launch and in several launches that
+may overlap, and a flat buffer of several buckets in one launch.  Every
 output of every bucket is checked (G-Binary and G-Ternary)."""
 import numpy as np
 import pytest
@@ -49,8 +49,12 @@ def run_binary(W, n, bucket_n, seed):
 
 
 @pytest.mark.parametrize("W,n,bucket_n,launches", [
-    (16, 8_300_000, 8_300_000, 1),      # 507 chunks: one launch, no shared slot
-    (16, 9_000_000, 9_000_000, 3),      # 550 chunks: slots shared, launches in order
+    (16, 8_300_000, 8_300_000, 1),      # 507 chunks: one launch, partials read directly
+    (16, 9_000_000, 9_000_000, 1),      # 550 chunks: one launch, groups of 2 partials
+    (16, 20_000_000, 20_000_000, 5),    # 1221 chunks: five launches, groups of 3
+    (16, 20_000_000, 9_000_000, 5),     # three buckets, the last of 123 chunks
+    (64, 3_000_000, 3_000_000, 1),      # 733 chunks of four workers per wavefront
+    (255, 600_000, 600_000, 1),         # 586 chunks, one thread per worker in the groups
     (8, 6_000_000, 1_310_720, 1),       # five buckets in one launch
 ])
 def test_pass1_launch_shapes(W, n, bucket_n, launches):
