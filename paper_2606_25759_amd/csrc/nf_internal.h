@@ -64,9 +64,12 @@ constexpr int kWordsPerWave2 = 64;
 constexpr int kMaxBlocks2 = 1024;
 
 // Words per worker and wavefront tile for WPW workers per wavefront: eight
-// words keep pass 1 within 64 VGPRs (eight wavefronts per SIMD) for up to
-// two workers per wavefront; more workers share 16 words.
-constexpr NF_HD int pass1_words(int wpw) { return wpw <= 2 ? 8 : 16 / wpw; }
+// words for one worker and four for two keep pass 1 within 64 VGPRs (eight
+// wavefronts per SIMD) without spills; more workers share 16 words.
+constexpr NF_HD int pass1_words(int wpw) { return wpw == 1 ? 8 : wpw == 2 ? 4 : 16 / wpw; }
+// Steps (64 elements) per wavefront of a whole chunk of kMaxG tiles of one
+// element group, for NW words per worker and tile.
+constexpr NF_HD int routed_steps(int nw) { return (kMaxG * nw + kWaves - 1) / kWaves; }
 
 struct Geometry {
   int W, wg, eg, wpw, T, tile, G;

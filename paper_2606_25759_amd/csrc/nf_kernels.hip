@@ -235,8 +235,103 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
     }
     chunk_fast = !__syncthreads_or(some_not) && a.sums != kSumsAll;
     // Every element routed to FP32 (all tiles full, no mask bit set).
-    chunk_routed = WPW == 1 && stage_on && !__syncthreads_or(some_set);
+    chunk_routed = stage_on && !__syncthreads_or(some_set) &&
+                   (WPW == 1 || (te - tb) * (tile / 64) <= (int64_t)kWaves * routed_steps(NW));
     if (all_full && !chunk_fast) consume(xa);
+  }
+
+  // Chunks with every element routed to FP32, several workers per
+  // wavefront: element-major like the one-worker case below, but the
+  // workers go in groups of GW (their loads and FP64 sums of squares fit
+  // the registers).  Lane l of wavefront v keeps the running FP32 sum of
+  // element 64s + l for each of its steps s = v, v + 16, ... in a register
+  // from one group to the next, so the workers are still added in order.
+  // After each group the wavefronts' sums of squares are added in wavefront
+  // order, through LDS, into the group's partials.
+  if constexpr (WPW > 1) {
+    if (chunk_routed) {
+      constexpr int GW = WPW <= 2 ? 8 : 16;  // workers per group
+      constexpr int MS = routed_steps(NW);   // steps per wavefront at most
+      const int64_t c0 = base + tb * tile;
+      const int nsteps = (int)((te - tb) * (tile / 64));
+      const int64_t slot = (int64_t)b * a.slots + c;
+      Partial* red = reinterpret_cast<Partial*>(smem);  // [kWaves][GW]
+      float run[MS];
+#pragma unroll
+      for (int i = 0; i < MS; ++i) run[i] = 0.0f;
+      for (int w0 = 0; w0 < a.W; w0 += GW) {
+        double q2[GW];
+        uint64_t nf2[GW];
+#pragma unroll
+        for (int w = 0; w < GW; ++w) {
+          q2[w] = 0.0;
+          nf2[w] = 0;
+        }
+#pragma unroll
+        for (int i = 0; i < MS; ++i) {
+          const int st = v + kWaves * i;
+          if (st >= nsteps) break;  // wavefront-uniform
+          const int64_t e = c0 + (int64_t)st * 64 + lane;
+          float x[GW];
+#pragma unroll
+          for (int w = 0; w < GW; ++w)
+            x[w] = w0 + w < a.W ? __builtin_nontemporal_load(g + (int64_t)(w0 + w) * a.wstride + e) : 0.0f;
+          float sum = w0 == 0 ? x[0] : run[i] + x[0];
+#pragma unroll
+          for (int w = 1; w < GW; ++w)
+            if (w0 + w < a.W) sum = sum + x[w];
+          run[i] = sum;
+#pragma unroll
+          for (int w = 0; w < GW; ++w) {
+            const double d = (double)x[w];
+            q2[w] = __builtin_fma(d, d, q2[w]);
+          }
+          // A non-finite value makes the running sum non-finite from its
+          // group on, so this finds every one.
+          if (__ballot(!finite32(sum))) {
+#pragma unroll
+            for (int w = 0; w < GW; ++w) nf2[w] += __popcll(__ballot(!finite32(x[w])));
+          }
+        }
+#pragma unroll
+        for (int w = 0; w < GW; ++w) {
+          const double s2 = wave_sum(q2[w]);
+          if (lane == 0) {
+            Partial p;
+            p.sabs = 0.0;
+            p.ssq = s2;
+            p.nonfinite = nf2[w];
+            red[v * GW + w] = p;
+          }
+        }
+        __syncthreads();
+        if ((int)threadIdx.x < GW && w0 + (int)threadIdx.x < a.W) {
+          const int w = threadIdx.x;
+          Partial p = red[w];
+          for (int v2 = 1; v2 < kWaves; ++v2) {
+            p.ssq += red[v2 * GW + w].ssq;
+            p.nonfinite += red[v2 * GW + w].nonfinite;
+          }
+          part[slot * a.W + w0 + w] = p;
+        }
+        __syncthreads();  // red is reused by the next group
+      }
+#pragma unroll
+      for (int i = 0; i < MS; ++i) {
+        const int st = v + kWaves * i;
+        if (st >= nsteps) break;
+        out[c0 + (int64_t)st * 64 + lane] = a.mean ? run[i] / (float)a.W : run[i];
+      }
+      if (PACK) {
+        const int64_t gw0 = c0 / 64;
+        for (int i = threadIdx.x; i < a.W * nsteps; i += kThreads1) {
+          const int w = i / nsteps;
+          bits[(int64_t)w * a.bstride + gw0 + (i - w * nsteps)] = 0ull;
+        }
+      }
+      if (threadIdx.x == 0) part_ne[slot] = 0;
+      return;
+    }
   }
 
   // Chunks with every element routed to FP32 (one worker per wavefront):
@@ -246,7 +341,7 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
   // adds them in worker order in FP32 and keeps each worker's FP64 sum of
   // squares in its own register.  Nothing is eligible, so the sign words
   // are 0 and every |g| sum over eligible elements is 0.
-  if (chunk_routed) {
+  if (WPW == 1 && chunk_routed) {
     constexpr int WR = kWaves;  // workers at most on this path
     double q2[WR];
     uint64_t nf2[WR];

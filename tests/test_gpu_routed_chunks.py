@@ -1,0 +1,54 @@
+"""Pass-1 chunks whose elements are all routed to FP32, with more than 16
+workers (several workers per wavefront).  Such a chunk is read element-major
+in groups of workers, each lane keeping its running FP32 sums from one group
+to the next.  The sizes give more than 512 chunks, so every chunk has its
+full number of tiles (up to 16 steps of 64 elements per wavefront).  Long
+FP32 runs hold whole routed chunks; non-finite values sit inside them, in
+workers of the first, a middle and the last group.  Every output is checked
+against the oracle: statistics, decision, sign words, counts and values."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as nfo
+import paper_2606_25759_amd as nf
+import synth
+from tests import nfgpu as H
+
+pytestmark = pytest.mark.gpu
+
+
+def _chunk(W):
+    """Elements per pass-1 chunk of the library's geometry for W > 16 (its
+    tiles, words per worker and LDS budget for sign words)."""
+    wpw = 1
+    while wpw < -(-W // 16):
+        wpw *= 2
+    nw = 8 if wpw == 1 else (4 if wpw == 2 else 16 // wpw)
+    return min(32, 4096 // (W * nw)) * 64 * nw
+
+
+@pytest.mark.parametrize("W", [17, 32, 33, 64, 100, 129, 255])
+def test_routed_chunks_wide(W):
+    n = 520 * _chunk(W) + 777
+    lay = synth.small(W, n, 4000 + W, elig_frac=0.5, nruns=40)
+    g = synth.generate_host(lay)
+    m = nfo.mask_from_segments(*synth.mask_segments(lay), n)
+    routed = np.flatnonzero(~H.mask_bool(m, n))
+    assert routed.size > 4 * _chunk(W)
+    rng = np.random.default_rng(W)
+    bad = [0, W // 2, W - 1]
+    vals = np.array([np.nan, np.inf, -np.inf], np.float32)
+    g_bad = g.copy()
+    for k, w in enumerate(bad):
+        pos = rng.choice(routed, 5, replace=False)
+        g_bad[w, pos] = vals[(np.arange(5) + k) % 3]
+    for gg, pol, what in ((g, nf.policy(), "clean"),
+                          (g, nf.policy(fp32_op=nf.NF_FP32_MEAN), "mean"),
+                          (g_bad, nf.policy(), "non-finite"),
+                          (g_bad, nf.policy(force_lowbit=1), "non-finite forced")):
+        run = H.Bucket(gg, m, n)
+        res = run.route(pol)
+        H.check_route(res, gg, m, n, pol, what=f"W={W} {what}")
+        del run, res
+        torch.cuda.empty_cache()
