@@ -392,7 +392,7 @@ def main():
     dec = torch.empty(nb * nf.DECISION_BYTES, dtype=torch.uint8, device=dev)
     ws = nf.empty_workspace(nf.nf_workspace_bytes_buckets(W, n, bn), dev)
     pol = nf.policy(force_lowbit=int(args.force_lowbit), format=int(ternary), tau=args.tau)
-    launches = nf.nf_pass1_launches(W, n, bn)
+    launches = nf.nf_pass1_launches(W, n, bn, sign_words=not ternary)
     torch.cuda.synchronize()
     print("[bench] inputs resident", file=sys.stderr, flush=True)
 

@@ -132,7 +132,7 @@ def load(path=None):
         "nf_route_buckets": (ctypes.c_int, [_P, _I64, _I32, _I64, _I64, _P, _P, _P, _I64, _P, _P,
                                             _P, _P, _P, _SZ, _P]),
         "nf_set_phase_events": (ctypes.c_int, [_P, _P, _P, _P]),
-        "nf_pass1_launches": (_I64, [_I32, _I64, _I64]),
+        "nf_pass1_launches": (_I64, [_I32, _I64, _I64, _I32]),
         "nf_ternary_threshold": (ctypes.c_int, [_P, _I32, _I64, ctypes.c_float, _P]),
         "nf_pack_ternary": (ctypes.c_int, [_P, _I64, _I32, _I64, _P, _P, _P, _I64, _P]),
         "nf_ternary_reduce": (ctypes.c_int, [_P, _I64, _I32, _I64, _P, _P, _I32, _P, _P, _P]),
@@ -475,9 +475,10 @@ def nf_set_phase_events(before_pass1=None, after_pass1=None, after_decide=None, 
     _check(load().nf_set_phase_events(before_pass1, after_pass1, after_decide, after_pass2))
 
 
-def nf_pass1_launches(W, n_total, bucket_n):
-    """Pass-1 kernel launches of one nf_route_buckets call (profiling)."""
-    return int(load().nf_pass1_launches(W, n_total, bucket_n))
+def nf_pass1_launches(W, n_total, bucket_n, sign_words=True):
+    """Pass-1 kernel launches of one nf_route_buckets call (profiling); pass
+    sign_words=False for a pass 1 without sign words (G-Ternary, health)."""
+    return int(load().nf_pass1_launches(W, n_total, bucket_n, int(bool(sign_words))))
 
 
 # ------------------------------------------------------- result decoding

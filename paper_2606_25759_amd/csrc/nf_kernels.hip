@@ -1380,7 +1380,7 @@ static hipError_t pass1_dispatch(const Geometry& geo, const Pass1Args& a, hipStr
   // partial slot and sign words.  The next ordered launch (the decision)
   // waits for all.
   const uint32_t overlap = hipExtAnyOrderLaunch;
-  const int64_t epoch = pass1_epoch(geo);
+  const int64_t epoch = pass1_launch_chunks(geo, PACK);
   for (int64_t q0 = 0; q0 < geo.total_chunks; q0 += epoch) {
     const int64_t left = geo.total_chunks - q0;
     const dim3 grid((unsigned)(left < epoch ? left : epoch));

@@ -206,6 +206,18 @@ def test_sliced_sizes():
     assert nf.nf_slice_workspace_bytes(16, 8) == 1024 and nf.nf_slice_workspace_bytes(0, 8) == 0
 
 
+def test_pass1_launch_counts():
+    # GPT-1.3B scale: 201 buckets of 400 chunks (the last 306), 80,306 chunks
+    assert nf.nf_pass1_launches(16, 1_315_723_264, 6_553_600) == 314
+    assert nf.nf_pass1_launches(16, 1_315_723_264, 6_553_600, sign_words=False) == 79
+    # small problems: one launch either way; empty and invalid sizes: none
+    assert nf.nf_pass1_launches(4, 1 << 20, 1 << 20) == 1
+    assert nf.nf_pass1_launches(4, 1 << 20, 1 << 20, sign_words=False) == 1
+    assert nf.nf_pass1_launches(16, 0, 100) == 0
+    assert nf.nf_pass1_launches(0, 100, 100) == 0
+    assert nf.nf_pass1_launches(256, 100, 100) == 0
+
+
 def test_workspace_sizes():
     assert nf.nf_workspace_bytes(0, 10) == 0
     a = nf.nf_workspace_bytes(16, 6_553_600)

@@ -48,17 +48,18 @@ def run_binary(W, n, bucket_n, seed):
         check_output(o_h[a:e], ref, mw, e - a, W, dc[b], pol.decode_mode, tag)
 
 
-@pytest.mark.parametrize("W,n,bucket_n,launches", [
-    (16, 8_300_000, 8_300_000, 1),      # 507 chunks: one launch, partials read directly
-    (16, 9_000_000, 9_000_000, 1),      # 550 chunks: one launch, groups of 2 partials
-    (16, 20_000_000, 20_000_000, 5),    # 1221 chunks: five launches, groups of 3
-    (16, 20_000_000, 9_000_000, 5),     # three buckets, the last of 123 chunks
-    (64, 3_000_000, 3_000_000, 1),      # 733 chunks of four workers per wavefront
-    (255, 600_000, 600_000, 1),         # 586 chunks, one thread per worker in the groups
-    (8, 6_000_000, 1_310_720, 1),       # five buckets in one launch
+@pytest.mark.parametrize("W,n,bucket_n,launches,launches_nosigns", [
+    (16, 8_300_000, 8_300_000, 1, 1),      # 507 chunks: one launch, partials read directly
+    (16, 9_000_000, 9_000_000, 1, 1),      # 550 chunks: one launch, groups of 2 partials
+    (16, 20_000_000, 20_000_000, 5, 2),    # 1221 chunks: five launches, groups of 3
+    (16, 20_000_000, 9_000_000, 5, 2),     # three buckets, the last of 123 chunks
+    (64, 3_000_000, 3_000_000, 1, 1),      # 733 chunks of four workers per wavefront
+    (255, 600_000, 600_000, 1, 1),         # 586 chunks, one thread per worker in the groups
+    (8, 6_000_000, 1_310_720, 1, 1),       # five buckets in one launch
 ])
-def test_pass1_launch_shapes(W, n, bucket_n, launches):
+def test_pass1_launch_shapes(W, n, bucket_n, launches, launches_nosigns):
     assert nf.nf_pass1_launches(W, n, bucket_n) == launches
+    assert nf.nf_pass1_launches(W, n, bucket_n, sign_words=False) == launches_nosigns
     run_binary(W, n, bucket_n, 31 + W)
 
 
@@ -71,3 +72,16 @@ def test_ternary_single_launch_flat():
     res = ternary_route(g, mask, n, pol, bucket_n=bn)
     for b in range(-(-n // bn)):
         check_ternary_bucket(res, g, mask, n, pol, b, bn, f"ternary flat bucket {b}")
+
+
+def test_ternary_multi_launch():
+    # 1,221 chunks: pass 1 without sign words in two launches (1,024 chunks
+    # each at most), the plane pack in five
+    W, n = 16, 20_000_000
+    assert nf.nf_pass1_launches(W, n, n, sign_words=False) == 2
+    lay = synth.small(W, n, 77, elig_frac=0.85, nruns=9)
+    g = synth.generate_host(lay)
+    mask = nfo.mask_from_segments(*synth.mask_segments(lay), n)
+    pol = nf.policy(format=nf.NF_FORMAT_TERNARY, tau=0.5)
+    res = ternary_route(g, mask, n, pol, bucket_n=n)
+    check_ternary_bucket(res, g, mask, n, pol, 0, n, "ternary 1,221 chunks")
