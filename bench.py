@@ -55,6 +55,7 @@ def parse():
                     help="buckets of the oracle's CPU sample (default: about 15 s of work)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-probe", action="store_true", help="skip the streaming-read reference")
+    ap.add_argument("--no-split", action="store_true", help="skip the standalone entry points on one bucket")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run the copy kernel of known traffic (counter calibration)")
     ap.add_argument("--contrast", action="store_true",
@@ -346,6 +347,42 @@ def sliced_run(args, reps=5):
     return 0
 
 
+def split_one_bucket(nf, torch, grads, mask, W, n, n_e, reps=10):
+    """Device time of each standalone entry point on one bucket of n elements
+    (the first), with the algorithmic bytes each one moves."""
+    dev = grads.device
+    nw = (n + 63) // 64
+    n_f = n - n_e
+    g0, m0 = grads[:, :n], mask[:nw]
+    bits = torch.empty((W, nw), dtype=torch.int64, device=dev)
+    counts = torch.empty(n, dtype=torch.uint8, device=dev)
+    out = torch.empty(n, dtype=torch.float32, device=dev)
+    stats = torch.empty(W * nf.STATS_BYTES, dtype=torch.uint8, device=dev)
+    ws = nf.empty_workspace(nf.nf_workspace_bytes(W, n), dev)
+    scale = torch.full((1,), 1e-4, dtype=torch.float32, device=dev)
+    calls = {
+        "nf_bucket_health": (lambda: nf.nf_bucket_health(g0, n, m0, stats, ws), 4 * W * n + 8 * nw),
+        "nf_pack_signs": (lambda: nf.nf_pack_signs(g0, n, m0, bits, stats, ws), 4 * W * n + 8 * nw + 8 * W * nw),
+        "nf_fp32_reduce": (lambda: nf.nf_fp32_reduce(g0, n, m0, nf.NF_SEL_ROUTED, nf.NF_FP32_SUM, out),
+                           4 * W * n_f + 8 * nw + 4 * n_f),
+        "nf_signcount_reduce": (lambda: nf.nf_signcount_reduce(bits, W, n, m0, scale, nf.NF_DECODE_SOFT, counts, out),
+                                8 * W * nw + 8 * nw + n + 4 * n_e),
+    }
+    res = {"bucket_elements": n, "eligible": n_e}
+    for name, (fn, nbytes) in calls.items():
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        res[name] = {"ms": round(ms, 4), "algorithmic_gbs": round(nbytes / ms / 1e6, 1)}
+    return res
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -451,6 +488,13 @@ def main():
     value = lay.input_bytes() / ((device_ms if args.cold else ms_per_step) * 1e-3) / 1e9
     achieved = pass1_bytes / (pass1_ms * 1e-3) / 1e9
 
+    # per-function split: the standalone entry points on the first bucket
+    split = None
+    if not ternary and not args.no_split:
+        split = split_one_bucket(nf, torch, grads, mask, W, min(bn, n), int(d["n_eligible"][0]))
+        print(f"[bench] standalone, first bucket: " + ", ".join(f"{k} {v['ms']:.3f} ms" for k, v in split.items()
+                                                            if isinstance(v, dict)), file=sys.stderr, flush=True)
+
     # reference: one plain streaming read of the same gradients
     achievable = None
     if not args.no_probe:
@@ -531,6 +575,7 @@ def main():
                       "pass2": round(pass2_ms, 4), "device_total": round(device_ms, 4),
                       "pass2_algorithmic_gbs": round(pass2_bytes / max(pass2_ms, 1e-9) / 1e6, 1)},
         "achievable_read_gbs": achievable,
+        "split_one_bucket": split,
         "routes": routes,
         "mgtr": round(mgtr, 4),
         "cpu_baseline": cpu,

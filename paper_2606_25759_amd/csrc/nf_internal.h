@@ -54,6 +54,7 @@ constexpr int kEpochBlocks = NF_EPOCH_BLOCKS;  // chunks per pass-1 launch
 // 256 -> 13.7 ms, 1024 -> 12.8 ms, 4096 -> 12.8 ms, one launch -> 12.9 ms.
 constexpr int64_t kEpochNoPack = NF_EPOCH_NOPACK;
 constexpr int kMaxG = NF_MAX_G;                // tiles per chunk at most
+static_assert(kMaxG <= 32, "pass 1 keeps a bit per tile of a chunk in 32 bits");
 // Small problems (at most 4 epochs of chunks) run as one launch: their few
 // stores cost less than the launch tails (measured on the 0.82 GB
 // ResNet-50-scale workload: pass 1 0.28 -> 0.19 ms).

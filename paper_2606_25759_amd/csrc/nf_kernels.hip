@@ -164,7 +164,13 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
   // LDS: the chunk's sign words [W][G * EG * NW], then the FP32 stage [W][tile]
   const int cw = a.G * a.eg * NW;  // sign words per worker and chunk
   uint64_t* wbuf = reinterpret_cast<uint64_t*>(smem);
-  float* stage = reinterpret_cast<float*>(smem + (PACK ? (size_t)a.W * cw * sizeof(uint64_t) : 0));
+  const size_t stage_off = PACK ? (size_t)a.W * cw * sizeof(uint64_t) : 0;
+  float* stage = reinterpret_cast<float*>(smem + stage_off);
+  // then the chunk's mask words [G * EG * NW] (mixed chunks)
+  uint64_t* mwords =
+      reinterpret_cast<uint64_t*>(smem + stage_off + (stage_on ? (size_t)a.W * tile * sizeof(float) : 0));
+  __shared__ uint32_t tflags;  // mixed chunks: bit i = tile tb + i has a routed element
+  if (threadIdx.x == 0) tflags = 0;
 
   double sabs[WPW], ssq[WPW];
   uint64_t nonf[WPW];
@@ -216,7 +222,7 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
   };
   // The mask load goes out first, unpredicated, so that only it is waited
   // for before the barrier.
-  bool chunk_fast, chunk_routed;
+  bool chunk_fast, chunk_routed, chunk_mixed;
   {
     const int64_t wbeg = (base + tb * tile) / 64;
     const int nwc = all_full ? (int)((te - tb) * (tile / 64)) : 0;
@@ -237,7 +243,23 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
     // Every element routed to FP32 (all tiles full, no mask bit set).
     chunk_routed = stage_on && !__syncthreads_or(some_set) &&
                    (WPW == 1 || (te - tb) * (tile / 64) <= (int64_t)kWaves * routed_steps(NW));
-    if (all_full && !chunk_fast) consume(xa);
+    // Every tile full, some element routed (or FP32 sums over all
+    // elements), one worker per wavefront: the chunk's mask words go to LDS,
+    // with a bit per tile that has a routed element, and the first tile
+    // stays in flight.  (With more workers per wavefront the registers of
+    // this loop would spill; such chunks take the general loop.)
+    chunk_mixed = WPW == 1 && all_full && !chunk_fast && !chunk_routed;
+    if (chunk_mixed) {
+      const int nwt = tile / 64;
+      for (int i = threadIdx.x; i < nwc; i += kThreads1) {
+        const uint64_t m1 = i < kThreads1 ? m0 : mask[wbeg + i];
+        mwords[i] = m1;
+        if (m1 != ~0ull) atomicOr(&tflags, 1u << (i / nwt));
+      }
+      __syncthreads();
+    } else if (all_full && !chunk_fast) {
+      consume(xa);
+    }
   }
 
   // Chunks with every element routed to FP32, several workers per
@@ -464,7 +486,101 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
     }
   }
 
-  for (int64_t t = chunk_fast ? te : tb; t < te; ++t) {
+  // Mixed chunks: the fast loop's structure (the next tile in flight while
+  // one is examined), with each wavefront's mask words read from LDS, sign
+  // and |g| contributions masked, and the tiles that hold a routed element
+  // staged in LDS and added in worker order between two block barriers.
+  if (WPW == 1 && chunk_mixed) {
+    const int nwt = tile / 64;  // mask words per tile
+    const uint32_t tfl = tflags;
+    auto mixed_body = [&](int64_t t, float (&X)[NX], float (&Xn)[NX]) {
+      issue_words(t + 1, Xn);
+      const int ti = (int)(t - tb);
+      const bool stage_tile = stage_on && (a.sums == kSumsAll || ((tfl >> ti) & 1u));  // block-uniform
+      if (active) {
+        uint64_t mw[NW];
+        uint64_t mine = ~0ull;
+#pragma unroll
+        for (int k = 0; k < NW; ++k) {
+          mw[k] = uniform64(mwords[ti * nwt + eg * NW + k]);
+          mine &= mw[k];
+        }
+        if (wg == 0) {
+          if (mine == ~0ull) {
+            ne += (uint64_t)(64 * NW);
+          } else {
+#pragma unroll
+            for (int k = 0; k < NW; ++k) ne += __popcll(mw[k]);
+          }
+        }
+#pragma unroll
+        for (int j = 0; j < WPW; ++j) {
+          const int w = wg + j * a.wg;
+          const float* x = &X[j * NW];
+          if (j > 0 && w >= a.W) {
+#pragma unroll
+            for (int k = 0; k < NW; ++k) asm volatile("" ::"v"(x[k]));
+            continue;
+          }
+          double s1 = 0.0, s2 = 0.0;
+          uint64_t bb[NW];
+#pragma unroll
+          for (int k = 0; k < NW; ++k) {
+            if (PACK) bb[k] = __ballot(x[k] > 0.0f) & mw[k];
+            const double d = (double)x[k];
+            s2 = __builtin_fma(d, d, s2);
+            s1 += ((mw[k] >> lane) & 1ull) ? __builtin_fabs(d) : 0.0;
+          }
+          if (PACK) {
+            uint32_t wlo, whi;
+            lanes_from_ballots<NW>(bb, wlo, whi);
+            if (lane < NW) wbuf[w * cw + (ti * a.eg + eg) * NW + lane] = ((uint64_t)whi << 32) | wlo;
+          }
+          if (__ballot(!finite64(s2))) {
+#pragma unroll
+            for (int k = 0; k < NW; ++k) nonf[j] += __popcll(__ballot(!finite32(x[k])));
+          }
+          sabs[j] += s1;
+          ssq[j] += s2;
+          if (stage_tile) {
+            float* st = stage + (int64_t)w * tile + eg * T + lane;
+#pragma unroll
+            for (int k = 0; k < NW; ++k) st[64 * k] = x[k];
+          }
+        }
+      } else {
+        consume(X);
+      }
+      if (stage_tile) {
+        __syncthreads();
+        const int64_t t0 = t * tile;
+        for (int kw = v; kw < nwt; kw += kWaves) {
+          const uint64_t pick = a.sums == kSumsAll ? ~0ull : ~mwords[ti * nwt + kw];
+          const int e = kw * 64 + lane;
+          if ((pick >> lane) & 1ull) {
+            float s2 = stage[e];
+            for (int w = 1; w < a.W; ++w) s2 = s2 + stage[w * tile + e];
+            if (a.mean) s2 = s2 / (float)a.W;
+            out[base + t0 + e] = s2;
+          }
+        }
+        __syncthreads();
+      }
+    };
+    int64_t t = tb;
+    for (int64_t p = (te - tb) >> 1; p > 0; --p, t += 2) {
+      mixed_body(t, xa, xb);
+      mixed_body(t + 1, xb, xa);
+    }
+    if ((te - tb) & 1) {
+      mixed_body(t, xa, xb);
+      consume(xb);
+    } else {
+      consume(xa);
+    }
+  }
+
+  for (int64_t t = (chunk_fast || chunk_mixed) ? te : tb; t < te; ++t) {
     const int64_t t0 = t * tile;
     const bool full = t0 + tile <= nbe;  // block-uniform
     const int64_t e0 = t0 + (int64_t)eg * T;
@@ -1359,6 +1475,7 @@ static hipError_t pass1_dispatch(const Geometry& geo, const Pass1Args& a, hipStr
   const int cw = geo.G * geo.eg * pass1_words(geo.wpw);
   size_t smem = PACK ? (size_t)geo.W * cw * sizeof(uint64_t) : 0;
   if (a.sums != kSumsNone) smem += (size_t)geo.W * geo.tile * sizeof(float);
+  smem += (size_t)geo.G * geo.eg * pass1_words(geo.wpw) * sizeof(uint64_t);  // mask words of a mixed chunk
   const size_t red = (size_t)geo.eg * geo.W * sizeof(Partial) + (size_t)geo.eg * sizeof(uint64_t);
   if (smem < red) smem = red;
   if (smem > 65536) {
