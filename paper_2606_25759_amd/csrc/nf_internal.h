@@ -59,8 +59,11 @@ static_assert(kMaxG <= 32, "pass 1 keeps a bit per tile of a chunk in 32 bits");
 // stores cost less than the launch tails (measured on the 0.82 GB
 // ResNet-50-scale workload: pass 1 0.28 -> 0.19 ms).
 constexpr int64_t kOneLaunchChunks = 4 * kEpochBlocks;
-// Chunks that keep every compute unit busy: two 16-wavefront blocks each.
-constexpr int64_t kFillChunks = 512;
+// Chunks of a small problem: two rounds of two 16-wavefront blocks per
+// compute unit.  One round and a part (ResNet-50 scale: 782 chunks of 32
+// tiles) leaves most units idle in the second; 1,000 chunks of 25 tiles ran
+// pass 1 0.185 -> 0.163 ms.
+constexpr int64_t kFillChunks = 1024;
 inline int64_t one_launch_epoch(int64_t total_chunks) {
   return total_chunks <= kOneLaunchChunks ? (total_chunks > 0 ? total_chunks : 1) : kEpochBlocks;
 }
@@ -126,7 +129,7 @@ inline Geometry make_geometry(int W, int64_t n_total, int64_t bucket_n) {
   auto total_for = [&](int G) { return (g.nb - 1) * ceil_div(tiles_full, G) + ceil_div(tiles_last, G); };
   // A problem of fewer than kFillChunks chunks would leave compute units
   // idle: it takes the smallest G that keeps it within kFillChunks chunks
-  // (so within one launch and with no shared partial slot).
+  // (so within one launch).
   if (total_for(g.G) < kFillChunks)
     for (int G = 1; G < g.G; ++G)
       if (total_for(G) <= kFillChunks) {

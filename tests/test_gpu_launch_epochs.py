@@ -49,13 +49,14 @@ def run_binary(W, n, bucket_n, seed):
 
 
 @pytest.mark.parametrize("W,n,bucket_n,launches,launches_nosigns", [
-    (16, 8_300_000, 8_300_000, 1, 1),      # 507 chunks: one launch, partials read directly
-    (16, 9_000_000, 9_000_000, 1, 1),      # 550 chunks: one launch, groups of 2 partials
-    (16, 20_000_000, 20_000_000, 5, 2),    # 1221 chunks: five launches, groups of 3
+    (16, 8_300_000, 8_300_000, 1, 1),      # a small problem: 1,014 chunks of 16 tiles, groups of 2 partials
+    (16, 9_000_000, 9_000_000, 1, 1),      # 977 chunks of 18 tiles
+    (16, 20_000_000, 20_000_000, 5, 2),    # 1,221 chunks of 32 tiles: five launches, groups of 3
     (16, 20_000_000, 9_000_000, 5, 2),     # three buckets, the last of 123 chunks
-    (64, 3_000_000, 3_000_000, 1, 1),      # 733 chunks of four workers per wavefront
-    (255, 600_000, 600_000, 1, 1),         # 586 chunks, one thread per worker in the groups
-    (8, 6_000_000, 1_310_720, 1, 1),       # five buckets in one launch
+    (64, 3_000_000, 3_000_000, 1, 1),      # 977 chunks, four workers per wavefront
+    (255, 600_000, 600_000, 1, 1),         # 938 chunks, one thread per worker in the groups
+    (16, 1_000_000, 1_000_000, 1, 1),      # 977 chunks of 2 tiles
+    (8, 6_000_000, 1_310_720, 1, 1),       # five buckets of at most 214 chunks: partials read directly
 ])
 def test_pass1_launch_shapes(W, n, bucket_n, launches, launches_nosigns):
     assert nf.nf_pass1_launches(W, n, bucket_n) == launches

@@ -1,7 +1,7 @@
 """Pass-1 chunks whose elements are all routed to FP32, with more than 16
 workers (several workers per wavefront).  Such a chunk is read element-major
 in groups of workers, each lane keeping its running FP32 sums from one group
-to the next.  The sizes give more than 512 chunks, so every chunk has its
+to the next.  The sizes give more than 1,024 chunks, so every chunk has its
 full number of tiles (up to 16 steps of 64 elements per wavefront).  Long
 FP32 runs hold whole routed chunks; non-finite values sit inside them, in
 workers of the first, a middle and the last group.  Every output is checked
@@ -30,7 +30,7 @@ def _chunk(W):
 
 @pytest.mark.parametrize("W", [17, 32, 33, 64, 100, 129, 255])
 def test_routed_chunks_wide(W):
-    n = 520 * _chunk(W) + 777
+    n = 1040 * _chunk(W) + 777
     lay = synth.small(W, n, 4000 + W, elig_frac=0.5, nruns=40)
     g = synth.generate_host(lay)
     m = nfo.mask_from_segments(*synth.mask_segments(lay), n)
