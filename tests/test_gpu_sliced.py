@@ -3,7 +3,7 @@ decode against the oracle, through the C ABI.
 
 Bars: compacted rows and compacted-order counts bit-exact; per-slice FP64
 sums within 1e-12 relative (different fixed summation order); scales within
-1e-6 relative (spec bar), and equal in the usual case; decoded values
+1e-6 relative (the FP32 bar of every parity test), and equal in the usual case; decoded values
 exactly fl32(scale_gpu[s] * q[c]) and within 1e-6 of the oracle.
 """
 import numpy as np
