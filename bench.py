@@ -285,7 +285,9 @@ def controller_run(args):
 def sliced_run(args, reps=5):
     """Kernel times of the compacted eligible-only payload and per-slice scales over the whole
     workload (every eligible tensor of the binding is one slice): compaction of the positional sign
-    rows, the per-slice statistics and scales, and the count + decode from the compacted rows."""
+    rows, the per-slice statistics and scales (with a second read of the gradients, and from pass
+    1's chunk partials), the count + decode from the compacted rows, and the whole sliced step:
+    pass 1 over the buffer as one bucket, compaction, scales from pass 1, count + decode."""
     import numpy as np
     import torch
     import paper_2606_25759_amd as nf
@@ -325,6 +327,18 @@ def sliced_run(args, reps=5):
         torch.cuda.synchronize()
         return a.elapsed_time(b) / reps  # ms per call
 
+    # pass 1 over the whole buffer as one bucket, whose chunk partials give the slice statistics
+    ws1 = nf.empty_workspace(nf.nf_workspace_bytes(W, n), dev)
+    stats1 = torch.empty(W * nf.STATS_BYTES, dtype=torch.uint8, device=dev)
+    t_pack = timed(lambda: nf.nf_pack_signs(grads, n, mask, bits, stats1, ws1))
+    t_from1 = timed(lambda: nf.nf_slice_scales_from_pass1(grads, n, sl, sums, scales, ws1))
+
+    def chain():
+        nf.nf_pack_signs(grads, n, mask, bits, stats1, ws1)
+        nf.nf_compact_signs(bits, W, n, sl, cbits)
+        nf.nf_slice_scales_from_pass1(grads, n, sl, sums, scales, ws1)
+        nf.nf_compact_signcount_reduce(cbits, W, sl, scales, 0, counts_c, out)
+    t_chain = timed(chain)
     t_compact = timed(lambda: nf.nf_compact_signs(bits, W, n, sl, cbits))
     t_scales = timed(lambda: nf.nf_slice_scales(grads, sl, sums, scales, ws2))
     t_reduce = timed(lambda: nf.nf_compact_signcount_reduce(cbits, W, sl, scales, 0, counts_c, out))
@@ -338,6 +352,10 @@ def sliced_run(args, reps=5):
            "config": {"workload": lay.name, "W": W, "n": n, "n_eligible": nE, "slices": S},
            "compact_ms": round(t_compact, 4), "compact_gbs": gbs(b_compact, t_compact),
            "slice_scales_ms": round(t_scales, 4), "slice_scales_gbs": gbs(b_scales, t_scales),
+           "slice_scales_from_pass1_ms": round(t_from1, 4),
+           "pack_one_bucket_ms": round(t_pack, 4),
+           "sliced_step_ms": round(t_chain, 4),
+           "sliced_step_gbs_fp32_equiv": gbs(lay.input_bytes(), t_chain),
            "compact_reduce_ms": round(t_reduce, 4), "compact_reduce_gbs": gbs(b_reduce, t_reduce),
            "of_which_count_ms": round(t_count, 4),
            "payload_bytes_per_worker": {"positional": 8 * nw, "compacted": 8 * nwc},

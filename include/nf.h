@@ -300,6 +300,25 @@ nf_status nf_slice_scales(const float* grads, int64_t worker_stride, int32_t W, 
                           double* sums, float* scales, void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * Per-slice statistics and scales as nf_slice_scales computes them (§5.2's
+ * mean-absolute scale per eligible slice), without a second read of the
+ * gradients: taken from the per-chunk partial statistics that pass 1 leaves
+ * in its workspace.  Call it after nf_pack_signs (with or without stats),
+ * nf_bucket_health or nf_route_bucket over the same grads, worker_stride,
+ * W and n, with a mask that is exactly the union of the slices, on the same
+ * stream and with the same workspace ws (ws_bytes >= nf_workspace_bytes(W,
+ * n); read only), before anything else writes to it.  Only the parts of
+ * the slices in pass-1 chunks that two slices share are read again (at most
+ * two chunks per slice).  off, len: device copies of the slice table (S
+ * slices, sorted, disjoint, non-empty, within [0, n)).  sums[s * W + w]
+ * (FP64; the chunks' partials in a fixed order, within 1e-12 relative of a
+ * sequential sum) and scales[s]: device arrays.  S = 0 is a no-op.
+ */
+nf_status nf_slice_scales_from_pass1(const float* grads, int64_t worker_stride, int32_t W, int64_t n,
+                                     const int64_t* off, const int64_t* len, int64_t S, double* sums,
+                                     float* scales, const void* ws, size_t ws_bytes, void* stream);
+
+/*
  * Read side over the compacted payload (§3.3 step 7 with per-slice scales):
  * counts_c[r] = sum over the W compacted rows of bit r (n_E bytes, in
  * compacted order; required, 4-byte aligned), then, when out is not NULL, out[i] =

@@ -32,7 +32,7 @@ NF_FORMAT_BINARY, NF_FORMAT_TERNARY = 0, 1
 EXPORTS = ["nf_abi_version", "nf_last_error", "nf_mask_from_segments", "nf_workspace_bytes",
            "nf_bucket_health", "nf_pack_signs", "nf_fp32_reduce", "nf_signcount_reduce",
            "nf_route_decide", "nf_route_bucket", "nf_workspace_bytes_buckets", "nf_route_buckets",
-           "nf_set_phase_events", "nf_pass1_launches", "nf_ternary_threshold", "nf_pack_ternary",
+           "nf_set_phase_events", "nf_pass1_launches", "nf_slice_scales_from_pass1", "nf_ternary_threshold", "nf_pack_ternary",
            "nf_ternary_reduce", "nf_partial_counts", "nf_partial_count_reduce", "nf_stock_signcount",
            "nf_supervisor_init", "nf_supervisor_policy", "nf_supervisor_update", "nf_endpoint_guard",
            "nf_sliced_layout_sizes", "nf_sliced_layout", "nf_compact_signs", "nf_slice_workspace_bytes",
@@ -132,6 +132,7 @@ def load(path=None):
         "nf_route_buckets": (ctypes.c_int, [_P, _I64, _I32, _I64, _I64, _P, _P, _P, _I64, _P, _P,
                                             _P, _P, _P, _SZ, _P]),
         "nf_set_phase_events": (ctypes.c_int, [_P, _P, _P, _P]),
+        "nf_slice_scales_from_pass1": (_I32, [_P, _I64, _I32, _I64, _P, _P, _I64, _P, _P, _P, _SZ, _P]),
         "nf_pass1_launches": (_I64, [_I32, _I64, _I64, _I32]),
         "nf_ternary_threshold": (ctypes.c_int, [_P, _I32, _I64, ctypes.c_float, _P]),
         "nf_pack_ternary": (ctypes.c_int, [_P, _I64, _I32, _I64, _P, _P, _P, _I64, _P]),
@@ -410,6 +411,16 @@ def nf_slice_scales(grads, lay, sums, scales, ws, stream=None):
                                   lay.S, lay.segments, _dev_ptr(sums, torch.float64, "sums"),
                                   _dev_ptr(scales, torch.float32, "scales"), _dev_ptr(ws, torch.uint8, "ws"),
                                   ws.numel(), _stream(stream)))
+
+
+def nf_slice_scales_from_pass1(grads, n, lay, sums, scales, ws, stream=None):
+    """Per-slice sums and scales from the partials a pass 1 over (grads, n,
+    lay's mask) left in ws."""
+    g, stride, W = _rows(grads)
+    _check(load().nf_slice_scales_from_pass1(g, stride, W, n, lay.d_off.data_ptr(), lay.d_len.data_ptr(), lay.S,
+                                             _dev_ptr(sums, torch.float64, "sums"),
+                                             _dev_ptr(scales, torch.float32, "scales"),
+                                             _dev_ptr(ws, torch.uint8, "ws"), ws.numel(), _stream(stream)))
 
 
 def nf_compact_signcount_reduce(cbits, W, lay, scales, decode_mode, counts_c, out, stream=None):

@@ -81,7 +81,7 @@ nf_status check_policy(const nf_route_policy* p) {
   return NF_OK;
 }
 
-nf_status check_ws(void* ws, size_t ws_bytes, size_t need) {
+nf_status check_ws(const void* ws, size_t ws_bytes, size_t need) {
   if (ws_bytes < need)
     return fail(NF_ERR_WORKSPACE, "workspace of %zu bytes < %zu required", ws_bytes, need);
   if (need && !ws) return fail(NF_ERR_WORKSPACE, "workspace is NULL");
@@ -629,6 +629,36 @@ nf_status nf_slice_scales(const float* grads, int64_t worker_stride, int32_t W, 
   a.W = W;
   hipError_t e = nf::launch_slice_scales(a, segments, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "slice scale launch");
+  return ok();
+}
+
+nf_status nf_slice_scales_from_pass1(const float* grads, int64_t worker_stride, int32_t W, int64_t n,
+                                     const int64_t* off, const int64_t* len, int64_t S, double* sums,
+                                     float* scales, const void* ws, size_t ws_bytes, void* stream) {
+  if (W < 1 || W > 255) return fail(NF_ERR_INVALID_ARG, "W=%d outside [1, 255]", W);
+  if (n < 0 || S < 0 || S > n || S > 0x7fffffff) return fail(NF_ERR_INVALID_ARG, "need 0 <= S <= n, S < 2^31");
+  if (worker_stride < n) return fail(NF_ERR_INVALID_ARG, "worker_stride %lld < n %lld", (long long)worker_stride,
+                                     (long long)n);
+  if (S == 0) return ok();
+  if (!grads || !off || !len || !sums || !scales) return fail(NF_ERR_INVALID_ARG, "NULL argument");
+  if (!aligned(grads, 4) || !aligned(sums, 8) || !aligned(scales, 4) || !aligned(off, 8) || !aligned(len, 8))
+    return fail(NF_ERR_ALIGNMENT, "misaligned argument");
+  const nf::Geometry geo = nf::make_geometry(W, n, n);
+  const nf::WorkspaceLayout lay = nf::workspace_layout(geo);
+  NF_TRY(check_ws(ws, ws_bytes, lay.total));
+  nf::SliceChunkArgs a;
+  a.g = grads;
+  a.wstride = worker_stride;
+  a.part = reinterpret_cast<const nf::Partial*>(static_cast<const char*>(ws) + lay.partials);
+  a.off = off;
+  a.len = len;
+  a.sums = sums;
+  a.scales = scales;
+  a.S = S;
+  a.CH = (int64_t)geo.G * geo.tile;
+  a.W = W;
+  hipError_t e = nf::launch_slice_chunks(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "slice statistics launch");
   return ok();
 }
 

@@ -372,6 +372,20 @@ struct CompactArgs {
   int32_t W;                // rows (filled by the launcher)
 };
 
+// Per-slice statistics from pass 1's chunk partials (one bucket of n
+// elements, chunks of CH elements).
+struct SliceChunkArgs {
+  const float* g;
+  int64_t wstride;
+  const Partial* part;  // [chunk][W]: pass 1's partial slots
+  const int64_t* off;   // [S]
+  const int64_t* len;   // [S]
+  double* sums;         // [S][W]
+  float* scales;        // [S]
+  int64_t S, CH;
+  int32_t W;
+};
+
 struct SliceArgs {
   const float* g;
   int64_t wstride;
@@ -399,6 +413,7 @@ struct ExpandArgs {
 
 hipError_t launch_compact(const CompactArgs& a, int W, hipStream_t s);
 hipError_t launch_slice_scales(const SliceArgs& a, int64_t segments, hipStream_t s);
+hipError_t launch_slice_chunks(const SliceChunkArgs& a, hipStream_t s);
 hipError_t launch_cexpand(const ExpandArgs& a, hipStream_t s);
 
 // Sets the thread-local message of nf_last_error (nf_api.hip) and returns st.

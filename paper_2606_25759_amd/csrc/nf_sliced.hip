@@ -182,6 +182,54 @@ __global__ __launch_bounds__(kThreadsS) void k_slice_scale(SliceArgs a) {
   }
 }
 
+// The same statistics without a second read of the gradients, from the
+// partials pass 1 left in its workspace: block s takes slice s = [o, e), in
+// chunks c0 = o / CH .. c1 = (e - 1) / CH.  A chunk that no other slice
+// touches holds only slice s's eligible elements, so its pass-1 partial is
+// slice s's share of it.  The first chunk is shared when the previous slice
+// ends in it, the last when the next slice starts in it (slices are sorted
+// and disjoint); a shared chunk's part of the slice is read and summed here.
+// Thread t adds the owned chunks t, t + 256, ... in order, then its share of
+// the shared parts' elements; a fixed tree adds the threads.
+__global__ __launch_bounds__(kThreadsS) void k_slice_chunks(SliceChunkArgs a) {
+  __shared__ double red[kThreadsS];
+  const int64_t s = blockIdx.x;
+  const int64_t o = a.off[s], e = o + a.len[s];
+  const int64_t c0 = o / a.CH, c1 = (e - 1) / a.CH;
+  const bool share0 = s > 0 && (a.off[s - 1] + a.len[s - 1] - 1) / a.CH == c0;
+  const bool share1 = s + 1 < a.S && a.off[s + 1] / a.CH == c1;
+  // parts of the slice read here: [r0, r0e) in chunk c0 and [r1, e) in c1
+  int64_t r0 = o, r0e = o, r1 = e;
+  if (c0 == c1) {
+    if (share0 || share1) r0e = e;
+  } else {
+    if (share0) r0e = (c0 + 1) * a.CH;
+    if (share1) r1 = c1 * a.CH;
+  }
+  const int64_t cb = r0e > r0 ? c0 + 1 : c0;  // owned chunks [cb, ce)
+  const int64_t ce = (c0 == c1) ? (r0e > r0 ? c0 : c0 + 1) : (r1 < e ? c1 : c1 + 1);
+  for (int w = 0; w < a.W; ++w) {
+    double t = 0.0;
+    for (int64_t c = cb + threadIdx.x; c < ce; c += kThreadsS) t += a.part[c * a.W + w].sabs;
+    const float* row = a.g + (int64_t)w * a.wstride;
+    for (int64_t i = r0 + threadIdx.x; i < r0e; i += kThreadsS) t += __builtin_fabs((double)row[i]);
+    for (int64_t i = r1 + threadIdx.x; i < e; i += kThreadsS) t += __builtin_fabs((double)row[i]);
+    red[threadIdx.x] = t;
+    __syncthreads();
+    for (int h = kThreadsS / 2; h > 0; h >>= 1) {
+      if ((int)threadIdx.x < h) red[threadIdx.x] += red[threadIdx.x + h];
+      __syncthreads();
+    }
+    if (threadIdx.x == 0) a.sums[s * a.W + w] = red[0];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    double acc = 0.0;
+    for (int w = 0; w < a.W; ++w) acc += a.sums[s * a.W + w] / (double)a.len[s];
+    a.scales[s] = (float)(acc / (double)a.W);
+  }
+}
+
 // A wavefront takes 64 consecutive positional words per task.  Lane t loads
 // mask word k0 + t; a scan of the popcounts gives each word's first rank
 // (prefix[k0] + the eligible elements of the task's earlier words).  The
@@ -323,6 +371,11 @@ hipError_t launch_slice_scales(const SliceArgs& a, int64_t segments, hipStream_t
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_slice_scale, dim3((unsigned)a.S), dim3(kThreadsS), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_slice_chunks(const SliceChunkArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(k_slice_chunks, dim3((unsigned)a.S), dim3(kThreadsS), 0, s, a);
   return hipGetLastError();
 }
 

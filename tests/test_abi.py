@@ -181,6 +181,21 @@ def test_invalid_arguments_return_codes_without_launch():
     need = nf.nf_slice_workspace_bytes(2, 3)
     assert lib.nf_slice_scales(fake, 640, 2, fake, fake, fake, 3, 3, fake, fake, ws, need - 1, None) == \
         nf.NF_ERR_WORKSPACE
+    # slice statistics from pass 1's partials: W, S <= n, stride, NULLs, alignment, workspace; S = 0 is a no-op
+    wneed = nf.nf_workspace_bytes(2, 640)
+    assert lib.nf_slice_scales_from_pass1(fake, 640, 0, 640, fake, fake, 3, fake, fake, ws, wneed, None) == \
+        nf.NF_ERR_INVALID_ARG
+    assert lib.nf_slice_scales_from_pass1(fake, 640, 2, 2, fake, fake, 3, fake, fake, ws, wneed, None) == \
+        nf.NF_ERR_INVALID_ARG
+    assert lib.nf_slice_scales_from_pass1(fake, 639, 2, 640, fake, fake, 3, fake, fake, ws, wneed, None) == \
+        nf.NF_ERR_INVALID_ARG
+    assert lib.nf_slice_scales_from_pass1(fake, 640, 2, 640, None, fake, 3, fake, fake, ws, wneed, None) == \
+        nf.NF_ERR_INVALID_ARG
+    assert lib.nf_slice_scales_from_pass1(fake, 640, 2, 640, P(0x1004), fake, 3, fake, fake, ws, wneed, None) == \
+        nf.NF_ERR_ALIGNMENT
+    assert lib.nf_slice_scales_from_pass1(fake, 640, 2, 640, fake, fake, 3, fake, fake, ws, wneed - 1, None) == \
+        nf.NF_ERR_WORKSPACE
+    assert lib.nf_slice_scales_from_pass1(None, 640, 2, 640, None, None, 0, None, None, None, 0, None) == nf.NF_OK
     assert lib.nf_compact_signcount_reduce(fake, 10, 2, 640, fake, fake, fake, fake, 2, 600, fake, 0, None, fake,
                                            None) == nf.NF_ERR_INVALID_ARG
     assert lib.nf_compact_signcount_reduce(fake, 10, 2, 640, fake, fake, fake, fake, 0, 600, fake, 0, fake, fake,

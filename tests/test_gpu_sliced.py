@@ -64,6 +64,57 @@ def test_slice_scales_match_oracle(W, n, count, max_len):
     assert np.mean(sc == ref_sc) >= 0.9, "scales equal in the usual case"
 
 
+# (W, n, slice count, longest slice): tiny slices that share pass-1 chunks,
+# slices across many chunks, a slice inside one chunk, many slices
+FROM_PASS1 = CASES + [(16, 3_000_000, 40, 400_000), (16, 2_000_000, 3000, 600), (64, 700_000, 6, 300_000),
+                      (4, 5_000_000, 25, 1_000_000), (255, 100_000, 50, 5000)]
+
+
+@pytest.mark.parametrize("W,n,count,max_len", FROM_PASS1)
+@pytest.mark.parametrize("first", ["pack", "pack_stats", "health", "route"])
+def test_slice_scales_from_pass1(W, n, count, max_len, first):
+    lay, g = case(W, n, count, max_len, 11 * W + n)
+    gp = np.zeros((W, -(-n // 64) * 64), np.float32)  # pass 1 takes rows of 16-byte multiples
+    gp[:, :n] = g
+    gd = to_dev(gp)
+    ws = nf.empty_workspace(nf.nf_workspace_bytes(W, n), DEV)
+    nw = (n + 63) // 64
+    stats = torch.zeros(W * nf.STATS_BYTES, dtype=torch.uint8, device=DEV)
+    bits = torch.zeros((W, nw), dtype=torch.int64, device=DEV)
+    if first == "pack":
+        nf.nf_pack_signs(gd, n, lay.d_mask, bits, None, ws)
+    elif first == "pack_stats":
+        nf.nf_pack_signs(gd, n, lay.d_mask, bits, stats, ws)
+    elif first == "health":
+        nf.nf_bucket_health(gd, n, lay.d_mask, stats, ws)
+    else:
+        counts = torch.zeros(n, dtype=torch.uint8, device=DEV)
+        out = torch.zeros(n, dtype=torch.float32, device=DEV)
+        dec = torch.zeros(nf.DECISION_BYTES, dtype=torch.uint8, device=DEV)
+        nf.nf_route_bucket(gd, n, lay.d_mask, nf.policy(), bits, counts, out, stats, dec, ws)
+    S = max(lay.S, 1)
+    sums = torch.full((S, W), float("nan"), dtype=torch.float64, device=DEV)
+    scales = torch.full((S,), float("nan"), dtype=torch.float32, device=DEV)
+    nf.nf_slice_scales_from_pass1(gd, n, lay, sums, scales, ws)
+    # the two-pass statistics on the GPU, for comparison
+    sums2 = torch.zeros((S, W), dtype=torch.float64, device=DEV)
+    scales2 = torch.zeros(S, dtype=torch.float32, device=DEV)
+    ws2 = nf.empty_workspace(nf.nf_slice_workspace_bytes(W, lay.segments), DEV)
+    nf.nf_slice_scales(gd, lay, sums2, scales2, ws2)
+    torch.cuda.synchronize()
+    ref_sums, ref_sc = nfo.slice_scales(g, lay.off, lay.len)
+    s1 = sums.cpu().numpy()[:lay.S]
+    sc = scales.cpu().numpy()[:lay.S]
+    assert np.allclose(s1, ref_sums, rtol=1e-12, atol=0), "slice sums"
+    assert np.all(np.abs(sc - ref_sc) <= 1e-6 * np.abs(ref_sc)), "slice scales"
+    assert np.mean(sc == ref_sc) >= 0.9, "scales equal in the usual case"
+    assert np.allclose(s1, sums2.cpu().numpy()[:lay.S], rtol=1e-12, atol=0), "same sums as the two-pass statistics"
+    if first == "pack_stats":
+        # every slice's sums add up to the bucket's eligible |g| sums of pass 1
+        st = nf.stats_host(stats, W)[0]
+        assert np.allclose(s1.sum(axis=0), st["sum_abs_elig"], rtol=1e-12, atol=0)
+
+
 @pytest.mark.parametrize("W,n,count,max_len", CASES)
 @pytest.mark.parametrize("mode", [nfo.DECODE_SOFT, nfo.DECODE_MAJORITY])
 def test_sliced_reduce_matches_oracle(W, n, count, max_len, mode):
