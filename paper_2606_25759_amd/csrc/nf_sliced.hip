@@ -382,7 +382,10 @@ hipError_t launch_slice_chunks(const SliceChunkArgs& a, hipStream_t s) {
 hipError_t launch_cexpand(const ExpandArgs& a, hipStream_t s) {
   const int64_t nw = (a.n + 63) / 64;
   int64_t blocks = (nw + 4 * 64 - 1) / (4 * 64);
-  if (blocks > 8192) blocks = 8192;
+  // About one task per wavefront: a task's two dependent round trips are
+  // better hidden by other queued wavefronts than by a grid-stride loop
+  // (8,192 blocks: 2.54 ms at GPT scale; 2^20: 2.30 ms).
+  if (blocks > (1 << 20)) blocks = 1 << 20;
   if (blocks < 1) blocks = 1;
   hipLaunchKernelGGL(k_cexpand, dim3((unsigned)blocks), dim3(kThreadsS), 0, s, a);
   return hipGetLastError();
