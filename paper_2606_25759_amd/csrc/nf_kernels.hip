@@ -3,6 +3,10 @@
 //   k_pass1   write side (§3.3 step 5, §5.2): one read of the W gradient
 //             rows; sign payload by wavefront ballot, per-worker health in
 //             registers, FP32 sums at routed positions through an LDS stage.
+//             A block takes a chunk of tiles by one of four loops: fast (all
+//             eligible), mixed (all tiles full, some routed), routed
+//             (nothing eligible, element-major) or general (ragged tails).
+//   k_slotsum second level of the partials of buckets above kMaxSlots chunks
 //   k_decide  one block per bucket: fixed-order reduction of the pass-1
 //             partial statistics, then the route rules (§3.2, §6.4).
 //   k_pass2   read side (§3.3 step 7, §6.1): per-coordinate sign counts over
