@@ -239,8 +239,10 @@ __global__ __launch_bounds__(kThreadsS) void k_slice_chunks(SliceChunkArgs a) {
 // first rank - prefix[k0] + the eligible bits below j) in LDS, its slice is
 // the one whose compacted range holds its rank (walked forward per lane,
 // ranks only grow).  The task's mask words and first ranks are read back
-// from LDS as broadcasts, four words at a time.  Slice starts and scales sit
-// in LDS when the table has at most kExpandLdsSlices slices.
+// from LDS as broadcasts, four words at a time.  A task inside one slice (the
+// usual case) takes its scale once; others walk the slices per element.
+// Slice starts and scales sit in LDS when the table has at most
+// kExpandLdsSlices slices.
 constexpr int kExpandLdsSlices = 1024;
 constexpr int kExpandStageWords = 4096 / 4 + 2;  // dwords per wavefront: 4096 counts + alignment
 constexpr int kExpandUnroll = 4;                 // words decoded together
@@ -327,6 +329,30 @@ __global__ __launch_bounds__(kThreadsS) void k_cexpand(ExpandArgs a) {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     int64_t s = slice_of_rank(rstart, a.S, base);  // every rank of the task is >= base
     const uint64_t below = (1ull << lane) - 1ull;
+    if (s + 1 >= a.S || rstart[s + 1] >= base + total) {
+      // The whole task lies in slice s (the usual case: slices are far
+      // longer than a task): one scale, no slice walk per element.
+      const float scale = scales[s];
+      float* orow = a.out + 64 * k0 + lane;
+      for (int t = 0; t < nk; t += kExpandUnroll) {
+        bool el[kExpandUnroll];
+        uint8_t c[kExpandUnroll];
+#pragma unroll
+        for (int u = 0; u < kExpandUnroll; ++u) {
+          const int tt = t + u < nk ? t + u : nk - 1;
+          const uint64_t m = t + u < nk ? tw[tt] : 0ull;
+          el[u] = (m >> lane) & 1ull;
+          c[u] = el[u] ? stb[off + te[tt] + __popcll(m & below)] : 0;
+        }
+#pragma unroll
+        for (int u = 0; u < kExpandUnroll; ++u)
+          if (el[u]) orow[64 * (t + u)] = scale * tab[c[u]];
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      continue;
+    }
     for (int t = 0; t < nk; t += kExpandUnroll) {
       bool el[kExpandUnroll];
       int rel[kExpandUnroll];
