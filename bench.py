@@ -95,9 +95,9 @@ class HipEvents:
 
 
 def kernel_source_sha():
-    """Hash of the pass-1 kernel source and the geometry that shapes its launches."""
+    """Hash of the pass-1 kernel source, its device helpers and the geometry that shapes its launches."""
     h = hashlib.sha256()
-    for name in ("nf_kernels.hip", "nf_internal.h"):
+    for name in ("nf_pass1.hip", "nf_device.h", "nf_internal.h"):
         h.update(open(os.path.join(ROOT, "paper_2606_25759_amd", "csrc", name), "rb").read())
     return h.hexdigest()[:16]
 

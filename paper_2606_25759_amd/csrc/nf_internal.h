@@ -419,7 +419,7 @@ hipError_t launch_cexpand(const ExpandArgs& a, hipStream_t s);
 // Sets the thread-local message of nf_last_error (nf_api.hip) and returns st.
 nf_status set_error(nf_status st, const char* msg);
 
-// Launchers (nf_kernels.hip).
+// Launchers (nf_pass1.hip, nf_pass2.hip, nf_ternary.hip, nf_sliced.hip).
 hipError_t launch_pass1(const Geometry& geo, const Pass1Args& a, hipStream_t s);
 hipError_t launch_decide(const Geometry& geo, const DecideArgs& a, hipStream_t s);
 hipError_t launch_pass2(const Geometry& geo, const Pass2Args& a, hipStream_t s);

@@ -11,23 +11,13 @@
 //
 // The counts over the compacted rows come from pass 2's bit-sliced counter
 // (k_pass2), run on the compacted rows as on any payload.
-#include "nf_internal.h"
+#include "nf_device.h"
 
 namespace nf {
 
 namespace {
 
 constexpr int kThreadsS = 256;
-
-__device__ __forceinline__ uint64_t uniform64(uint64_t x) {
-  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
-  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(x >> 32));
-  return ((uint64_t)hi << 32) | lo;
-}
-
-__device__ __forceinline__ uint64_t low_mask(int64_t r) {
-  return r >= 64 ? ~0ull : (r <= 0 ? 0ull : ((1ull << r) - 1ull));
-}
 
 // The bits of x at the positions of the set bits of m, packed towards bit 0
 // in their order ("compress", the generalized extract of Hacker's Delight,
@@ -75,15 +65,15 @@ __global__ __launch_bounds__(kThreadsS) void k_compact(CompactArgs a) {
     const int64_t k = a.start[o];
     const int skip = (int)(r0 - (int64_t)a.prefix[k]);
     uint64_t m0 = a.mask[k];
-    if (k == nw - 1) m0 &= low_mask(a.n - 64 * k);
+    if (k == nw - 1) m0 &= low_bits(a.n - 64 * k);
     const int c0 = __popcll(m0) - skip;  // ranks of word k at or above 64o (>= 1)
     uint64_t m1 = 0;
     if (c0 < need && k + 1 < nw) {
       m1 = a.mask[k + 1];
-      if (k + 1 == nw - 1) m1 &= low_mask(a.n - 64 * (k + 1));
+      if (k + 1 == nw - 1) m1 &= low_bits(a.n - 64 * (k + 1));
     }
     const bool two = c0 >= need || c0 + __popcll(m1) >= need;
-    const uint64_t keep = low_mask(need);
+    const uint64_t keep = low_bits(need);
     if (two) {
       for (int w0 = 0; w0 < W; w0 += kCompactRows) {
         uint64_t x0[kCompactRows], x1[kCompactRows];
@@ -119,7 +109,7 @@ __global__ __launch_bounds__(kThreadsS) void k_compact(CompactArgs a) {
         sk = 0;
         if (got >= need || ++kk >= nw) break;
         m = a.mask[kk];
-        if (kk == nw - 1) m &= low_mask(a.n - 64 * kk);
+        if (kk == nw - 1) m &= low_bits(a.n - 64 * kk);
       }
       a.cbits[(int64_t)w * a.cstride + o] = acc & keep;
     }
@@ -287,7 +277,7 @@ __global__ __launch_bounds__(kThreadsS) void k_cexpand(ExpandArgs a) {
   for (int64_t k0 = wave * 64; k0 < nw; k0 += waves * 64) {
     const int nk = (int)((nw - k0) < 64 ? (nw - k0) : 64);
     uint64_t mw = lane < nk ? a.mask[k0 + lane] : 0ull;
-    if (k0 + lane == nw - 1) mw &= low_mask(a.n - 64 * (nw - 1));
+    if (k0 + lane == nw - 1) mw &= low_bits(a.n - 64 * (nw - 1));
     // inclusive scan of the popcounts over the wavefront
     int incl = __popcll(mw);
 #pragma unroll
