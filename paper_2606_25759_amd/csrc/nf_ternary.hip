@@ -114,9 +114,30 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
 
   float xa[NX], xb[NX];
   uint64_t ma[NW], mb[NW];
+  if (te_full > tb) issue(tb, xa, ma);
+  // A chunk with no eligible element: both planes are zero and nothing more
+  // is read (mask bits past the bucket's end do not count).
+  {
+    const int64_t cn = ((te * tile < nbe) ? te * tile : nbe) - tb * tile;  // elements of the chunk
+    const int nwc = cn > 0 ? (int)((cn + 63) / 64) : 0;
+    const uint64_t* cm = a.mask + (base + tb * tile) / 64;
+    int any = 0;
+    for (int i = threadIdx.x; i < nwc; i += kThreads1)
+      any |= (cm[i] & (i == nwc - 1 ? low_bits(cn - 64 * (int64_t)i) : ~0ull)) != 0ull;
+    if (!__syncthreads_or(any)) {
+      if (te_full > tb) consume(xa);
+      const int64_t gz = (base + tb * tile) / 64;
+      for (int i = threadIdx.x; i < a.W * nwc; i += kThreads1) {
+        const int w = i / nwc;
+        const int o = i - w * nwc;
+        a.bits[(int64_t)w * a.bstride + gz + o] = 0ull;
+        a.bits[(int64_t)(a.W + w) * a.bstride + gz + o] = 0ull;
+      }
+      return;
+    }
+  }
   int64_t t = tb;
   if (te_full > tb) {
-    issue(tb, xa, ma);
     // Pairs of full tiles with the next one in flight, then the odd one.
     for (int64_t p = (te_full - tb) >> 1; p > 0; --p, t += 2) {
       issue(t + 1, xb, mb);
