@@ -237,6 +237,8 @@ __global__ __launch_bounds__(kThreads2) void k_psum(PsumArgs a) {
     const int cnt = (a.n - i0) < 16 ? (int)(a.n - i0) : 16;
     uint32_t c[4] = {0u, 0u, 0u, 0u};
     if (cnt == 16) {
+      // unrolled so that the partial rows' loads are in flight together
+#pragma unroll 8
       for (int gr = 0; gr < a.G; ++gr) {
         const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(a.partial + (int64_t)gr * a.pstride + i0));
         c[0] += v[0];
@@ -265,7 +267,11 @@ __global__ __launch_bounds__(kThreads2) void k_psum(PsumArgs a) {
         const int64_t j = i0 + 4 * q;
         if (cnt == 16 && o16 && mq == 15u) {
           const f32x4 y = {tab[cw & 255u], tab[(cw >> 8) & 255u], tab[(cw >> 16) & 255u], tab[cw >> 24]};
-          __builtin_nontemporal_store(y, reinterpret_cast<f32x4*>(a.out + j));
+          // A cached store: the four stores of a thread are 64 bytes apart
+          // across the lanes, and L2 merges them into whole lines (as
+          // nontemporal stores the exchange took 38 us instead of 16 us at
+          // 6,553,600 elements).
+          *reinterpret_cast<f32x4*>(a.out + j) = y;
         } else {
           for (int e = 0; e < 4; ++e)
             if (4 * q + e < cnt && ((mq >> e) & 1u)) a.out[j + e] = tab[(cw >> (8 * e)) & 255u];
