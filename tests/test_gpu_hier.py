@@ -85,6 +85,13 @@ def check_partial_count_reduce(W, P, n, mode):
     assert np.all(np.isnan(o[~m])), "routed positions untouched"
 
 
+@pytest.mark.parametrize("W,P", [(16, 4), (64, 8)])
+def test_contrast_shapes(W, P):
+    """The shapes `bench.py --contrast` times at a full bucket: 4 nodes x 4
+    GPUs and 8 x 8, 6,553,600 elements."""
+    check_partial_count_reduce(W, P, 6_553_600, nfo.DECODE_SOFT)
+
+
 @pytest.mark.parametrize("W,R", [(1, 1), (8, 8), (16, 3), (64, 2), (255, 2)])
 @pytest.mark.parametrize("n", [1, 65, 4097, 100_003])
 def test_stock_replicas_equal_direct_count(W, R, n):
