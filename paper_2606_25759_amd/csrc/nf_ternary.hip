@@ -70,9 +70,11 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
   const float* dp = a.g + (int64_t)wg * a.wstride + base + lane;
   const uint64_t* dm = a.mask + base / 64;
 
+  bool chunk_all = false, chunk_any = true;  // set below, after the first tile's loads are out
+
   // Loads of a full tile (or, for an idle wavefront or a tile past the full
   // ones, of the bucket's first words).
-  auto issue = [&](int64_t tt, float (&X)[NX], uint64_t (&M)[NW]) {
+  auto issue_data = [&](int64_t tt, float (&X)[NX]) {
     const bool ok = active && tt < te_full;
     const int64_t o = tt * tile;
 #pragma unroll
@@ -81,9 +83,23 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
 #pragma unroll
       for (int k = 0; k < NW; ++k) X[j * NW + k] = __builtin_nontemporal_load(row + 64 * k);
     }
+  };
+  auto issue_mask = [&](int64_t tt, uint64_t (&M)[NW]) {
+    const bool ok = active && tt < te_full;
+    const int64_t o = tt * tile;
+    if (chunk_all) {
+      // every element of the chunk eligible: no mask words to load
+#pragma unroll
+      for (int k = 0; k < NW; ++k) M[k] = ~0ull;
+      return;
+    }
     const uint64_t* mrow = ok ? mbase + o / 64 : dm;
 #pragma unroll
     for (int k = 0; k < NW; ++k) M[k] = uniform64(mrow[k]);
+  };
+  auto issue = [&](int64_t tt, float (&X)[NX], uint64_t (&M)[NW]) {
+    issue_data(tt, X);
+    issue_mask(tt, M);
   };
   auto body = [&](int64_t t, const float (&X)[NX], const uint64_t (&M)[NW]) {
     const int ti = (int)(t - tb);
@@ -114,18 +130,30 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
 
   float xa[NX], xb[NX];
   uint64_t ma[NW], mb[NW];
-  if (te_full > tb) issue(tb, xa, ma);
-  // A chunk with no eligible element: both planes are zero and nothing more
-  // is read (mask bits past the bucket's end do not count).
+  if (te_full > tb) issue_data(tb, xa);
+  // Whether every element of the chunk is eligible (then the tiles need no
+  // mask words), and whether any is: a chunk with none is not read.
   {
     const int64_t cn = ((te * tile < nbe) ? te * tile : nbe) - tb * tile;  // elements of the chunk
     const int nwc = cn > 0 ? (int)((cn + 63) / 64) : 0;
     const uint64_t* cm = a.mask + (base + tb * tile) / 64;
-    int any = 0;
-    for (int i = threadIdx.x; i < nwc; i += kThreads1)
-      any |= (cm[i] & (i == nwc - 1 ? low_bits(cn - 64 * (int64_t)i) : ~0ull)) != 0ull;
-    if (!__syncthreads_or(any)) {
-      if (te_full > tb) consume(xa);
+    int any = 0, notall = cn % 64 != 0;  // a ragged chunk keeps its mask loads
+    for (int i = threadIdx.x; i < nwc; i += kThreads1) {
+      const uint64_t m = cm[i] & (i == nwc - 1 ? low_bits(cn - 64 * (int64_t)i) : ~0ull);
+      any |= m != 0ull;
+      notall |= m != ~0ull;
+    }
+    chunk_any = __syncthreads_or(any);
+    chunk_all = !__syncthreads_or(notall);
+  }
+
+  // A chunk with no eligible element: both planes are zero and nothing more
+  // is read (mask bits past the bucket's end do not count).
+  if (!chunk_any) {
+    if (te_full > tb) consume(xa);
+    {
+      const int64_t cn = ((te * tile < nbe) ? te * tile : nbe) - tb * tile;
+      const int nwc = cn > 0 ? (int)((cn + 63) / 64) : 0;
       const int64_t gz = (base + tb * tile) / 64;
       for (int i = threadIdx.x; i < a.W * nwc; i += kThreads1) {
         const int w = i / nwc;
@@ -136,6 +164,7 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
       return;
     }
   }
+  if (te_full > tb) issue_mask(tb, ma);
   int64_t t = tb;
   if (te_full > tb) {
     // Pairs of full tiles with the next one in flight, then the odd one.
