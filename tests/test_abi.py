@@ -140,6 +140,12 @@ def test_invalid_arguments_return_codes_without_launch():
     pol = nf.policy(format=nf.NF_FORMAT_TERNARY, tau=-1.0)
     assert lib.nf_route_bucket(fake, 640, 2, 640, fake, ctypes.byref(pol), fake, 10, None, fake, fake, fake,
                                ws, 1 << 24, None) == nf.NF_ERR_INVALID_ARG
+    # flat buffers: bucket_n > 0 and, when there are several buckets, a multiple of 64
+    pol = nf.policy()
+    assert lib.nf_route_buckets(fake, 640, 2, 640, 0, fake, ctypes.byref(pol), fake, 10, None, fake, fake, fake,
+                                ws, 1 << 24, None) == nf.NF_ERR_INVALID_ARG
+    assert lib.nf_route_buckets(fake, 640, 2, 640, 100, fake, ctypes.byref(pol), fake, 10, None, fake, fake, fake,
+                                ws, 1 << 24, None) == nf.NF_ERR_INVALID_ARG
     pol = nf.policy(format=nf.NF_FORMAT_TERNARY, tau=float("nan"))
     assert lib.nf_route_bucket(fake, 640, 2, 640, fake, ctypes.byref(pol), fake, 10, None, fake, fake, fake,
                                ws, 1 << 24, None) == nf.NF_ERR_INVALID_ARG

@@ -210,6 +210,25 @@ def _fault_cases():
     return cases
 
 
+@pytest.mark.parametrize("W", [3, 16, 64])
+def test_route_fp32_overflow(W):
+    """Finite inputs whose FP32 sums overflow: +Inf and -Inf at routed
+    positions (added in worker order, as the oracle does), NaN where
+    opposite overflows meet; the statistics stay finite in FP64."""
+    n = 70_001
+    g = _grads(W, n, 1200 + W)
+    m = _clean_mask(_mask("rand", n, 1201), n)
+    routed = np.flatnonzero(~H.mask_bool(m, n))
+    g[:, routed[:50]] = np.float32(3e38)
+    g[:, routed[50:100]] = np.float32(-3e38)
+    g[: W // 2 + 1, routed[100:150]] = np.float32(3e38)
+    g[W // 2 + 1:, routed[100:150]] = np.float32(-3e38)
+    for pol in (nf.policy(), nf.policy(fp32_op=nf.NF_FP32_MEAN), nf.policy(veto=1)):
+        run = H.Bucket(g, m, n)
+        res = run.route(pol)
+        H.check_route(res, g, m, n, pol, what=f"overflow W={W}")
+
+
 @pytest.mark.parametrize("case", list(_fault_cases().keys()))
 @pytest.mark.parametrize("force", [0, 1])
 def test_route_faults(case, force):
