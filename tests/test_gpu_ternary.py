@@ -161,6 +161,18 @@ def test_route_bucket_ternary(W, n, tau):
     assert route == nfo.ROUTE_L
 
 
+@pytest.mark.parametrize("W", [2, 16, 64])
+def test_route_ternary_everything_gated(W):
+    """A gate above every |g|: both planes empty, every eligible element
+    decodes from d = 0; routed elements keep their FP32 sums."""
+    n = 65_537
+    g, mask = layout(W, n, 21 * W)
+    pol = nf.policy(format=nf.NF_FORMAT_TERNARY, tau=1e30)
+    res = ternary_route(g, mask, n, pol)
+    assert check_ternary_bucket(res, g, mask, n, pol, 0, n, f"gated W={W}") == nfo.ROUTE_L
+    assert not res["bits"][:, :(n + 63) // 64].any(), "every plane word zero"
+
+
 def test_route_buckets_ternary_flat():
     W, n, bn = 16, 1_000_000, 131_072
     g, mask = layout(W, n, 99)
