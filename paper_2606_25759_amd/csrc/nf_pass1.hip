@@ -761,7 +761,11 @@ __global__ __launch_bounds__(256) void k_slotsum(DecideArgs a) {
   }
 }
 
-__global__ __launch_bounds__(256) void k_decide(DecideArgs a) {
+// 1024 threads: sixteen wavefronts take the workers in turn (at W = 64,
+// four each), so that fewer slot sums wait on each other.
+constexpr int kDecideThreads = 1024;
+
+__global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
   __shared__ nf_worker_stats st[256];
   __shared__ uint64_t ne_s;
   __shared__ int kfin_s;
@@ -778,7 +782,7 @@ __global__ __launch_bounds__(256) void k_decide(DecideArgs a) {
   const int used = (int)(two ? (chunks + a.gs - 1) / a.gs : chunks);
   // The slot loops are unrolled so that their loads are in flight together;
   // the adds keep their order.
-  for (int w = v; w < a.W; w += 4) {
+  for (int w = v; w < a.W; w += kDecideThreads / 64) {
     double s1 = 0.0, s2 = 0.0;
     uint64_t nf = 0;
 #pragma unroll 8
@@ -805,7 +809,7 @@ __global__ __launch_bounds__(256) void k_decide(DecideArgs a) {
     if (lane == 0) ne_s = s;
   }
   __syncthreads();
-  for (int w = threadIdx.x; w < a.W; w += 256) a.stats[(int64_t)b * a.W + w] = st[w];
+  for (int w = threadIdx.x; w < a.W; w += kDecideThreads) a.stats[(int64_t)b * a.W + w] = st[w];
   if (!a.dec) return;
   if (threadIdx.x == 0) {
     int k = 0;
@@ -815,7 +819,7 @@ __global__ __launch_bounds__(256) void k_decide(DecideArgs a) {
   }
   __syncthreads();
   const int kfin = kfin_s;
-  for (int w = threadIdx.x; w < a.W; w += 256)
+  for (int w = threadIdx.x; w < a.W; w += kDecideThreads)
     if (finite64(st[w].sum_sq) && ssq_rank(st, a.W, w) == (kfin - 1) / 2) med_s = st[w].sum_sq;
   __syncthreads();
   if (threadIdx.x == 0) {
@@ -884,7 +888,7 @@ hipError_t launch_decide(const Geometry& geo, const DecideArgs& a, hipStream_t s
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(k_decide, dim3((unsigned)geo.nb), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(k_decide, dim3((unsigned)geo.nb), dim3(kDecideThreads), 0, s, a);
   return hipGetLastError();
 }
 
