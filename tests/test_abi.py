@@ -250,3 +250,39 @@ def test_workspace_sizes():
     b = nf.nf_workspace_bytes_buckets(16, 6_553_600 * 201, 6_553_600)
     assert b == 30_873_600 + 643_328
     assert nf.nf_workspace_bytes_buckets(16, 100, 0) == 0
+
+
+def declared_prototypes():
+    """name -> list of parameter declarations, from include/nf.h."""
+    src = open(os.path.join(ROOT, "include", "nf.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", "", src)
+    out = {}
+    for m in re.finditer(r"\b(nf_[a-z0-9_]+)\s*\(([^;{]*?)\)\s*;", src, flags=re.S):
+        params = [p.strip() for p in m.group(2).split(",")]
+        out[m.group(1)] = [] if params == ["void"] or params == [""] else params
+    return out
+
+
+def _ctype_class(param):
+    if "*" in param:
+        return "pointer"
+    for c, k in (("int64_t", "i64"), ("int32_t", "i32"), ("size_t", "size"), ("double", "f64"), ("float", "f32"),
+                 ("int", "i32")):
+        if re.search(rf"\b{c}\b", param):
+            return k
+    return "other"
+
+
+def test_binding_signatures_match_the_header():
+    lib = nf.load()
+    kinds = {ctypes.c_void_p: "pointer", ctypes.c_char_p: "pointer", ctypes.c_int64: "i64", ctypes.c_int32: "i32",
+             ctypes.c_size_t: "size", ctypes.c_double: "f64", ctypes.c_float: "f32"}
+    protos = declared_prototypes()
+    assert sorted(protos) == declared_functions()
+    for name, params in protos.items():
+        args = getattr(lib, name).argtypes or []
+        assert len(args) == len(params), f"{name}: {len(args)} ctypes arguments, {len(params)} declared"
+        for a, p in zip(args, params):
+            k = kinds.get(a, "pointer" if issubclass(a, (ctypes._Pointer, ctypes.Structure)) else "other")
+            assert k == _ctype_class(p), f"{name}: {p!r} bound as {a}"
