@@ -563,6 +563,8 @@ def main():
                "sample_parity": "ok" if ok else "MISMATCH"}
         print(f"[bench] oracle: {cpu['value']} GB/s over {k} buckets ({t_cpu:.1f} s)", file=sys.stderr, flush=True)
 
+    # HBM bytes per pass-1 launch from the committed counters (null unless taken on this kernel source)
+    traffic = counter_traffic(lay.name) if not ternary else None
     rec = {
         "metric": "reducer FP32-equiv input GB/s (pack+signcount+fp32) and % of HBM peak",
         "value": round(value, 2),
@@ -585,7 +587,8 @@ def main():
         "device_ms": {"mean": round(device_ms, 4), "median": round(dev_med, 4), "min": round(dev_min, 4)},
         "roofline": {"kernel": "k_pass1", "bound": "hbm", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": counter_traffic(lay.name),
+                     "traffic": traffic,
+                     "traffic_gbs": None if traffic is None else round(traffic / (pass1_ms / launches) / 1e6, 1),
                      "launches_per_step": launches,
                      "algorithmic_bytes_per_launch": round(pass1_bytes / launches),
                      "avg_launch_ms": round(pass1_ms / launches, 5)},
