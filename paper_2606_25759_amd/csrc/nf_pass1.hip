@@ -165,8 +165,9 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
   // the registers).  Lane l of wavefront v keeps the running FP32 sum of
   // element 64s + l for each of its steps s = v, v + 16, ... in a register
   // from one group to the next, so the workers are still added in order.
-  // After each group the wavefronts' sums of squares are added in wavefront
-  // order, through LDS, into the group's partials.
+  // Each wavefront leaves its per-worker sums of squares in LDS; after the
+  // last group, one barrier, and each worker's are added in wavefront order
+  // (one barrier per group took 0.19 ms more on a 64-worker bucket).
   if constexpr (WPW > 1) {
     if (chunk_routed) {
       constexpr int GW = WPW <= 2 ? 8 : 16;  // workers per group
@@ -174,7 +175,7 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
       const int64_t c0 = base + tb * tile;
       const int nsteps = (int)((te - tb) * (tile / 64));
       const int64_t slot = (int64_t)b * a.slots + c;
-      Partial* red = reinterpret_cast<Partial*>(smem);  // [kWaves][GW]
+      Partial* red = reinterpret_cast<Partial*>(smem);  // [kWaves][W]
       float run[MS];
 #pragma unroll
       for (int i = 0; i < MS; ++i) run[i] = 0.0f;
@@ -215,25 +216,24 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
 #pragma unroll
         for (int w = 0; w < GW; ++w) {
           const double s2 = wave_sum(q2[w]);
-          if (lane == 0) {
+          if (lane == 0 && w0 + w < a.W) {
             Partial p;
             p.sabs = 0.0;
             p.ssq = s2;
             p.nonfinite = nf2[w];
-            red[v * GW + w] = p;
+            red[v * a.W + w0 + w] = p;
           }
         }
-        __syncthreads();
-        if ((int)threadIdx.x < GW && w0 + (int)threadIdx.x < a.W) {
-          const int w = threadIdx.x;
-          Partial p = red[w];
-          for (int v2 = 1; v2 < kWaves; ++v2) {
-            p.ssq += red[v2 * GW + w].ssq;
-            p.nonfinite += red[v2 * GW + w].nonfinite;
-          }
-          part[slot * a.W + w0 + w] = p;
+      }
+      // one barrier for the chunk: each worker's wavefront partials in order
+      __syncthreads();
+      for (int w = threadIdx.x; w < a.W; w += kThreads1) {
+        Partial p = red[w];
+        for (int v2 = 1; v2 < kWaves; ++v2) {
+          p.ssq += red[v2 * a.W + w].ssq;
+          p.nonfinite += red[v2 * a.W + w].nonfinite;
         }
-        __syncthreads();  // red is reused by the next group
+        part[slot * a.W + w] = p;
       }
 #pragma unroll
       for (int i = 0; i < MS; ++i) {
@@ -838,7 +838,10 @@ static hipError_t pass1_dispatch(const Geometry& geo, const Pass1Args& a, hipStr
   size_t smem = PACK ? (size_t)geo.W * cw * sizeof(uint64_t) : 0;
   if (a.sums != kSumsNone) smem += (size_t)geo.W * geo.tile * sizeof(float);
   smem += (size_t)geo.G * geo.eg * pass1_words(geo.wpw) * sizeof(uint64_t);  // mask words of a mixed chunk
-  const size_t red = (size_t)geo.eg * geo.W * sizeof(Partial) + (size_t)geo.eg * sizeof(uint64_t);
+  size_t red = (size_t)geo.eg * geo.W * sizeof(Partial) + (size_t)geo.eg * sizeof(uint64_t);
+  // routed chunks with several workers per wavefront: [kWaves][W] partials
+  if (geo.wpw > 1 && a.sums != kSumsNone && red < (size_t)kWaves * geo.W * sizeof(Partial))
+    red = (size_t)kWaves * geo.W * sizeof(Partial);
   if (smem < red) smem = red;
   if (smem > 65536) {
     // Above 64 KiB of dynamic LDS the kernel must opt in (gfx950 has 160 KiB per CU).
