@@ -191,6 +191,18 @@ def decode_table(W, mode=DECODE_SOFT, lib=None):
     return q
 
 
+def output(mask, n, counts, y, q, scale, route, lib=None):
+    """Step 10 on its own: decoded values at mask = 1 under route L, the FP32
+    path elsewhere (and everywhere under F and P)."""
+    lib = lib or load()
+    out = np.zeros(max(n, 1), dtype=np.float32)
+    m = np.ascontiguousarray(mask, np.uint64)
+    lib.nfo_output(_ptr(m if m.size else np.zeros(1, np.uint64)), n, _ptr(np.ascontiguousarray(counts, np.uint8)),
+                   _ptr(np.ascontiguousarray(y, np.float32)), _ptr(np.ascontiguousarray(q, np.float32)),
+                   ctypes.c_float(scale), route, _ptr(out))
+    return out[:n]
+
+
 def reduce_bucket(g, mask, pol=None, lib=None):
     """Whole bucket.  Returns dict(bits, counts, out, stats, decision)."""
     lib = lib or load()
@@ -246,6 +258,19 @@ def ternary_decode_table(W, mode=DECODE_SOFT, lib=None):
     q = np.zeros(2 * W + 1, dtype=np.float32)
     lib.nfo_ternary_decode_table(W, mode, _ptr(q))
     return q
+
+
+def ternary_output(mask, n, cpos, cneg, y, q, scale, W, route, lib=None):
+    """The G-Ternary output step on its own (R20): fl32(scale * q[c+ - c-])
+    at mask = 1 under route L, the FP32 path elsewhere."""
+    lib = lib or load()
+    out = np.zeros(max(n, 1), dtype=np.float32)
+    m = np.ascontiguousarray(mask, np.uint64)
+    lib.nfo_ternary_output(_ptr(m if m.size else np.zeros(1, np.uint64)), n,
+                           _ptr(np.ascontiguousarray(cpos, np.uint8)), _ptr(np.ascontiguousarray(cneg, np.uint8)),
+                           _ptr(np.ascontiguousarray(y, np.float32)), _ptr(np.ascontiguousarray(q, np.float32)),
+                           ctypes.c_float(scale), W, route, _ptr(out))
+    return out[:n]
 
 
 def reduce_bucket_ternary(g, mask, pol, lib=None):

@@ -12,8 +12,20 @@ import torch
 
 import oracle as nfo
 import paper_2606_25759_amd as nf
+import synth
 
 REL_TOL = 1e-6
+POOL = 16  # host threads for oracle work: the CPU share of one GPU on the test box
+
+
+def oracle_masks(lay):
+    """(the mask the GPU reads, from the library's host builder; the oracle's
+    own mask from the same segments), checked equal word for word."""
+    segs = synth.mask_segments(lay)
+    m_dev = nf.nf_mask_from_segments(*segs, lay.n_total)
+    m_o = nfo.mask_from_segments(*segs, lay.n_total)
+    assert np.array_equal(m_dev, m_o), f"{lay.name}: mask builders disagree"
+    return m_dev, m_o
 
 
 def dev():

@@ -108,8 +108,10 @@ def ternary_route(g, mask, n, pol, bucket_n=None):
                 stats=nf.stats_host(stats, W, nb), dec=nf.decisions_host(dec, nb))
 
 
-def check_ternary_bucket(res, g, mask, n, pol, b, bucket_n, tag):
-    """Every output of bucket b against the oracle's ternary whole bucket."""
+def check_ternary_bucket(res, g, mask, n, pol, b, bucket_n, tag, thresholds_agree=False):
+    """Every output of bucket b against the oracle's ternary whole bucket.
+    With thresholds_agree, the two sides' thresholds must be equal bit for
+    bit (then the planes are compared bit for bit everywhere)."""
     W = g.shape[0]
     a, e = b * bucket_n, min((b + 1) * bucket_n, n)
     ka, ke = a // 64, (e + 63) // 64
@@ -128,6 +130,8 @@ def check_ternary_bucket(res, g, mask, n, pol, b, bucket_n, tag):
     th_ref = np.array([nfo.ternary_threshold(ref["stats"][w], ne, pol.tau) for w in range(W)], np.float32)
     pos, neg = res["bits"][:W, ka:ke], res["bits"][W:2 * W, ka:ke]
     same_th = np.array_equal(th_gpu.view(np.uint32), th_ref.view(np.uint32))
+    assert same_th or not thresholds_agree, \
+        f"{tag} thresholds differ for workers {np.nonzero(th_gpu.view(np.uint32) != th_ref.view(np.uint32))[0]}"
     if same_th:
         assert np.array_equal(pos, ref["pos"]) and np.array_equal(neg, ref["neg"]), f"{tag} planes"
         assert np.array_equal(res["counts"][a:e], ref["cpos"]), f"{tag} c+"
