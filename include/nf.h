@@ -423,6 +423,28 @@ nf_status nf_route_buckets(const float* grads, int64_t worker_stride, int32_t W,
                            nf_worker_stats* stats, nf_route_decision* decisions, void* ws,
                            size_t ws_bytes, void* stream);
 
+/*
+ * nf_route_buckets without a workspace, for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc.  Same arguments (less ws and ws_bytes), semantics
+ * and results as nf_route_buckets.  The partial statistics go to a static
+ * device array of NF_STATIC_SCRATCH_BYTES that the library holds on every
+ * GPU it runs on until the process ends; the call allocates nothing.  A size
+ * whose workspace (nf_workspace_bytes_buckets) exceeds that array returns
+ * NF_ERR_WORKSPACE before anything is launched (64 MiB covers, e.g., 201
+ * buckets of 16 x 6,553,600 elements, or one bucket of 64 x 100M).  Every
+ * call on one GPU uses that GPU's one array, whose contents the next call
+ * overwrites: calls that may overlap in time on one GPU (other streams or
+ * threads without ordering between them) race, and must not be made.
+ */
+#define NF_STATIC_SCRATCH_BYTES (64ull << 20)
+nf_status nf_route_buckets_noalloc(const float* grads, int64_t worker_stride, int32_t W,
+                                   int64_t n_total, int64_t bucket_n, const uint64_t* mask,
+                                   const nf_route_policy* policy_host, uint64_t* bits,
+                                   int64_t bits_stride_words, uint8_t* counts, float* out,
+                                   nf_worker_stats* stats, nf_route_decision* decisions,
+                                   void* stream);
+
 /* ------------------------------------------------------------------------
  * Controller inputs on the host (§4.3 Supervisor recovery, §4.4 online
  * control, §6.4 endpoint-capacity guard).  These functions produce the

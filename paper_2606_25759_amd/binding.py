@@ -32,6 +32,7 @@ NF_FORMAT_BINARY, NF_FORMAT_TERNARY = 0, 1
 EXPORTS = ["nf_abi_version", "nf_last_error", "nf_mask_from_segments", "nf_workspace_bytes",
            "nf_bucket_health", "nf_pack_signs", "nf_fp32_reduce", "nf_signcount_reduce",
            "nf_route_decide", "nf_route_bucket", "nf_workspace_bytes_buckets", "nf_route_buckets",
+           "nf_route_buckets_noalloc",
            "nf_set_phase_events", "nf_pass1_launches", "nf_slice_scales_from_pass1", "nf_ternary_threshold", "nf_pack_ternary",
            "nf_ternary_reduce", "nf_partial_counts", "nf_partial_count_reduce", "nf_stock_signcount",
            "nf_supervisor_init", "nf_supervisor_policy", "nf_supervisor_update", "nf_endpoint_guard",
@@ -131,6 +132,8 @@ def load(path=None):
                                            _P, _SZ, _P]),
         "nf_route_buckets": (ctypes.c_int, [_P, _I64, _I32, _I64, _I64, _P, _P, _P, _I64, _P, _P,
                                             _P, _P, _P, _SZ, _P]),
+        "nf_route_buckets_noalloc": (ctypes.c_int, [_P, _I64, _I32, _I64, _I64, _P, _P, _P, _I64, _P,
+                                                    _P, _P, _P, _P]),
         "nf_set_phase_events": (ctypes.c_int, [_P, _P, _P, _P]),
         "nf_slice_scales_from_pass1": (_I32, [_P, _I64, _I32, _I64, _P, _P, _I64, _P, _P, _P, _SZ, _P]),
         "nf_pass1_launches": (_I64, [_I32, _I64, _I64, _I32]),
@@ -479,6 +482,22 @@ def nf_route_buckets(grads, n_total, bucket_n, mask, pol, bits, counts, out, sta
                                    _dev_ptr(stats, torch.uint8, "stats"),
                                    _dev_ptr(decisions, torch.uint8, "decisions"),
                                    _dev_ptr(ws, torch.uint8, "ws"), ws.numel(), _stream(stream)))
+
+
+NF_STATIC_SCRATCH_BYTES = 64 << 20
+
+
+def nf_route_buckets_noalloc(grads, n_total, bucket_n, mask, pol, bits, counts, out, stats, decisions,
+                             stream=None):
+    """nf_route_buckets with the library's static device scratch instead of a
+    caller workspace (no allocation by the call)."""
+    g, stride, W = _rows(grads)
+    b, bstride = _bits_rows(bits)
+    _check(load().nf_route_buckets_noalloc(g, stride, W, n_total, bucket_n, _words(mask), ctypes.byref(pol),
+                                           b, bstride, _dev_ptr(counts, torch.uint8, "counts"),
+                                           _dev_ptr(out, torch.float32, "out"),
+                                           _dev_ptr(stats, torch.uint8, "stats"),
+                                           _dev_ptr(decisions, torch.uint8, "decisions"), _stream(stream)))
 
 
 def nf_set_phase_events(before_pass1=None, after_pass1=None, after_decide=None, after_pass2=None):

@@ -4,11 +4,24 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
 #include <string>
 
 #include "nf_internal.h"
 
 namespace {
+
+// Device scratch of the allocation-free driver (nf_route_buckets_noalloc):
+// the partial-statistics workspace of one call, in a file-scope array that
+// every GPU running the library holds until the process ends.  In host code
+// the array's name stands for a host-side shadow, never a device address:
+// each device's address comes from hipGetSymbolAddress, taken once per
+// device on the first call there, and only that address reaches a kernel.
+constexpr size_t kStaticScratchBytes = (size_t)NF_STATIC_SCRATCH_BYTES;
+__device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};
 
 thread_local std::string g_err;
 thread_local hipEvent_t g_phase_ev[4] = {nullptr, nullptr, nullptr, nullptr};
@@ -38,6 +51,26 @@ nf_status hip_fail(hipError_t e, const char* what) {
 }
 
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+// The current device's address of `scratch`, looked up on its first use.
+nf_status scratch_address(void** p) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(NF_ERR_UNSUPPORTED, "device %d: the static scratch is tracked for devices 0..%d", dev,
+                kMaxDevices - 1);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* a = nullptr;
+    e = hipGetSymbolAddress(&a, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!a) return fail(NF_ERR_HIP, "hipGetSymbolAddress(scratch) gave a null address");
+    g_scratch_dev[dev] = a;
+  }
+  *p = g_scratch_dev[dev];
+  return NF_OK;
+}
 
 // Checks shared by every entry point that reads gradient rows.
 nf_status check_grads(const float* g, int64_t stride, int32_t W, int64_t n) {
@@ -815,6 +848,27 @@ nf_status nf_route_buckets(const float* grads, int64_t worker_stride, int32_t W,
     return fail(NF_ERR_INVALID_ARG, "bucket_n=%lld must be a multiple of 64", (long long)bucket_n);
   return route_flat(grads, worker_stride, W, n_total, bucket_n, mask, policy_host, bits,
                     bits_stride_words, counts, out, stats, decisions, ws, ws_bytes, stream);
+}
+
+nf_status nf_route_buckets_noalloc(const float* grads, int64_t worker_stride, int32_t W,
+                                   int64_t n_total, int64_t bucket_n, const uint64_t* mask,
+                                   const nf_route_policy* policy_host, uint64_t* bits,
+                                   int64_t bits_stride_words, uint8_t* counts, float* out,
+                                   nf_worker_stats* stats, nf_route_decision* decisions,
+                                   void* stream) {
+  if (bucket_n <= 0) return fail(NF_ERR_INVALID_ARG, "bucket_n must be > 0");
+  if (bucket_n < n_total && bucket_n % 64)
+    return fail(NF_ERR_INVALID_ARG, "bucket_n=%lld must be a multiple of 64", (long long)bucket_n);
+  if (W < 1 || W > 255) return fail(NF_ERR_INVALID_ARG, "W=%d outside [1, 255]", W);
+  if (n_total < 0) return fail(NF_ERR_INVALID_ARG, "n_total < 0");
+  const size_t need = nf::workspace_layout(nf::make_geometry(W, n_total, bucket_n)).total;
+  if (need > kStaticScratchBytes)
+    return fail(NF_ERR_WORKSPACE, "W=%d, n_total=%lld, bucket_n=%lld needs %zu bytes of scratch, above the "
+                "static %zu", W, (long long)n_total, (long long)bucket_n, need, kStaticScratchBytes);
+  void* ws = nullptr;
+  NF_TRY(scratch_address(&ws));
+  return route_flat(grads, worker_stride, W, n_total, bucket_n, mask, policy_host, bits,
+                    bits_stride_words, counts, out, stats, decisions, ws, kStaticScratchBytes, stream);
 }
 
 }  // extern "C"

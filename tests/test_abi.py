@@ -123,6 +123,16 @@ def test_invalid_arguments_return_codes_without_launch():
     assert lib.nf_fp32_reduce(fake, 64, 2, 64, fake, 0, 9, fake, None) == nf.NF_ERR_INVALID_ARG
     # bits stride too small
     assert lib.nf_pack_signs(fake, 640, 2, 640, fake, fake, 9, None, ws, 1 << 20, None) == nf.NF_ERR_INVALID_ARG
+    # the allocation-free driver: sizes beyond its static scratch, bad sizes, before any launch
+    big = 100_000_000
+    assert nf.nf_workspace_bytes(255, big) > nf.NF_STATIC_SCRATCH_BYTES
+    assert lib.nf_route_buckets_noalloc(fake, big, 255, big, big, fake, None, fake, big, None, fake, fake, fake,
+                                        None) == nf.NF_ERR_WORKSPACE
+    assert "static" in nf.nf_last_error()
+    assert lib.nf_route_buckets_noalloc(fake, 640, 0, 640, 640, fake, None, fake, 10, None, fake, fake, fake,
+                                        None) == nf.NF_ERR_INVALID_ARG
+    assert lib.nf_route_buckets_noalloc(fake, 640, 2, 640, 100, fake, None, fake, 10, None, fake, fake, fake,
+                                        None) == nf.NF_ERR_INVALID_ARG
     # workspace too small
     need = nf.nf_workspace_bytes(2, 640)
     assert need > 0
