@@ -41,8 +41,10 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="gpt1p3b",
-                    choices=["tiny", "resnet50", "vitb16", "gpt1p3b", "stress"])
+    ap.add_argument("--workload", default=None,
+                    choices=["tiny", "resnet50", "vitb16", "gpt1p3b", "stress"],
+                    help="measure this workload only (default: the GPT-1.3B-scale headline, then a few "
+                         "steps of every other workload in the JSON line's `configs`)")
     ap.add_argument("--force-lowbit", action="store_true", help="guard disabled (forced low-bit)")
     ap.add_argument("--no-counts", action="store_true", help="do not write the uint8 counts")
     ap.add_argument("--cold", action="store_true",
@@ -99,6 +101,17 @@ def kernel_source_sha():
     h = hashlib.sha256()
     for name in ("nf_pass1.hip", "nf_device.h", "nf_internal.h"):
         h.update(open(os.path.join(ROOT, "paper_2606_25759_amd", "csrc", name), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def all_kernels_sha():
+    """Hash of every kernel source of the library and the geometry header."""
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2606_25759_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        if name.endswith((".hip", ".h")):
+            h.update(name.encode())
+            h.update(open(os.path.join(csrc, name), "rb").read())
     return h.hexdigest()[:16]
 
 
@@ -370,7 +383,6 @@ def split_one_bucket(nf, torch, grads, mask, W, n, n_e, reps=10):
     (the first), with the algorithmic bytes each one moves."""
     dev = grads.device
     nw = (n + 63) // 64
-    n_f = n - n_e
     g0, m0 = grads[:, :n], mask[:nw]
     bits = torch.empty((W, nw), dtype=torch.int64, device=dev)
     counts = torch.empty(n, dtype=torch.uint8, device=dev)
@@ -381,8 +393,9 @@ def split_one_bucket(nf, torch, grads, mask, W, n, n_e, reps=10):
     calls = {
         "nf_bucket_health": (lambda: nf.nf_bucket_health(g0, n, m0, stats, ws), 4 * W * n + 8 * nw),
         "nf_pack_signs": (lambda: nf.nf_pack_signs(g0, n, m0, bits, stats, ws), 4 * W * n + 8 * nw + 8 * W * nw),
-        "nf_fp32_reduce": (lambda: nf.nf_fp32_reduce(g0, n, m0, nf.NF_SEL_ROUTED, nf.NF_FP32_SUM, out),
-                           4 * W * n_f + 8 * nw + 4 * n_f),
+        # the FP32 path at every position (route F/P's full-precision sum of the bucket)
+        "nf_fp32_reduce": (lambda: nf.nf_fp32_reduce(g0, n, m0, nf.NF_SEL_ALL, nf.NF_FP32_SUM, out),
+                           4 * W * n + 8 * nw + 4 * n),
         "nf_signcount_reduce": (lambda: nf.nf_signcount_reduce(bits, W, n, m0, scale, nf.NF_DECODE_SOFT, counts, out),
                                 8 * W * nw + 8 * nw + n + 4 * n_e),
     }
@@ -399,6 +412,247 @@ def split_one_bucket(nf, torch, grads, mask, W, n, n_e, reps=10):
         ms = e0.elapsed_time(e1) / reps
         res[name] = {"ms": round(ms, 4), "algorithmic_gbs": round(nbytes / ms / 1e6, 1)}
     return res
+
+
+class Workload:
+    """One workload's device buffers, generated once, and measurements of
+    nf_route_buckets over all of its buckets under a given policy."""
+
+    def __init__(self, nf, torch, name, planes=1):
+        import numpy as np
+        import synth
+        self.nf, self.torch, self.np = nf, torch, np
+        self.dev = torch.device("cuda:0")
+        self.lay = lay = synth.CONFIGS[name]()
+        self.W, self.n, self.bn, self.nb = lay.W, lay.n_total, lay.bucket_n, lay.nb
+        W, n, nb = self.W, self.n, self.nb
+        self.nw = (n + 63) // 64
+        print(f"[bench] {lay.name}: W={W} n={n:,} buckets={nb} bucket_n={self.bn:,} "
+              f"input={lay.input_bytes() / 1e9:.2f} GB", file=sys.stderr, flush=True)
+        self.grads = torch.empty((W, lay.stride), dtype=torch.float32, device=self.dev)
+        synth.generate_device(lay, self.grads)
+        self.segs = synth.mask_segments(lay)
+        self.mask_h = nf.nf_mask_from_segments(*self.segs, n)
+        self.mask = torch.from_numpy(self.mask_h.view(np.int64)).to(self.dev)
+        self.planes = planes  # 2: room for G-Ternary's positive and negative planes
+        self.bits = torch.empty((planes * W, self.nw), dtype=torch.int64, device=self.dev)
+        self.counts = torch.empty(planes * n, dtype=torch.uint8, device=self.dev)
+        self.out = torch.empty(n, dtype=torch.float32, device=self.dev)
+        self.stats = torch.empty(nb * W * nf.STATS_BYTES, dtype=torch.uint8, device=self.dev)
+        self.dec = torch.empty(nb * nf.DECISION_BYTES, dtype=torch.uint8, device=self.dev)
+        self.ws = nf.empty_workspace(nf.nf_workspace_bytes_buckets(W, n, self.bn), self.dev)
+        torch.cuda.synchronize()
+        print("[bench] inputs resident", file=sys.stderr, flush=True)
+
+    def release(self):
+        del self.grads, self.mask, self.bits, self.counts, self.out, self.stats, self.dec, self.ws
+        self.torch.cuda.synchronize()
+        self.torch.cuda.empty_cache()
+
+    def step(self, pol, counts=True):
+        ternary = pol.format == self.nf.NF_FORMAT_TERNARY
+        cnt = self.counts[: (2 if ternary else 1) * self.n] if counts else None
+        self.nf.nf_route_buckets(self.grads, self.n, self.bn, self.mask, pol, self.bits, cnt, self.out,
+                                 self.stats, self.dec, self.ws)
+
+    def measure(self, pol, steps, warmup, cold=False, counts=True):
+        """Wall and device time of `steps` steps; algorithmic bytes and rates per phase."""
+        nf, torch, np = self.nf, self.torch, self.np
+        W, n, bn, nb = self.W, self.n, self.bn, self.nb
+        ternary = pol.format == nf.NF_FORMAT_TERNARY
+        for _ in range(warmup):
+            self.step(pol, counts)
+        torch.cuda.synchronize()
+        hip = HipEvents()
+        evs = [[hip.create() for _ in range(4)] for _ in range(steps)]
+        scrub = torch.zeros(1 << 28, dtype=torch.float32, device=self.dev) if cold else None
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for k in range(steps):
+            if scrub is not None:
+                scrub.add_(1.0)
+            nf.nf_set_phase_events(*evs[k])
+            self.step(pol, counts)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        nf.nf_set_phase_events()
+        del scrub
+        ms_per_step = (t1 - t0) * 1e3 / steps
+        ph = np.array([[hip.elapsed_ms(e[0], e[1]), hip.elapsed_ms(e[1], e[2]), hip.elapsed_ms(e[2], e[3]),
+                        hip.elapsed_ms(e[0], e[3])] for e in evs])
+        for e in evs:
+            for x in e:
+                hip.destroy(x)
+        pass1_ms, decide_ms, pass2_ms, device_ms = (float(v) for v in ph.mean(axis=0))
+        dev_med, dev_min = float(np.median(ph[:, 3])), float(ph[:, 3].min())
+        d = nf.decisions_host(self.dec, nb)
+        routes = {"L": int((d["route"] == 0).sum()), "F": int((d["route"] == 1).sum()),
+                  "P": int((d["route"] == 2).sum())}
+        nbs = np.array([min(bn, n - b * bn) for b in range(nb)], dtype=np.int64)
+        ne = d["n_eligible"].astype(np.int64)
+        nwb = (nbs + 63) // 64
+        # pass 1: gradients once, mask once, sign words out (G-Binary only), FP32 sums at routed positions out
+        pass1_bytes = float((4 * W * nbs + 8 * nwb + (0 if ternary else 8 * W * nwb) + 4 * (nbs - ne)).sum())
+        is_l, is_f = d["route"] == 0, d["route"] == 1
+        cbytes = (2 if ternary else 1) * nbs if counts else 0
+        if ternary:
+            # second read of the eligible elements, two planes out and back in, mask, counts, decode
+            l_bytes = 4 * W * ne + 8 * nwb + 16 * W * nwb + 16 * W * nwb + 8 * nwb + cbytes + 4 * ne
+        else:
+            l_bytes = 8 * W * nwb + 8 * nwb + cbytes + 4 * ne
+        pass2_bytes = float((l_bytes * is_l).sum() + ((4 * W * ne + 8 * nwb + 4 * ne) * is_f).sum())
+        launches = nf.nf_pass1_launches(W, n, bn, sign_words=not ternary)
+        # a cold run's wall clock includes the overwrites: its value comes from the device events
+        value = self.lay.input_bytes() / ((device_ms if cold else ms_per_step) * 1e-3) / 1e9
+        achieved = pass1_bytes / (pass1_ms * 1e-3) / 1e9
+        print(f"[bench] {self.lay.name} {'ternary' if ternary else 'binary'}"
+              f"{' forced' if pol.force_lowbit else ''}{' cold' if cold else ''}: {steps} steps, "
+              f"{ms_per_step:.4f} ms/step wall, device {device_ms:.4f} (pass1 {pass1_ms:.4f}, decide "
+              f"{decide_ms:.4f}, pass2 {pass2_ms:.4f}), {value:.1f} GB/s", file=sys.stderr, flush=True)
+        return {
+            "steps": steps, "warmup": warmup, "ms_per_step": round(ms_per_step, 4),
+            "value": round(value, 2), "pct_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
+            "device_ms": {"mean": round(device_ms, 4), "median": round(dev_med, 4), "min": round(dev_min, 4)},
+            "phases_ms": {"pass1": round(pass1_ms, 4), "decide": round(decide_ms, 4),
+                          "pass2": round(pass2_ms, 4), "device_total": round(device_ms, 4),
+                          "pass2_algorithmic_gbs": round(pass2_bytes / max(pass2_ms, 1e-9) / 1e6, 1)},
+            "pass1": {"kernel": "k_pass1", "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "launches_per_step": launches,
+                      "algorithmic_bytes_per_launch": round(pass1_bytes / launches),
+                      "avg_launch_ms": round(pass1_ms / launches, 5)},
+            "routes": routes,
+            "mgtr": round(float(d["bytes_route"].sum() / d["bytes_fp32"].sum()), 4),
+            "eligible_frac": round(float(ne.sum()) / n, 4),
+        }
+
+    def cpu_baseline(self, pol, seconds):
+        """The oracle, single-threaded and pinned to one host core, on the first
+        buckets (or, for a one-bucket workload, a leading range) of the data the
+        GPU just reduced, with the oracle's own mask; its results are checked
+        against the GPU's on the sample."""
+        import oracle as nfo
+        nf, np = self.nf, self.np
+        W, n, bn, nb = self.W, self.n, self.bn, self.nb
+        ternary = pol.format == nf.NF_FORMAT_TERNARY
+        opol = nfo.policy(admitted=pol.admitted, veto=pol.veto, guard_ok=pol.guard_ok,
+                          force_lowbit=pol.force_lowbit, decode_mode=pol.decode_mode, fp32_op=pol.fp32_op,
+                          kappa=pol.kappa, format=pol.format, tau=pol.tau)
+        mask_o = nfo.mask_from_segments(*self.segs, n)
+        rate_guess = 0.55e9  # bytes per second of the single-threaded oracle
+        one_bucket = nb == 1 and n * 4 * W > rate_guess * seconds
+        if one_bucket:
+            # a leading 64-aligned range of the one bucket, reduced by the oracle as a bucket of its own:
+            # its decision is not the GPU's, so only the element-wise results are compared
+            span = max(64, int(rate_guess * seconds / (4 * W)) // 64 * 64)
+            ranges = [(0, min(span, n))]
+        else:
+            k = max(1, min(nb, int(rate_guess * seconds / (4 * W * min(bn, n)))))
+            ranges = [(b * bn, min((b + 1) * bn, n)) for b in range(k)]
+        model, ncpu = host_cpu()
+        old_aff = os.sched_getaffinity(0)
+        core = min(old_aff)
+        dh = nf.decisions_host(self.dec, nb)
+        sh = nf.stats_host(self.stats, W, nb)
+        # a sample far below a second of oracle work (the tiny bucket) is reduced several times over
+        reps = max(1, int(1.0 / (4 * W * sum(e - a for a, e in ranges) / rate_guess)))
+        t_cpu, nbytes, bad = 0.0, 0, []
+        try:
+            os.sched_setaffinity(0, {core})
+            for b, (a, e) in enumerate(ranges):
+                gh = self.grads[:, a:e].cpu().numpy()
+                mh = np.ascontiguousarray(mask_o[a // 64:(e + 63) // 64])
+                c0 = time.perf_counter()
+                for _ in range(reps):
+                    ref = (nfo.reduce_bucket_ternary if ternary else nfo.reduce_bucket)(gh, mh, opol)
+                t_cpu += time.perf_counter() - c0
+                nbytes += reps * 4 * W * (e - a)
+                bad += sample_mismatches(nf, np, self, ref, b, a, e, mh, ternary, whole_bucket=not one_bucket)
+        finally:
+            os.sched_setaffinity(0, old_aff)
+        what = (f"elements 0..{ranges[0][1] - 1} of the one bucket, reduced as a bucket of their own"
+                if one_bucket else f"buckets 0..{len(ranges) - 1} ({len(ranges)} x {min(bn, n):,} elements)")
+        if reps > 1:
+            what += f", reduced {reps} times"
+        rec = {"value": round(nbytes / t_cpu / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+               "sample": f"{self.lay.name} {what} x {W} workers, single-threaded C++ oracle pinned to core "
+                         f"{core} of {ncpu} ({model}), {t_cpu:.1f} s",
+               "sample_parity": "ok" if not bad else "MISMATCH: " + "; ".join(bad[:4]),
+               "sample_parity_checks": (("FP32 values (the planes' thresholds need the whole bucket)" if ternary
+                                         else "bits, counts, FP32 values") if one_bucket else
+                                        ("planes" if ternary else "bits") +
+                                        ", counts, outputs, statistics, route, reasons, n_E, modeled bytes")}
+        print(f"[bench] oracle on {self.lay.name}: {rec['value']} GB/s ({t_cpu:.1f} s), sample parity "
+              f"{rec['sample_parity']}", file=sys.stderr, flush=True)
+        return rec
+
+
+def sample_mismatches(nf, np, wl, ref, b, a, e, mh, ternary, whole_bucket):
+    """What differs between the GPU's results and the oracle's on elements
+    [a, e) (bucket b when whole_bucket).  Bars as in the parity tests: bit-exact
+    integers, FP32 sums and modeled bytes; statistics, scale and decoded values
+    within 1e-6 relative."""
+    W, n = wl.W, wl.n
+    bad = []
+    m = np.unpackbits(mh.view(np.uint8), bitorder="little")[: e - a].astype(bool)
+    got_bits = wl.bits[: (2 if ternary else 1) * W, a // 64:(e + 63) // 64].cpu().numpy().view(np.uint64)
+    out = wl.out[a:e].cpu().numpy()
+
+    def close(x, y, tol=1e-6):
+        x, y = np.asarray(x, np.float64), np.asarray(y, np.float64)
+        same = (x == y) | (np.isnan(x) & np.isnan(y))
+        with np.errstate(invalid="ignore"):
+            return bool(np.all(same | (np.abs(x - y) <= tol * np.abs(y))))
+
+    def same32(x, y):
+        x, y = np.asarray(x, np.float32), np.asarray(y, np.float32)
+        nx, ny = np.isnan(x), np.isnan(y)
+        return bool(np.array_equal(nx, ny) and np.array_equal(x[~nx].view(np.uint32), y[~ny].view(np.uint32)))
+
+    if whole_bucket:
+        d, rd, st = wl.nf.decisions_host(wl.dec, wl.nb)[b], ref["decision"], nf.stats_host(wl.stats, W, wl.nb)[b]
+        if (int(d["route"]), int(d["reasons"]), int(d["n_eligible"])) != (rd.route, rd.reasons, rd.n_eligible):
+            bad.append(f"bucket {b} decision")
+        if float(d["bytes_route"]) != rd.bytes_route or float(d["bytes_fp32"]) != rd.bytes_fp32:
+            bad.append(f"bucket {b} modeled bytes")
+        if not close(d["scale"], rd.scale):
+            bad.append(f"bucket {b} scale")
+        if not (np.array_equal(st["nonfinite"], ref["stats"]["nonfinite"]) and
+                close(st["sum_abs_elig"], ref["stats"]["sum_abs_elig"]) and close(st["sum_sq"], ref["stats"]["sum_sq"])):
+            bad.append(f"bucket {b} statistics")
+        route, scale = int(d["route"]), np.float32(d["scale"])
+    else:
+        route, scale = int(wl.nf.decisions_host(wl.dec, 1)[0]["route"]), None
+    if ternary:
+        # the planes' thresholds come from the whole bucket's statistics: a leading range reduced as a
+        # bucket of its own has other thresholds, so there only its FP32 values are compared
+        if whole_bucket and route == 0 and not (np.array_equal(got_bits[:W], ref["pos"]) and
+                                                np.array_equal(got_bits[W:], ref["neg"])):
+            bad.append(f"bucket {b} planes")
+    elif not np.array_equal(got_bits, ref["bits"]):
+        bad.append(f"range {b} bits")
+    if route == 0 and (whole_bucket or not ternary):
+        cnt = wl.counts[a:e].cpu().numpy()
+        want_c = ref["cpos"] if ternary else ref["counts"]
+        if not np.array_equal(cnt, want_c):
+            bad.append(f"range {b} counts")
+    if route != 0 or not whole_bucket:
+        # the FP32 path: every position off route L, the routed positions on it
+        sel = np.ones(e - a, bool) if route != 0 else ~m
+        if whole_bucket and not same32(out[sel], ref["out"][sel]):
+            bad.append(f"range {b} FP32 values")
+        if not whole_bucket:
+            import oracle as nfo
+            y = nfo.fp32_path(wl.grads[:, a:e].cpu().numpy(), 0)
+            if not same32(out[sel], y[sel]):
+                bad.append(f"range {b} FP32 values")
+    if ternary and not whole_bucket and route == 0:
+        return bad  # routed positions were compared above
+    if whole_bucket and route == 0:
+        if not same32(out[~m], ref["out"][~m]):
+            bad.append(f"bucket {b} routed values")
+        if not close(out[m], ref["out"][m]):
+            bad.append(f"bucket {b} decoded values")
+    return bad
 
 
 def main():
@@ -418,6 +672,8 @@ def main():
         return calibrate_copy()
     if args.contrast:
         return contrast()
+    if args.controller or args.sliced:
+        args.workload = args.workload or "gpt1p3b"
     if args.controller:
         return controller_run(args)
     if args.sliced:
@@ -426,183 +682,133 @@ def main():
     import paper_2606_25759_amd as nf
     import synth
 
-    dev = torch.device("cuda:0")
-    lay = synth.CONFIGS[args.workload]()
-    W, n, bn, nb = lay.W, lay.n_total, lay.bucket_n, lay.nb
-    nw = (n + 63) // 64
-    print(f"[bench] {lay.name}: W={W} n={n:,} buckets={nb} bucket_n={bn:,} "
-          f"input={lay.input_bytes() / 1e9:.2f} GB", file=sys.stderr, flush=True)
-
-    grads = torch.empty((W, lay.stride), dtype=torch.float32, device=dev)
-    synth.generate_device(lay, grads)
-    off, ln, el = synth.mask_segments(lay)
-    mask_h = nf.nf_mask_from_segments(off, ln, el, n)
-    mask = torch.from_numpy(mask_h.view(np.int64)).to(dev)
+    sweep = args.workload is None
+    name = args.workload or "gpt1p3b"
     ternary = args.format == "ternary"
-    planes = 2 if ternary else 1  # G-Ternary: positive and negative plane per worker
-    bits = torch.empty((planes * W, nw), dtype=torch.int64, device=dev)
-    counts = None if args.no_counts else torch.empty(planes * n, dtype=torch.uint8, device=dev)
-    out = torch.empty(n, dtype=torch.float32, device=dev)
-    stats = torch.empty(nb * W * nf.STATS_BYTES, dtype=torch.uint8, device=dev)
-    dec = torch.empty(nb * nf.DECISION_BYTES, dtype=torch.uint8, device=dev)
-    ws = nf.empty_workspace(nf.nf_workspace_bytes_buckets(W, n, bn), dev)
     pol = nf.policy(force_lowbit=int(args.force_lowbit), format=int(ternary), tau=args.tau)
-    launches = nf.nf_pass1_launches(W, n, bn, sign_words=not ternary)
-    torch.cuda.synchronize()
-    print("[bench] inputs resident", file=sys.stderr, flush=True)
+    # the headline workload, with room for the G-Ternary planes when the sweep measures them too
+    wl = Workload(nf, torch, name, planes=2 if (ternary or sweep) else 1)
+    m = wl.measure(pol, args.steps, args.warmup, cold=args.cold, counts=not args.no_counts)
 
-    def step():
-        nf.nf_route_buckets(grads, n, bn, mask, pol, bits, counts, out, stats, dec, ws)
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-
-    hip = HipEvents()
-    evs = [[hip.create() for _ in range(4)] for _ in range(args.steps)]
-    scrub = torch.zeros(1 << 28, dtype=torch.float32, device=dev) if args.cold else None
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for k in range(args.steps):
-        if scrub is not None:
-            scrub.add_(1.0)
-        nf.nf_set_phase_events(*evs[k])
-        step()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    nf.nf_set_phase_events()
-    ms_per_step = (t1 - t0) * 1e3 / args.steps
-    ph = np.array([[hip.elapsed_ms(e[0], e[1]), hip.elapsed_ms(e[1], e[2]), hip.elapsed_ms(e[2], e[3]),
-                    hip.elapsed_ms(e[0], e[3])] for e in evs])
-    for e in evs:
-        for x in e:
-            hip.destroy(x)
-    pass1_ms, decide_ms, pass2_ms, device_ms = (float(v) for v in ph.mean(axis=0))
-    dev_med, dev_min = float(np.median(ph[:, 3])), float(ph[:, 3].min())
-    print(f"[bench] {args.steps} steps: {ms_per_step:.3f} ms/step wall, device {device_ms:.3f} ms "
-          f"(median {dev_med:.3f}, min {dev_min:.3f}; pass1 {pass1_ms:.3f}, decide {decide_ms:.3f}, "
-          f"pass2 {pass2_ms:.3f})", file=sys.stderr, flush=True)
-
-    # decisions, routes and algorithmic bytes
-    d = nf.decisions_host(dec, nb)
-    routes = {"L": int((d["route"] == 0).sum()), "F": int((d["route"] == 1).sum()),
-              "P": int((d["route"] == 2).sum())}
-    mgtr = float(d["bytes_route"].sum() / d["bytes_fp32"].sum())
-    nbs = np.array([min(bn, n - b * bn) for b in range(nb)], dtype=np.int64)
-    ne = d["n_eligible"].astype(np.int64)
-    nwb = (nbs + 63) // 64
-    # pass 1: gradients once, mask once, sign words out (G-Binary only), FP32 sums at routed
-    # positions out
-    pass1_bytes = float((4 * W * nbs + 8 * nwb + (0 if ternary else 8 * W * nwb) + 4 * (nbs - ne)).sum())
-    is_l, is_f = d["route"] == 0, d["route"] == 1
-    cbytes = 0 if args.no_counts else planes * nbs
-    if ternary:
-        # second read of the eligible elements, two planes out and back in, counts, decode
-        l_bytes = 4 * W * ne + 8 * nwb + 16 * W * nwb + 16 * W * nwb + 8 * nwb + cbytes + 4 * ne
-    else:
-        l_bytes = 8 * W * nwb + 8 * nwb + cbytes + 4 * ne
-    pass2_bytes = float((l_bytes * is_l).sum() + ((4 * W * ne + 8 * nwb + 4 * ne) * is_f).sum())
-    # a cold run's wall clock includes the overwrites: its value comes from the device events
-    value = lay.input_bytes() / ((device_ms if args.cold else ms_per_step) * 1e-3) / 1e9
-    achieved = pass1_bytes / (pass1_ms * 1e-3) / 1e9
-
-    # per-function split: the standalone entry points on the first bucket
     split = None
     if not ternary and not args.no_split:
-        split = split_one_bucket(nf, torch, grads, mask, W, min(bn, n), int(d["n_eligible"][0]))
+        split = split_one_bucket(nf, torch, wl.grads, wl.mask, wl.W, min(wl.bn, wl.n),
+                                 int(nf.decisions_host(wl.dec, wl.nb)["n_eligible"][0]))
         print(f"[bench] standalone, first bucket: " + ", ".join(f"{k} {v['ms']:.3f} ms" for k, v in split.items()
                                                             if isinstance(v, dict)), file=sys.stderr, flush=True)
-
-    # reference: one plain streaming read of the same gradients
     achievable = None
     if not args.no_probe:
-        sink = torch.zeros(1024, dtype=torch.float32, device=dev)
-        synth.read_probe(grads, sink)
+        sink = torch.zeros(1024, dtype=torch.float32, device=wl.dev)
+        synth.read_probe(wl.grads, sink)
         torch.cuda.synchronize()
         a0 = time.perf_counter()
         for _ in range(3):
-            synth.read_probe(grads, sink)
+            synth.read_probe(wl.grads, sink)
         torch.cuda.synchronize()
         probe_ms = (time.perf_counter() - a0) * 1e3 / 3
-        achievable = round(4 * grads.numel() / (probe_ms * 1e-3) / 1e9, 1)
+        achievable = round(4 * wl.grads.numel() / (probe_ms * 1e-3) / 1e9, 1)
         print(f"[bench] streaming read of the input: {achievable} GB/s", file=sys.stderr, flush=True)
-
-    # CPU baseline: the oracle, single-threaded, pinned to one core, on the first buckets
-    cpu = None
-    if not args.no_cpu_baseline:
-        import oracle as nfo
-        # about 15 s of single-core oracle work at its ~0.55 GB/s
-        k = args.cpu_buckets or max(1, min(nb, int(8.4e9 / (4 * W * min(bn, n)))))
-        opol = nfo.policy(force_lowbit=int(args.force_lowbit), format=int(ternary), tau=args.tau)
-        model, ncpu = host_cpu()
-        old_aff = os.sched_getaffinity(0)
-        core = min(old_aff)
-        t_cpu, nbytes, ok = 0.0, 0, True
-        try:
-            os.sched_setaffinity(0, {core})
-            for b in range(k):
-                a, e = b * bn, min((b + 1) * bn, n)
-                gh = grads[:, a:e].contiguous().cpu().numpy()
-                mh = np.ascontiguousarray(mask_h[a // 64:(e + 63) // 64])
-                c0 = time.perf_counter()
-                ref = (nfo.reduce_bucket_ternary if ternary else nfo.reduce_bucket)(gh, mh, opol)
-                t_cpu += time.perf_counter() - c0
-                nbytes += 4 * W * (e - a)
-                rd = ref["decision"]
-                ok &= int(d["route"][b]) == rd.route and int(d["reasons"][b]) == rd.reasons
-                if rd.route == 0 or not ternary:  # G-Ternary planes are built on route L only
-                    got = bits[:, a // 64:(e + 63) // 64].cpu().numpy().view(np.uint64)
-                    want = np.concatenate([ref["pos"], ref["neg"]]) if ternary else ref["bits"]
-                    ok &= bool(np.array_equal(got, want))
-        finally:
-            os.sched_setaffinity(0, old_aff)
-        cpu = {"value": round(nbytes / t_cpu / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
-               "sample": f"{lay.name} buckets 0..{k - 1} ({k} x {min(bn, n):,} elements x {W} workers), "
-                         f"single-threaded C++ oracle pinned to core {core} of {ncpu} ({model}), "
-                         f"{t_cpu:.1f} s",
-               "sample_parity": "ok" if ok else "MISMATCH"}
-        print(f"[bench] oracle: {cpu['value']} GB/s over {k} buckets ({t_cpu:.1f} s)", file=sys.stderr, flush=True)
+    cpu = None if args.no_cpu_baseline else wl.cpu_baseline(pol, 10.0)
 
     # HBM bytes per pass-1 launch from the committed counters (null unless taken on this kernel source)
-    traffic = counter_traffic(lay.name) if not ternary else None
+    traffic = counter_traffic(name) if not ternary else None
+    roofline = dict(m["pass1"])
+    roofline["traffic"] = traffic
+    roofline["traffic_gbs"] = (None if traffic is None else
+                               round(traffic / (m["phases_ms"]["pass1"] / roofline["launches_per_step"]) / 1e6, 1))
     rec = {
         "metric": "reducer FP32-equiv input GB/s (pack+signcount+fp32) and % of HBM peak",
-        "value": round(value, 2),
+        "value": m["value"],
         "unit": "GB/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 4),
+        "ms_per_step": m["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "pct_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
-        "config": {"workload": lay.name, "W": W, "n_total": n, "buckets": nb, "bucket_n": bn,
-                   "eligible_frac": round(float(ne.sum()) / n, 4),
+        "pct_hbm_peak": m["pct_hbm_peak"],
+        "config": {"workload": wl.lay.name, "W": wl.W, "n_total": wl.n, "buckets": wl.nb, "bucket_n": wl.bn,
+                   "eligible_frac": m["eligible_frac"],
                    "policy": "forced low-bit" if args.force_lowbit else "admitted, guard ok",
                    "format": args.format, "counts_written": not args.no_counts,
                    "caches": "cold (1 GiB overwritten before each step)" if args.cold else "warm"},
-        "device_ms": {"mean": round(device_ms, 4), "median": round(dev_med, 4), "min": round(dev_min, 4)},
-        "roofline": {"kernel": "k_pass1", "bound": "hbm", "achieved": round(achieved, 1),
-                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": traffic,
-                     "traffic_gbs": None if traffic is None else round(traffic / (pass1_ms / launches) / 1e6, 1),
-                     "launches_per_step": launches,
-                     "algorithmic_bytes_per_launch": round(pass1_bytes / launches),
-                     "avg_launch_ms": round(pass1_ms / launches, 5)},
-        "phases_ms": {"pass1": round(pass1_ms, 4), "decide": round(decide_ms, 4),
-                      "pass2": round(pass2_ms, 4), "device_total": round(device_ms, 4),
-                      "pass2_algorithmic_gbs": round(pass2_bytes / max(pass2_ms, 1e-9) / 1e6, 1)},
+        "device_ms": m["device_ms"],
+        "roofline": roofline,
+        "phases_ms": m["phases_ms"],
         "achievable_read_gbs": achievable,
         "split_one_bucket": split,
-        "routes": routes,
-        "mgtr": round(mgtr, 4),
+        "routes": m["routes"],
+        "mgtr": m["mgtr"],
         "cpu_baseline": cpu,
     }
+    if sweep:
+        rec["configs"] = sweep_configs(nf, torch, wl, args)
+    else:
+        wl.release()
     print(json.dumps(rec), flush=True)
     return 0
+
+
+def config_record(wl, m, pol, cold, cpu, counters):
+    """One row of the per-workload list: rate, share of peak, the pass-1
+    roofline, the oracle's sample and the committed counter bytes."""
+    ternary = pol.format == 1
+    row = {"workload": wl.lay.name, "W": wl.W, "n_total": wl.n, "buckets": wl.nb, "bucket_n": wl.bn,
+           "format": "ternary" if ternary else "binary",
+           "policy": "forced low-bit" if pol.force_lowbit else "admitted, guard ok",
+           "caches": "cold (1 GiB overwritten before each step)" if cold else "warm",
+           "input_gb": round(wl.lay.input_bytes() / 1e9, 4)}
+    row.update({k: m[k] for k in ("value", "pct_hbm_peak", "ms_per_step", "steps", "device_ms", "phases_ms",
+                                  "routes", "mgtr")})
+    row["unit"] = "GB/s"
+    row["roofline_pass1"] = m["pass1"]
+    row["cpu_baseline"] = cpu
+    row["counter_bytes"] = counters
+    return row
+
+
+def committed_counters(workload, fmt):
+    """Counter-measured HBM bytes per dispatch of the step's kernels from the
+    committed rocprofv3 summaries of this workload, where the kernel source is
+    the one they were taken on; else None."""
+    path = os.path.join(ROOT, "profiles", f"counters_{workload}_{fmt}.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    if rec.get("kernel_sha") != all_kernels_sha():
+        return None
+    return rec.get("kernels")
+
+
+def sweep_configs(nf, torch, gpt, args):
+    """Every workload of the sweep after the headline: G-Ternary on the same
+    GPT-scale buffer, then ViT-B/16 scale, ResNet-50 scale, the tiny bucket
+    (warm and cold caches) and the stress bucket (route F, forced low-bit,
+    forced low-bit G-Ternary).  Each row is a few timed steps and a bounded
+    oracle sample."""
+    rows = []
+    tern = nf.policy(format=nf.NF_FORMAT_TERNARY, tau=args.tau)
+    m = gpt.measure(tern, 10, 2)
+    rows.append(config_record(gpt, m, tern, False, None if args.no_cpu_baseline else gpt.cpu_baseline(tern, 3.0),
+                              committed_counters(gpt.lay.name, "ternary")))
+    gpt.release()
+    plan = [("vitb16", [(nf.policy(), False, 20)]),
+            ("resnet50", [(nf.policy(), False, 50)]),
+            ("tiny", [(nf.policy(), False, 200), (nf.policy(), True, 50)]),
+            ("stress", [(nf.policy(), False, 10), (nf.policy(force_lowbit=1), False, 10),
+                        (nf.policy(force_lowbit=1, format=nf.NF_FORMAT_TERNARY, tau=args.tau), False, 10)])]
+    for name, runs in plan:
+        wl = Workload(nf, torch, name, planes=2 if any(p.format for p, _, _ in runs) else 1)
+        for pol, cold, steps in runs:
+            m = wl.measure(pol, steps, 3, cold=cold)
+            cpu = None if (args.no_cpu_baseline or cold) else wl.cpu_baseline(pol, 3.0)
+            fmt = "ternary" if pol.format else ("forced" if pol.force_lowbit else "binary")
+            rows.append(config_record(wl, m, pol, cold, cpu, committed_counters(name, fmt)))
+        wl.release()
+    return rows
 
 
 if __name__ == "__main__":
