@@ -58,7 +58,6 @@ def load(path=None):
         "nfo_mask_from_segments": (ctypes.c_int, [_P, _P, _P, _I64, _I64, _P]),
         "nfo_count_eligible": (_I64, [_P, _I64]),
         "nfo_health": (None, [_P, _I64, _I32, _I64, _P, _P]),
-        "nfo_health_acc": (None, [_P, _I64, _I32, _I64, _P, _P]),
         "nfo_scale": (ctypes.c_float, [_P, _I32, _I64]),
         "nfo_decide": (None, [_P, _I32, _I64, _I64, _P, _P]),
         "nfo_pack": (None, [_P, _I64, _I32, _I64, _P, _P, _I64]),
@@ -128,16 +127,6 @@ def health(g, mask, lib=None):
     st = np.zeros(W, dtype=STATS_DTYPE)
     lib.nfo_health(_ptr(g), stride, W, n, _ptr(np.ascontiguousarray(mask, np.uint64)), _ptr(st))
     return st
-
-
-def health_acc(g, mask, stats, lib=None):
-    """Continue `stats` (STATS_DTYPE, length W) over the chunk g (start % 64 == 0)."""
-    lib = lib or load()
-    g, stride = _grads(g)
-    W, n = g.shape
-    lib.nfo_health_acc(_ptr(g), stride, W, n, _ptr(np.ascontiguousarray(mask, np.uint64)),
-                       _ptr(stats))
-    return stats
 
 
 def scale(stats, n_eligible, lib=None):

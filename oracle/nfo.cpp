@@ -18,8 +18,8 @@
  *   R4  Counts are uint8, so 1 <= W <= 255.
  *   R5  One scale per bucket: the mean over workers of each worker's mean
  *       |g| over eligible elements (§5.2 records a mean-absolute scale).
- *       Per-worker sums in FP64 with i ascending; the combination divides
- *       each worker sum by n_E, adds in worker order, divides by W, and
+ *       The per-worker sums are those of R8; the combination divides each
+ *       worker sum by n_E, adds in worker order in FP64, divides by W, and
  *       rounds to FP32 once.
  *   R6  Decode: SOFT q_c = (2c - W) / W, the vote margin (default); MAJORITY
  *       q_c = sign(2c - W) with a tie giving 0 (§5.2's majority voting).
@@ -29,8 +29,13 @@
  *       for w = 1..W-1 (worker order, no contraction).  SUM returns s, MEAN
  *       returns fl32(s / W) by IEEE division.
  *   R8  Health per worker: nonfinite count over all n; sum |g| over eligible
- *       elements; sum g*g over all n (the FP64 product of two FP32 values is
- *       exact).  FP64 accumulators start at +0.0.
+ *       elements; sum g*g over all n.  Both sums are the exact real sums of
+ *       their terms, rounded once to FP64 (to nearest, ties to even), so they
+ *       depend on no summation order.  A NaN term makes a sum NaN; otherwise
+ *       an infinite term makes it +Inf (as IEEE addition of non-negative
+ *       terms does).  The paper fixes no precision for these statistics; the
+ *       exact sum is the one every correct implementation can reproduce bit
+ *       for bit, which the G-Ternary threshold (R18) needs.
  *   R9  Reason bits are all evaluated every time (nfo.h lists them).
  *   R10 Any non-finite input value in any worker sends the bucket to FP32.
  *   R11 A worker whose eligible |g| sum is exactly 0 (n_E > 0) sends the
@@ -48,8 +53,9 @@
  * the gating pattern around the vote; the paper fixes neither the rule nor
  * its point):
  *   R18 Gating is on the write side, before aggregation (§2.2), per worker:
- *       theta_w = fl32(tau * fl32(S_w / n_E)), S_w the worker's FP64 |g| sum
- *       over eligible elements (R8), tau >= 0 a policy input (default 0.5).
+ *       theta_w = fl32(tau * fl32(S_w / n_E)), S_w the worker's |g| sum over
+ *       eligible elements (R8, exact and rounded once), tau >= 0 a policy
+ *       input (default 0.5).
  *       An eligible element with |g| < theta_w (FP32 comparison) is gated to
  *       0.  NaN compares false, so it is never gated and never votes.
  *   R19 The payload is two positional planes per worker (R2 layout): pos =
@@ -114,27 +120,101 @@ int64_t nfo_count_eligible(const uint64_t* mask, int64_t n) {
 }
 
 /* ---- a2: per-worker health (R8) ----------------------------------------- */
-void nfo_health_acc(const float* g, int64_t stride, int32_t W, int64_t n,
-                    const uint64_t* mask, nfo_stats* stats) {
-  for (int32_t w = 0; w < W; ++w) {
-    const float* row = g + (int64_t)w * stride;
-    for (int64_t i = 0; i < n; ++i) {
-      double x = (double)row[i];
-      if (is_nonfinite(row[i])) stats[w].nonfinite += 1;
-      stats[w].sum_sq += x * x;
-      if (mask_bit(mask, i)) stats[w].sum_abs_elig += fabs(x);
-    }
+
+/* Exact sums.  A finite FP32 value is m * 2^(e - 150) with a 24-bit integer
+ * significand m and e = max(biased exponent, 1), so |g| is an integer number
+ * of units 2^-149 and g*g (m*m < 2^48) an integer number of units 2^-298.  A
+ * sum of such terms is kept exactly as an unsigned integer in base-2^32
+ * digits (least significant first); 20 digits hold any sum of fewer than
+ * 2^40 terms of either kind.  Carries are propagated lazily: a term adds
+ * less than 2^32 to each of three digits, so a digit stays below 2^63 for
+ * 2^31 terms between propagations. */
+#define NFO_XDIG 20
+typedef struct {
+  uint64_t d[NFO_XDIG];
+  uint32_t pending; /* terms added since the last carry propagation */
+} nfo_xsum;
+
+static void xsum_carry(nfo_xsum* a) {
+  for (int i = 0; i + 1 < NFO_XDIG; ++i) {
+    a->d[i + 1] += a->d[i] >> 32;
+    a->d[i] &= 0xffffffffu;
   }
+  a->pending = 0;
+}
+
+/* a += v * 2^p (v < 2^48, 0 <= p <= 506). */
+static void xsum_add(nfo_xsum* a, uint64_t v, int p) {
+  unsigned __int128 t = (unsigned __int128)v << (p % 32); /* < 2^80 */
+  int i = p / 32;
+  a->d[i] += (uint64_t)(t & 0xffffffffu);
+  a->d[i + 1] += (uint64_t)((t >> 32) & 0xffffffffu);
+  a->d[i + 2] += (uint64_t)(t >> 64);
+  if (++a->pending == (1u << 31)) xsum_carry(a);
+}
+
+static int xsum_bit(const nfo_xsum* a, int i) {
+  return (int)((a->d[i / 32] >> (i % 32)) & 1u);
+}
+
+/* The integer a times 2^unit_exp, rounded once to FP64, to nearest with ties
+ * to even.  The results here are far inside FP64's normal range. */
+static double xsum_round(nfo_xsum* a, int unit_exp) {
+  xsum_carry(a);
+  int top = -1; /* index of the highest set bit */
+  for (int i = 32 * NFO_XDIG - 1; i >= 0; --i)
+    if (xsum_bit(a, i)) {
+      top = i;
+      break;
+    }
+  if (top < 0) return 0.0;
+  int low = top - 52; /* lowest bit kept in a 53-bit significand */
+  if (low < 0) low = 0;
+  uint64_t m = 0;
+  for (int i = top; i >= low; --i) m = (m << 1) | (uint64_t)xsum_bit(a, i);
+  if (low > 0) {
+    int half = xsum_bit(a, low - 1); /* the first bit dropped */
+    int below = 0;                   /* any later bit dropped */
+    for (int i = low - 2; i >= 0; --i) below |= xsum_bit(a, i);
+    if (half && (below || (m & 1u))) m += 1; /* may carry to 2^53: still exact */
+  }
+  return ldexp((double)m, low + unit_exp);
 }
 
 void nfo_health(const float* g, int64_t stride, int32_t W, int64_t n,
                 const uint64_t* mask, nfo_stats* stats) {
   for (int32_t w = 0; w < W; ++w) {
+    const float* row = g + (int64_t)w * stride;
+    nfo_xsum sabs, ssq;
+    memset(&sabs, 0, sizeof sabs);
+    memset(&ssq, 0, sizeof ssq);
+    int abs_nan = 0, abs_inf = 0, sq_nan = 0, sq_inf = 0;
     stats[w].nonfinite = 0;
-    stats[w].sum_abs_elig = 0.0;
-    stats[w].sum_sq = 0.0;
+    for (int64_t i = 0; i < n; ++i) {
+      float x = row[i];
+      int elig = mask_bit(mask, i);
+      if (is_nonfinite(x)) {
+        stats[w].nonfinite += 1;
+        int nan = x != x;
+        sq_nan |= nan;
+        sq_inf |= !nan;
+        if (elig) {
+          abs_nan |= nan;
+          abs_inf |= !nan;
+        }
+        continue;
+      }
+      uint32_t u;
+      memcpy(&u, &x, sizeof u);
+      uint32_t e = (u >> 23) & 0xffu;
+      uint64_t m = (u & 0x7fffffu) | (e ? 0x800000u : 0u);
+      int p = (int)(e ? e : 1) - 1; /* |x| = m * 2^p units of 2^-149 */
+      xsum_add(&ssq, m * m, 2 * p); /* x*x = m*m * 2^2p units of 2^-298 */
+      if (elig) xsum_add(&sabs, m, p);
+    }
+    stats[w].sum_abs_elig = abs_nan ? NAN : abs_inf ? INFINITY : xsum_round(&sabs, -149);
+    stats[w].sum_sq = sq_nan ? NAN : sq_inf ? INFINITY : xsum_round(&ssq, -298);
   }
-  nfo_health_acc(g, stride, W, n, mask, stats);
 }
 
 /* ---- a5 part 1: bucket scale (§5.2, R5) --------------------------------- */

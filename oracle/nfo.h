@@ -66,8 +66,10 @@ enum { NFO_FORMAT_BINARY = 0, NFO_FORMAT_TERNARY = 1 };
 
 typedef struct {
   uint64_t nonfinite;   /* count of non-finite values of worker w over all n   */
-  double sum_abs_elig;  /* sum of |g| over eligible elements, FP64, i ascending */
-  double sum_sq;        /* sum of g*g over all n elements, FP64, i ascending    */
+  double sum_abs_elig;  /* sum of |g| over eligible elements: exact, rounded
+                           once to FP64 (R8)                                  */
+  double sum_sq;        /* sum of g*g over all n elements: exact, rounded once
+                           to FP64 (R8)                                       */
 } nfo_stats;
 
 typedef struct {
@@ -98,13 +100,9 @@ int nfo_mask_from_segments(const int64_t* off, const int64_t* len,
                            uint64_t* mask);
 int64_t nfo_count_eligible(const uint64_t* mask, int64_t n);
 
-/* Health (R7, R8).  nfo_health zeroes stats then accumulates; the _acc form
- * continues a previous call so a bucket can be fed in ascending chunks whose
- * starts are multiples of 64 (mask points at the chunk's first word). */
+/* Health (R8): non-finite counts and the two exact sums of each worker. */
 void nfo_health(const float* g, int64_t stride, int32_t W, int64_t n,
                 const uint64_t* mask, nfo_stats* stats);
-void nfo_health_acc(const float* g, int64_t stride, int32_t W, int64_t n,
-                    const uint64_t* mask, nfo_stats* stats);
 
 float nfo_scale(const nfo_stats* stats, int32_t W, int64_t n_eligible);
 void nfo_decide(const nfo_stats* stats, int32_t W, int64_t n,

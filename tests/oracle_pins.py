@@ -257,7 +257,35 @@ def pin_fp32_path(lib):
     assert nfo.fp32_path(g, nfo.OP_MEAN, lib=lib)[0] == want, "MEAN by division"
 
 
+def f64_round(x):
+    """Round a positive Fraction to the nearest FP64 value, ties to even.
+
+    Written from the definition, for values inside FP64's normal range: find
+    the binade, scale to a 53-bit integer significand, round half to even.
+    """
+    x = Fraction(x)
+    assert x > 0
+    e = x.numerator.bit_length() - x.denominator.bit_length()
+    if Fraction(2) ** e > x:
+        e -= 1
+    while Fraction(2) ** (e + 1) <= x:
+        e += 1
+    quantum = Fraction(2) ** (e - 52)
+    q, r = divmod(x, quantum)
+    q = int(q)
+    if r > quantum / 2 or (r == quantum / 2 and q % 2 == 1):
+        q += 1
+    return float(q * quantum)  # exact: q * quantum has at most 53 significant bits
+
+
+def exact_sum64(vals):
+    """The exact sum of FP32 values (as Fractions), rounded once to FP64."""
+    t = sum((Fraction(float(v)) for v in vals), Fraction(0))
+    return 0.0 if t == 0 else f64_round(t)
+
+
 def pin_health(lib):
+    """R8: non-finite counts, and both sums exact and rounded once to FP64."""
     rng = np.random.default_rng(15)
     W, n = 5, 1000
     g = (rng.standard_normal((W, n)) * 1e-3).astype(np.float32)
@@ -265,36 +293,56 @@ def pin_health(lib):
     g[1, 20] = np.inf
     g[3, 999] = -np.inf
     m = (rng.random(n) < 0.6).astype(np.uint8)
+    m[10] = m[20] = 1  # a NaN and an infinity, both eligible
+    m[999] = 0
     words = mask_of(m)
     st = nfo.health(g, words, lib=lib)
     assert st["nonfinite"].tolist() == (~np.isfinite(g)).sum(axis=1).tolist(), "nonfinite"
     for w in range(W):
         x = g[w].astype(np.float64)
         if np.all(np.isfinite(x)):
-            ssq = math.fsum((x * x).tolist())
-            sab = math.fsum(np.abs(x[m == 1]).tolist())
-            assert abs(st["sum_sq"][w] - ssq) <= 2 * n * 2.0 ** -53 * ssq, f"ssq w={w}"
-            assert abs(st["sum_abs_elig"][w] - sab) <= 2 * n * 2.0 ** -53 * sab, f"sabs w={w}"
-        else:
-            assert not np.isfinite(st["sum_sq"][w]), "nonfinite ssq"
-    # ssq runs over all n, sabs over the eligible elements only: dyadic values
-    # make every FP64 sum exact, so equality is exact
-    g = rng.integers(-64, 65, size=(3, 300)).astype(np.float32) / np.float32(32)
-    m = (rng.random(300) < 0.5).astype(np.uint8)
+            # math.fsum returns the correctly rounded sum of its terms, and
+            # each term (|g|, or g*g: 48 significant bits) is exact in FP64
+            assert st["sum_sq"][w] == math.fsum((x * x).tolist()), f"ssq w={w}"
+            assert st["sum_abs_elig"][w] == math.fsum(np.abs(x[m == 1]).tolist()), f"sabs w={w}"
+    # IEEE semantics of non-finite terms: NaN wins, else +Inf; |g| only where eligible
+    assert np.isnan(st["sum_sq"][1]) and np.isnan(st["sum_abs_elig"][1]), "NaN in worker 1"
+    assert st["sum_sq"][3] == np.inf, "-Inf squared"
+    assert st["sum_abs_elig"][3] == math.fsum(np.abs(g[3, m == 1].astype(np.float64)).tolist()), \
+        "an infinity off the mask leaves |g| finite"
+    # exact rationals on the full FP32 range: the largest finite value,
+    # subnormals, and sums that land on or next to a rounding midpoint
+    cases = [
+        [1.0, 2.0 ** -53],                          # midpoint, even below: 1
+        [1.0, 2.0 ** -52, 2.0 ** -53],              # midpoint, even above: 1 + 2^-51
+        [1.0, 2.0 ** -53, 2.0 ** -149],             # just past the midpoint: up
+        [2.0 ** -53, 1.0, 2.0 ** -149],
+        [3.4028234663852886e38] * 7 + [2.0 ** -149] * 3,
+        [2.0 ** -149, 2.0 ** -140, 2.0 ** -126, 1.5e-45],
+        [1.0, 2.0 ** -27, 2.0 ** -27],              # g*g: 1 + 2 * 2^-54, a midpoint
+        [1.0, 2.0 ** -27, 2.0 ** -27, 2.0 ** -27],  # g*g: 1 + 3 * 2^-54, up
+        [7.0, -2.0 ** -60, 2.0 ** -49, -3.0e-39, 1e30, -1e-30],
+    ]
+    for k, vals in enumerate(cases):
+        g = np.array([vals], dtype=np.float32)
+        m = np.ones(len(vals), np.uint8)
+        m[-1] = 0 if len(vals) > 3 else 1
+        st = nfo.health(g, mask_of(m), lib=lib)
+        want_abs = exact_sum64([abs(float(v)) for v, e in zip(g[0], m) if e])
+        want_sq = exact_sum64([float(v) * float(v) for v in g[0]])
+        assert st["sum_abs_elig"][0] == want_abs, f"sabs exact case {k}"
+        assert st["sum_sq"][0] == want_sq, f"ssq exact case {k}"
+    # the exact sum depends on no order: a permutation gives the same bits
+    g = (rng.standard_normal((3, 777)) * np.exp(rng.uniform(-40, 40, (3, 777)))).astype(np.float32)
+    m = (rng.random(777) < 0.8).astype(np.uint8)
     st = nfo.health(g, mask_of(m), lib=lib)
+    perm = rng.permutation(777)
+    st2 = nfo.health(np.ascontiguousarray(g[:, perm]), mask_of(m[perm]), lib=lib)
+    assert st.tobytes() == st2.tobytes(), "order"
     for w in range(3):
-        assert st["sum_sq"][w] == float(sum(Fraction(float(v)) ** 2 for v in g[w])), "ssq exact"
-        assert st["sum_abs_elig"][w] == float(sum(abs(Fraction(float(v)))
-                                                  for v, e in zip(g[w], m) if e)), "sabs exact"
-    # chunked accumulation in ascending chunks equals one pass
-    g = gauss(rng, 4, 640)
-    m = (rng.random(640) < 0.7).astype(np.uint8)
-    words = mask_of(m)
-    whole = nfo.health(g, words, lib=lib)
-    part = np.zeros(4, dtype=nfo.STATS_DTYPE)
-    for c0 in range(0, 640, 128):
-        nfo.health_acc(np.ascontiguousarray(g[:, c0:c0 + 128]), words[c0 // 64:], part, lib=lib)
-    assert part.tobytes() == whole.tobytes(), "chunked health"
+        x = g[w].astype(np.float64)
+        assert st["sum_sq"][w] == math.fsum((x * x).tolist()), "ssq wide range"
+        assert st["sum_abs_elig"][w] == math.fsum(np.abs(x[m == 1]).tolist()), "sabs wide range"
 
 
 def pin_scale(lib):

@@ -33,11 +33,18 @@ MUTANTS = [
     ("fp32_reversed_order", "    for (int32_t w = 1; w < W; ++w) s = s + g[(int64_t)w * stride + i];",
      "    s = g[(int64_t)(W - 1) * stride + i];\n"
      "    for (int32_t w = W - 2; w >= 0; --w) s = s + g[(int64_t)w * stride + i];"),
-    ("ssq_eligible_only", "      stats[w].sum_sq += x * x;", "      if (mask_bit(mask, i)) stats[w].sum_sq += x * x;"),
-    ("ssq_fp32_accumulate", "      stats[w].sum_sq += x * x;", "      stats[w].sum_sq = (float)(stats[w].sum_sq + x * x);"),
-    ("sabs_all_elements", "      if (mask_bit(mask, i)) stats[w].sum_abs_elig += fabs(x);",
-     "      stats[w].sum_abs_elig += fabs(x);"),
-    ("sabs_signed", "stats[w].sum_abs_elig += fabs(x);", "stats[w].sum_abs_elig += x;"),
+    ("ssq_eligible_only", "      xsum_add(&ssq, m * m, 2 * p);", "      if (elig) xsum_add(&ssq, m * m, 2 * p);"),
+    ("ssq_exponent_not_doubled", "xsum_add(&ssq, m * m, 2 * p);", "xsum_add(&ssq, m * m, p);"),
+    ("sabs_all_elements", "      if (elig) xsum_add(&sabs, m, p);", "      xsum_add(&sabs, m, p);"),
+    ("sabs_no_implicit_bit", "(e ? 0x800000u : 0u)", "0u"),
+    ("sabs_subnormal_exponent", "int p = (int)(e ? e : 1) - 1;", "int p = (int)e;"),
+    ("sum_truncated", "    if (half && (below || (m & 1u))) m += 1;", ""),
+    ("sum_ties_away", "if (half && (below || (m & 1u))) m += 1;", "if (half) m += 1;"),
+    ("sum_ignores_sticky", "if (half && (below || (m & 1u))) m += 1;", "if (half && (m & 1u)) m += 1;"),
+    ("sum_drops_carry", "    a->d[i + 1] += a->d[i] >> 32;\n", ""),
+    ("sum_drops_third_digit", "  a->d[i + 2] += (uint64_t)(t >> 64);\n", ""),
+    ("sum_inf_before_nan", "abs_nan ? NAN : abs_inf ? INFINITY", "abs_inf ? INFINITY : abs_nan ? NAN"),
+    ("sum_nonfinite_any_position", "        if (elig) {\n          abs_nan |= nan;", "        if (1) {\n          abs_nan |= nan;"),
     ("nonfinite_nan_only", "return ((u >> 23) & 0xffu) == 0xffu;", "return isnan(x);"),
     ("scale_over_n", "d->scale = nfo_scale(stats, W, n_eligible);", "d->scale = nfo_scale(stats, W, n);"),
     ("scale_missing_mean_over_workers", "return (float)(acc / (double)W);", "return (float)acc;"),
@@ -77,8 +84,8 @@ MUTANTS = [
     ("mask_no_bounds_check", "    if (off[s] < 0 || len[s] < 0 || off[s] + len[s] > n) return -1;\n", ""),
     ("count_eligible_all", "  for (int64_t i = 0; i < n; ++i) c += mask_bit(mask, i);",
      "  for (int64_t i = 0; i < n; ++i) c += 1;"),
-    ("health_skips_last_element", "    for (int64_t i = 0; i < n; ++i) {\n      double x",
-     "    for (int64_t i = 0; i + 1 < n; ++i) {\n      double x"),
+    ("health_skips_last_element", "    for (int64_t i = 0; i < n; ++i) {\n      float x",
+     "    for (int64_t i = 0; i + 1 < n; ++i) {\n      float x"),
     # G-Ternary (R18-R21)
     ("tern_gate_le", "if (fabsf(x) < theta[w]) continue;", "if (fabsf(x) <= theta[w]) continue;"),
     ("tern_gate_signed", "if (fabsf(x) < theta[w]) continue;", "if (x < theta[w]) continue;"),
