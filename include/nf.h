@@ -38,10 +38,14 @@
  *     are ignored.  One mask is shared by all W workers (the binding is per
  *     model, §5.1).  Bitmap row w starts at bits + w * bits_stride_words.
  *   - Floating point: FP32 sums add workers in order w = 0..W-1 in FP32
- *     without contraction, so they are bit-reproducible; per-worker health
+ *     without contraction, so they are bit-reproducible.  Per-worker health
  *     sums are FP64 in a fixed order (deterministic, within 1e-12 relative
- *     of a sequential FP64 sum); no floating-point atomics are used, so two
- *     calls on the same inputs give bitwise identical results.
+ *     of the exact sum); where a pass builds no sign payload
+ *     (nf_bucket_health, the G-Ternary route, and routes the policy fixes
+ *     before reading) each worker's sum of |g| over eligible elements is
+ *     the exact sum rounded once to FP64 (ties to even), because the
+ *     G-Ternary gate derives from it (§2.2).  No floating-point atomics are
+ *     used, so two calls on the same inputs give bitwise identical results.
  *   - Calls on different streams with different workspaces may run
  *     concurrently.  The library keeps no mutable state besides the
  *     thread-local error string and the thread-local profiling events of
@@ -118,7 +122,10 @@ typedef struct {
   uint32_t reasons;     /* NF_REASON_* bitmask                                 */
   float scale;          /* mean over workers of the mean |g| over eligible
                            elements, rounded once to FP32; 0 if n_E == 0      */
-  uint32_t reserved;    /* 0                                                   */
+  uint32_t resummed;    /* workers whose |g| sum was re-summed exactly from
+                           the gradients because its carried error bound
+                           could not certify the rounding (diagnostic; 0
+                           from nf_route_decide and with sign words)          */
   int64_t n_eligible;   /* n_E: mask bits set in [0, n)                        */
   double bytes_route;   /* modeled payload bytes per worker of this route:
                            b*n_E/8 + 4 + 4(n - n_E) for L with b = 1 bit per

@@ -55,7 +55,7 @@ class nf_route_policy(ctypes.Structure):
 
 class nf_route_decision(ctypes.Structure):
     _fields_ = [("route", ctypes.c_int32), ("reasons", ctypes.c_uint32),
-                ("scale", ctypes.c_float), ("reserved", ctypes.c_uint32),
+                ("scale", ctypes.c_float), ("resummed", ctypes.c_uint32),
                 ("n_eligible", ctypes.c_int64), ("bytes_route", ctypes.c_double),
                 ("bytes_fp32", ctypes.c_double)]
 
@@ -88,7 +88,7 @@ class nf_endpoint_model(ctypes.Structure):
 
 STATS_DTYPE = np.dtype([("nonfinite", "<u8"), ("sum_abs_elig", "<f8"), ("sum_sq", "<f8")])
 DECISION_DTYPE = np.dtype([("route", "<i4"), ("reasons", "<u4"), ("scale", "<f4"),
-                           ("reserved", "<u4"), ("n_eligible", "<i8"),
+                           ("resummed", "<u4"), ("n_eligible", "<i8"),
                            ("bytes_route", "<f8"), ("bytes_fp32", "<f8")])
 STATS_BYTES = ctypes.sizeof(nf_worker_stats)        # 24
 DECISION_BYTES = ctypes.sizeof(nf_route_decision)   # 40

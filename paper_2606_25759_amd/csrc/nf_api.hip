@@ -170,6 +170,10 @@ nf_status run_pass1_decide(const nf::Geometry& geo, const float* g, int64_t stri
   nf::DecideArgs d;
   d.part = a.part;
   d.part_ne = a.part_ne;
+  d.g = g;
+  d.wstride = stride;
+  d.mask = mask;
+  d.exact = bits == nullptr;  // pass 1 without sign words tracks exact |g| sums
   d.stats = stats;
   d.dec = dec;
   if (pol) {

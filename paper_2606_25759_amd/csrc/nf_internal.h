@@ -151,11 +151,17 @@ inline Geometry make_geometry(int W, int64_t n_total, int64_t bucket_n) {
   return g;
 }
 
-// Per (bucket, block, worker) partial statistics written by pass 1.
+// Per (bucket, slot, worker) partial statistics written by pass 1.  The |g|
+// sum is carried as s + c with an error bound b (an XSum, nf_device.h): its
+// exact value lies within b of sabs + sabs_c.  Pass 1 without sign words
+// tracks every rounding error (exact mode); with sign words c and b start at
+// 0 and only the reductions after pass 1 track theirs.
 struct Partial {
   double sabs;
   double ssq;
   uint64_t nonfinite;
+  double sabs_c;
+  double sabs_b;
 };
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -198,6 +204,13 @@ struct Pass1Args {
 struct DecideArgs {
   const Partial* part;
   const uint64_t* part_ne;
+  // Exact mode (pass 1 without sign words): each worker's |g| sum is
+  // rounded once from its exact value, re-summed from the gradients when
+  // the carried error bound cannot certify the rounding.
+  const float* g;
+  int64_t wstride;
+  const uint64_t* mask;
+  int32_t exact;
   Partial* part2;          // second-level sums (gs > 0)
   uint64_t* part2_ne;
   nf_worker_stats* stats;
@@ -313,7 +326,7 @@ NF_HD inline void decide_from(const nf_worker_stats* st, int W, int64_t n, int64
   d->route = route;
   d->reasons = r;
   d->scale = bucket_scale(st, W, ne);
-  d->reserved = 0;
+  d->resummed = 0;
   d->n_eligible = ne;
   d->bytes_fp32 = 4.0 * (double)n;
   // one bit (binary) or two planes (ternary) per eligible element

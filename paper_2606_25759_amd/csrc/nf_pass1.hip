@@ -3,12 +3,18 @@
 //   k_pass1   write side (§3.3 step 5, §5.2): one read of the W gradient
 //             rows; sign payload by wavefront ballot, per-worker health in
 //             registers, FP32 sums at routed positions through an LDS stage.
+//             Without sign words (PACK false) each lane's |g| sum is proven
+//             exact tile by tile (or, past a failed proof, kept with its
+//             rounding errors), so that the decision can round the exact sum
+//             once.
 //             A block takes a chunk of tiles by one of four loops: fast (all
 //             eligible), mixed (all tiles full, some routed), routed
 //             (nothing eligible, element-major) or general (ragged tails).
 //   k_slotsum second level of the partials of buckets above kMaxSlots chunks
 //   k_decide  one block per bucket: fixed-order reduction of the pass-1
-//             partial statistics, then the route rules (§3.2, §6.4).
+//             partial statistics, then the route rules (§3.2, §6.4).  In
+//             exact mode it certifies each |g| sum's rounding and re-sums
+//             the worker exactly where it cannot.
 //
 // The path is bound by HBM bandwidth, so there is no MFMA: every step is a
 // streaming scan with a handful of VALU operations per element and worker.
@@ -18,6 +24,24 @@
 
 namespace nf {
 
+// The wavefront's |g| sum of one worker as an XSum: in exact mode from the
+// lanes' (s, c) pairs, otherwise the plain wavefront sum with no error kept.
+template <bool EXACT>
+__device__ __forceinline__ XSum lane_sum(double s, double c, uint32_t nz) {
+  if constexpr (EXACT) return wave_xsum(xlane(s, c, nz));
+  return XSum{wave_sum(s), 0.0, 0.0};
+}
+
+// p += q for partial statistics; the |g| sums as XSums.
+__device__ __forceinline__ void part_add(Partial& p, const Partial& q) {
+  const XSum x = xcombine(XSum{p.sabs, p.sabs_c, p.sabs_b}, XSum{q.sabs, q.sabs_c, q.sabs_b});
+  p.sabs = x.s;
+  p.sabs_c = x.c;
+  p.sabs_b = x.b;
+  p.ssq += q.ssq;
+  p.nonfinite += q.nonfinite;
+}
+
 // ------------------------------------------------------------------ pass 1
 //
 // WPW workers per wavefront and NW = pass1_words(WPW) words (64 elements
@@ -25,8 +49,12 @@ namespace nf {
 // word k, so every load instruction reads 256 contiguous bytes and the ballot
 // of "g > 0" over the wavefront is exactly bitmap word k.  A block takes one
 // chunk (G tiles of one bucket); launch q0 takes chunks q0 .. q0 + grid - 1.
+// Occupancy: eight wavefronts per SIMD (64 VGPRs) for one or two workers
+// per wavefront with sign words; four without (the exact |g| sums need a few
+// registers more, and at 64 they spilled: G-Ternary's first pass at GPT
+// scale 23.2 ms against 13.6 ms at four) or with more workers.
 template <int WPW, bool PACK>
-__global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <= 2 ? 8 : 4, WPW <= 2 ? 8 : 4))) void k_pass1(
+__global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <= 2 && PACK ? 8 : 4, WPW <= 2 && PACK ? 8 : 4))) void k_pass1(
     const float* __restrict__ g, const uint64_t* __restrict__ mask, uint64_t* __restrict__ bits,
     float* __restrict__ out, Partial* __restrict__ part, uint64_t* __restrict__ part_ne, Pass1Args a,
     int64_t q0) {
@@ -69,13 +97,22 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
   __shared__ uint32_t tflags;  // mixed chunks: bit i = tile tb + i has a routed element
   if (threadIdx.x == 0) tflags = 0;
 
-  double sabs[WPW], ssq[WPW];
+  // Per-worker health of this lane.  Exact mode (no sign words): sabs[j] +
+  // sabc[j] is the lane's exact |g| sum (TwoSum per term).
+  constexpr bool EXACT = !PACK;
+  double sabs[WPW], sabc[WPW], ssq[WPW];
   uint64_t nonf[WPW];
+  uint32_t snz[WPW], um[WPW];  // exact mode: see tile_into_lane
+  bool tw[WPW];
 #pragma unroll
   for (int j = 0; j < WPW; ++j) {
     sabs[j] = 0.0;
+    sabc[j] = 0.0;
     ssq[j] = 0.0;
     nonf[j] = 0;
+    snz[j] = 0;
+    um[j] = ~0u;
+    tw[j] = false;
   }
   uint64_t ne = 0;
 
@@ -219,6 +256,8 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
           if (lane == 0 && w0 + w < a.W) {
             Partial p;
             p.sabs = 0.0;
+            p.sabs_c = 0.0;
+            p.sabs_b = 0.0;
             p.ssq = s2;
             p.nonfinite = nf2[w];
             red[v * a.W + w0 + w] = p;
@@ -308,6 +347,8 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
       if (lane == 0 && w < a.W) {
         Partial p;
         p.sabs = 0.0;
+        p.sabs_c = 0.0;
+        p.sabs_b = 0.0;
         p.ssq = s2;
         p.nonfinite = nf2[w];
         red[v * a.W + w] = p;
@@ -345,6 +386,7 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
         continue;
       }
       double s1 = 0.0, s2 = 0.0;
+      uint32_t umt = ~0u;
       uint64_t bb[NW];
 #pragma unroll
       for (int k = 0; k < NW; ++k) {
@@ -352,7 +394,9 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
         const double d = (double)x[k];
         s2 = __builtin_fma(d, d, s2);
         s1 += __builtin_fabs(d);
+        if constexpr (EXACT) umt = term_umin(umt, x[k]);
       }
+      if constexpr (EXACT) tile_into_lane<NW>(sabs[j], sabc[j], snz[j], um[j], tw[j], s1, umt, rp[j] + t * tile, ~0u);
       if (PACK) {
         uint32_t wlo, whi;
         lanes_from_ballots<NW>(bb, wlo, whi);
@@ -362,7 +406,7 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
 #pragma unroll
         for (int k = 0; k < NW; ++k) nonf[j] += __popcll(__ballot(!finite32(x[k])));
       }
-      sabs[j] += s1;
+      if constexpr (!EXACT) sabs[j] += s1;
       ssq[j] += s2;
     }
   };
@@ -420,13 +464,22 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
             continue;
           }
           double s1 = 0.0, s2 = 0.0;
+          uint32_t umt = ~0u;
           uint64_t bb[NW];
 #pragma unroll
           for (int k = 0; k < NW; ++k) {
             if (PACK) bb[k] = __ballot(x[k] > 0.0f) & mw[k];
             const double d = (double)x[k];
             s2 = __builtin_fma(d, d, s2);
-            s1 += ((mw[k] >> lane) & 1ull) ? __builtin_fabs(d) : 0.0;
+            const bool el = (mw[k] >> lane) & 1ull;
+            s1 += el ? __builtin_fabs(d) : 0.0;
+            if constexpr (EXACT) umt = term_umin(umt, el ? x[k] : 0.0f);
+          }
+          if constexpr (EXACT) {
+            uint32_t el = 0;
+#pragma unroll
+            for (int k = 0; k < NW; ++k) el |= (uint32_t)((mw[k] >> lane) & 1ull) << k;
+            tile_into_lane<NW>(sabs[j], sabc[j], snz[j], um[j], tw[j], s1, umt, rp[j] + t * tile, el);
           }
           if (PACK) {
             uint32_t wlo, whi;
@@ -437,7 +490,7 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
 #pragma unroll
             for (int k = 0; k < NW; ++k) nonf[j] += __popcll(__ballot(!finite32(x[k])));
           }
-          sabs[j] += s1;
+          if constexpr (!EXACT) sabs[j] += s1;
           ssq[j] += s2;
           if (stage_tile) {
             float* st = stage + (int64_t)w * tile + eg * T + lane;
@@ -566,6 +619,7 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
           }
         }
         double s1 = 0.0, s2 = 0.0;
+        uint32_t umt = ~0u;
         uint64_t bb[NW];
         if (mine_all) {
 #pragma unroll
@@ -574,6 +628,7 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
             const double d = (double)x[k];
             s2 = __builtin_fma(d, d, s2);
             s1 += __builtin_fabs(d);
+            if constexpr (EXACT) umt = term_umin(umt, x[k]);
           }
         } else {
 #pragma unroll
@@ -581,8 +636,17 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
             if (PACK) bb[k] = __ballot(x[k] > 0.0f) & mw[k];
             const double d = (double)x[k];
             s2 = __builtin_fma(d, d, s2);
-            s1 += ((mw[k] >> lane) & 1ull) ? __builtin_fabs(d) : 0.0;
+            const bool el = (mw[k] >> lane) & 1ull;
+            s1 += el ? __builtin_fabs(d) : 0.0;
+            if constexpr (EXACT) umt = term_umin(umt, el ? x[k] : 0.0f);
           }
+        }
+        if constexpr (EXACT) {
+          uint32_t el = 0;
+#pragma unroll
+          for (int k = 0; k < NW; ++k) el |= (uint32_t)((mw[k] >> lane) & 1ull) << k;
+          tile_into_lane<NW>(sabs[j], sabc[j], snz[j], um[j], tw[j], s1, umt,
+                             g + (int64_t)w * a.wstride + base + e0 + lane, el);
         }
         if (PACK) {
           uint32_t wlo, whi;
@@ -594,7 +658,7 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
 #pragma unroll
           for (int k = 0; k < NW; ++k) nonf[j] += __popcll(__ballot(!finite32(x[k])));
         }
-        sabs[j] += s1;
+        if constexpr (!EXACT) sabs[j] += s1;
         ssq[j] += s2;
         if (stage_tile) {
           float* st = stage + (int64_t)w * tile + eg * T + lane;
@@ -641,11 +705,13 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
       if (w >= a.W) break;
       if (PACK)
         for (int o = lane; o < valid; o += 64) bits[(int64_t)w * a.bstride + gw0 + o] = wbuf[w * cw + o];
-      const double s1 = wave_sum(sabs[j]);
+      const XSum x1 = lane_sum<EXACT>(sabs[j], sabc[j], snz[j]);
       const double s2 = wave_sum(ssq[j]);
       if (lane == 0) {
         Partial p;
-        p.sabs = s1;
+        p.sabs = x1.s;
+        p.sabs_c = x1.c;
+        p.sabs_b = x1.b;
         p.ssq = s2;
         p.nonfinite = nonf[j];
         part[slot * a.W + w] = p;
@@ -679,11 +745,13 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
     for (int j = 0; j < WPW; ++j) {
       const int w = wg + j * a.wg;
       if (w >= a.W) break;
-      const double s1 = wave_sum(sabs[j]);
+      const XSum x1 = lane_sum<EXACT>(sabs[j], sabc[j], snz[j]);
       const double s2 = wave_sum(ssq[j]);
       if (lane == 0) {
         Partial p;
-        p.sabs = s1;
+        p.sabs = x1.s;
+        p.sabs_c = x1.c;
+        p.sabs_b = x1.b;
         p.ssq = s2;
         p.nonfinite = nonf[j];
         red[eg * a.W + w] = p;
@@ -694,12 +762,7 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
   __syncthreads();
   for (int w = threadIdx.x; w < a.W; w += kThreads1) {
     Partial p = red[w];
-    for (int e = 1; e < a.eg; ++e) {
-      const Partial q2 = red[e * a.W + w];
-      p.sabs += q2.sabs;
-      p.ssq += q2.ssq;
-      p.nonfinite += q2.nonfinite;
-    }
+    for (int e = 1; e < a.eg; ++e) part_add(p, red[e * a.W + w]);
     part[slot * a.W + w] = p;
   }
   if (threadIdx.x == 0) {
@@ -729,27 +792,17 @@ __global__ __launch_bounds__(256) void k_slotsum(DecideArgs a) {
   const Partial* P = a.part + ((int64_t)b * a.slots + s0) * a.W;
   if (t < parts * a.W) {
     const int w = t % a.W;
-    double s1 = 0.0, s2 = 0.0;
-    uint64_t nf = 0;
+    Partial r;
+    r.sabs = r.sabs_c = r.sabs_b = r.ssq = 0.0;
+    r.nonfinite = 0;
 #pragma unroll 8
-    for (int k = t / a.W; k < cnt; k += parts) {
-      const Partial q = P[(int64_t)k * a.W + w];
-      s1 += q.sabs;
-      s2 += q.ssq;
-      nf += q.nonfinite;
-    }
-    red[t].sabs = s1;
-    red[t].ssq = s2;
-    red[t].nonfinite = nf;
+    for (int k = t / a.W; k < cnt; k += parts) part_add(r, P[(int64_t)k * a.W + w]);
+    red[t] = r;
   }
   __syncthreads();
   if (t < a.W) {
     Partial r = red[t];
-    for (int p = 1; p < parts; ++p) {
-      r.sabs += red[p * a.W + t].sabs;
-      r.ssq += red[p * a.W + t].ssq;
-      r.nonfinite += red[p * a.W + t].nonfinite;
-    }
+    for (int p = 1; p < parts; ++p) part_add(r, red[p * a.W + t]);
     a.part2[((int64_t)b * a.groups + grp) * a.W + t] = r;
   }
   if (t < 64) {
@@ -767,6 +820,8 @@ constexpr int kDecideThreads = 1024;
 
 __global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
   __shared__ nf_worker_stats st[256];
+  __shared__ uint8_t redo[256];            // exact mode: re-sum this worker
+  __shared__ unsigned long long hist[256];  // exponent bins of the re-summation
   __shared__ uint64_t ne_s;
   __shared__ int kfin_s;
   __shared__ double med_s;
@@ -783,22 +838,21 @@ __global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
   // The slot loops are unrolled so that their loads are in flight together;
   // the adds keep their order.
   for (int w = v; w < a.W; w += kDecideThreads / 64) {
-    double s1 = 0.0, s2 = 0.0;
-    uint64_t nf = 0;
+    Partial r;
+    r.sabs = r.sabs_c = r.sabs_b = r.ssq = 0.0;
+    r.nonfinite = 0;
 #pragma unroll 8
-    for (int k = lane; k < used; k += 64) {
-      const Partial p = P[(int64_t)k * a.W + w];
-      s1 += p.sabs;
-      s2 += p.ssq;
-      nf += p.nonfinite;
-    }
-    s1 = wave_sum(s1);
-    s2 = wave_sum(s2);
-    nf = wave_sum_u64(nf);
+    for (int k = lane; k < used; k += 64) part_add(r, P[(int64_t)k * a.W + w]);
+    const XSum x1 = wave_xsum(XSum{r.sabs, r.sabs_c, r.sabs_b});
+    const double s2 = wave_sum(r.ssq);
+    const uint64_t nf = wave_sum_u64(r.nonfinite);
     if (lane == 0) {
+      double s1;
+      const bool certified = xround(x1, s1);
       st[w].nonfinite = nf;
       st[w].sum_abs_elig = s1;
       st[w].sum_sq = s2;
+      redo[w] = a.exact && !certified;
     }
   }
   if (v == 0) {
@@ -809,6 +863,19 @@ __global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
     if (lane == 0) ne_s = s;
   }
   __syncthreads();
+  // Exact mode: a worker whose rounding the bound could not certify is
+  // summed again from its gradients, exactly (rare: it takes a total within
+  // the bound of a rounding midpoint).
+  uint32_t resummed = 0;
+  if (a.exact) {
+    for (int w = 0; w < a.W; ++w) {
+      if (!redo[w]) continue;  // block-uniform
+      const double e = exact_abs_sum(a.g + (int64_t)w * a.wstride, a.mask, (int64_t)b * a.bucket_n, nbe, hist);
+      if (threadIdx.x == 0) st[w].sum_abs_elig = e;
+      ++resummed;
+    }
+    __syncthreads();
+  }
   for (int w = threadIdx.x; w < a.W; w += kDecideThreads) a.stats[(int64_t)b * a.W + w] = st[w];
   if (!a.dec) return;
   if (threadIdx.x == 0) {
@@ -825,6 +892,7 @@ __global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
   if (threadIdx.x == 0) {
     nf_route_decision d;
     decide_from(st, a.W, nbe, (int64_t)ne_s, a.pol, kfin, med_s, &d);
+    d.resummed = resummed;
     a.dec[b] = d;
   }
 }

@@ -253,12 +253,12 @@ def test_workspace_sizes():
     assert nf.nf_workspace_bytes(0, 10) == 0
     # One bucket of 6,553,600 elements at W=16 is a small problem: 12,800 tiles
     # in 985 chunks of 13, so 985 partial slots and 493 groups of two;
-    # 24-byte partials and 8-byte counts, each array 256-byte aligned.
+    # 40-byte partials and 8-byte counts, each array 256-byte aligned.
     a = nf.nf_workspace_bytes(16, 6_553_600)
-    assert a == 378_368 + 7_936 + 189_440 + 4_096
+    assert a == 630_528 + 7_936 + 315_648 + 4_096
     # 201 such buckets: 400 chunks of 32 tiles each, no second level.
     b = nf.nf_workspace_bytes_buckets(16, 6_553_600 * 201, 6_553_600)
-    assert b == 30_873_600 + 643_328
+    assert b == 51_456_000 + 643_328
     assert nf.nf_workspace_bytes_buckets(16, 100, 0) == 0
 
 

@@ -8,9 +8,9 @@ the host at a time).  Stress (W = 64, one 100M-element bucket, forced
 low-bit): statistics per worker row over every element, the thresholds from
 them, then the oracle's element-wise steps (planes, c+ and c-, FP32 path,
 output) over consecutive ranges covering the bucket, every word and value
-compared.  At these sizes the two sides' thresholds are required to agree
-bit for bit, so the planes are compared bit for bit everywhere.  The oracle
-builds its own mask from the layout's segments.
+compared.  Both sides round each worker's exact |g| sum once, so the sums,
+the thresholds, the scale, the planes and every decoded value are compared
+bit for bit.  The oracle builds its own mask from the layout's segments.
 """
 from concurrent.futures import ThreadPoolExecutor
 
@@ -21,7 +21,7 @@ import torch
 import oracle as nfo
 import paper_2606_25759_amd as nf
 import synth
-from tests.nfgpu import POOL, check_stats, mask_bool, oracle_masks, rel_close, same_f32
+from tests.nfgpu import POOL, check_decision, check_stats, mask_bool, oracle_masks, same_f32
 from tests.test_gpu_ternary import check_ternary_bucket
 
 pytestmark = pytest.mark.gpu
@@ -66,7 +66,7 @@ class FullTernary:
                    out=self.out[a:e].cpu().numpy(), stats=self.stats[b:b + 1], dec=self.dec[b:b + 1])
         gh = self.g[:, a:e].cpu().numpy()
         return check_ternary_bucket(res, gh, np.ascontiguousarray(self.mask_o[ka:ke]), e - a, self.pol, 0, e - a,
-                                    f"{self.lay.name} bucket {b}", thresholds_agree=True)
+                                    f"{self.lay.name} bucket {b}")
 
 
 def test_fullsize_ternary_gpt1p3b_every_bucket():
@@ -89,10 +89,11 @@ def test_fullsize_ternary_stress_forced_lowbit():
         with ThreadPoolExecutor(POOL) as ex:
             ref_st = np.array(list(ex.map(lambda w: nfo.health(gh[w:w + 1], mask)[0], range(W))),
                               dtype=nfo.STATS_DTYPE)
-        check_stats(f.stats[0], ref_st, "stress ternary")
+        check_stats(f.stats[0], ref_st, "stress ternary", exact_abs=True)
         d = f.dec[0]
         assert int(d["route"]) == nfo.ROUTE_L
         rd = nfo.decide(ref_st, n, n_e, nfo.policy(force_lowbit=1, format=nfo.FORMAT_TERNARY, tau=0.5))
+        check_decision(d, rd, "stress ternary", exact_scale=True)
         th_gpu = nf.nf_ternary_threshold(f.stats[0], n_e, 0.5)
         th_ref = np.array([nfo.ternary_threshold(ref_st[w], n_e, 0.5) for w in range(W)], np.float32)
         assert np.array_equal(th_gpu.view(np.uint32), th_ref.view(np.uint32)), "thresholds"
@@ -115,10 +116,7 @@ def test_fullsize_ternary_stress_forced_lowbit():
             out = f.out[a:e].cpu().numpy()
             m = mask_bool(mw, e - a)
             assert same_f32(out[~m], ref[~m]), f"{tag} routed positions"
-            want = (np.float32(d["scale"]) * q[cp.astype(int) - cn.astype(int) + W]).astype(np.float32)
-            assert same_f32(out[m], want[m]), f"{tag} decoded values vs fl32(scale*q[d])"
-            ok, err = rel_close(out[m], ref[m])
-            assert ok, f"{tag} decoded values vs oracle: {err}"
+            assert same_f32(out[m], ref[m]), f"{tag} decoded values"
             return e - a
 
         with ThreadPoolExecutor(POOL) as ex:

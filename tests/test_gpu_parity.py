@@ -90,7 +90,8 @@ def test_bucket_health(W, n):
     nf.nf_bucket_health(H.to_dev(g), n, H.to_dev(m if len(m) else np.zeros(1, np.uint64), torch.int64),
                         stats, ws)
     ref = nfo.health(np.ascontiguousarray(g[:, :n]), _clean_mask(m, n))
-    H.check_stats(nf.stats_host(stats, W)[0], ref)
+    # without sign words the |g| sums are the exact sums rounded once
+    H.check_stats(nf.stats_host(stats, W)[0], ref, exact_abs=True)
 
 
 # -------------------------------------------------------------- nf_pack_signs
