@@ -573,6 +573,17 @@ nf_status nf_set_phase_events(void* before_pass1, void* after_pass1, void* after
  */
 int64_t nf_pass1_launches(int32_t W, int64_t n_total, int64_t bucket_n, int32_t sign_words);
 
+/*
+ * Geometry query (no paper counterpart): the number of elements of every
+ * pass-1 chunk (a block's share of one bucket, the unit of its partial
+ * statistics; a bucket's last chunk may be shorter) for these sizes, and in
+ * *chunks_per_bucket (nullable) the chunks of a full bucket.  Pass 1 takes a
+ * chunk with no eligible element, or with every element eligible, by a loop
+ * of its own; tests use this to build such chunks.  0 for n_total = 0 or
+ * invalid sizes.  Pure host function.
+ */
+int64_t nf_pass1_chunk_elems(int32_t W, int64_t n_total, int64_t bucket_n, int64_t* chunks_per_bucket);
+
 #ifdef __cplusplus
 }
 #endif

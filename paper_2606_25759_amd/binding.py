@@ -33,7 +33,7 @@ EXPORTS = ["nf_abi_version", "nf_last_error", "nf_mask_from_segments", "nf_works
            "nf_bucket_health", "nf_pack_signs", "nf_fp32_reduce", "nf_signcount_reduce",
            "nf_route_decide", "nf_route_bucket", "nf_workspace_bytes_buckets", "nf_route_buckets",
            "nf_route_buckets_noalloc",
-           "nf_set_phase_events", "nf_pass1_launches", "nf_slice_scales_from_pass1", "nf_ternary_threshold", "nf_pack_ternary",
+           "nf_set_phase_events", "nf_pass1_launches", "nf_pass1_chunk_elems", "nf_slice_scales_from_pass1", "nf_ternary_threshold", "nf_pack_ternary",
            "nf_ternary_reduce", "nf_partial_counts", "nf_partial_count_reduce", "nf_stock_signcount",
            "nf_supervisor_init", "nf_supervisor_policy", "nf_supervisor_update", "nf_endpoint_guard",
            "nf_sliced_layout_sizes", "nf_sliced_layout", "nf_compact_signs", "nf_slice_workspace_bytes",
@@ -137,6 +137,7 @@ def load(path=None):
         "nf_set_phase_events": (ctypes.c_int, [_P, _P, _P, _P]),
         "nf_slice_scales_from_pass1": (_I32, [_P, _I64, _I32, _I64, _P, _P, _I64, _P, _P, _P, _SZ, _P]),
         "nf_pass1_launches": (_I64, [_I32, _I64, _I64, _I32]),
+        "nf_pass1_chunk_elems": (_I64, [_I32, _I64, _I64, _P]),
         "nf_ternary_threshold": (ctypes.c_int, [_P, _I32, _I64, ctypes.c_float, _P]),
         "nf_pack_ternary": (ctypes.c_int, [_P, _I64, _I32, _I64, _P, _P, _P, _I64, _P]),
         "nf_ternary_reduce": (ctypes.c_int, [_P, _I64, _I32, _I64, _P, _P, _I32, _P, _P, _P]),
@@ -509,6 +510,14 @@ def nf_pass1_launches(W, n_total, bucket_n, sign_words=True):
     """Pass-1 kernel launches of one nf_route_buckets call (profiling); pass
     sign_words=False for a pass 1 without sign words (G-Ternary, health)."""
     return int(load().nf_pass1_launches(W, n_total, bucket_n, int(bool(sign_words))))
+
+
+def nf_pass1_chunk_elems(W, n_total, bucket_n):
+    """(elements per pass-1 chunk, chunks of a full bucket) for these sizes
+    (geometry query); (0, 0) for invalid sizes."""
+    cpb = ctypes.c_int64(0)
+    e = int(load().nf_pass1_chunk_elems(W, n_total, bucket_n, ctypes.byref(cpb)))
+    return e, int(cpb.value)
 
 
 # ------------------------------------------------------- result decoding

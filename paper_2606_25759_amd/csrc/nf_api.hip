@@ -308,6 +308,13 @@ int64_t nf_pass1_launches(int32_t W, int64_t n_total, int64_t bucket_n, int32_t 
   return nf::ceil_div(geo.total_chunks, nf::pass1_launch_chunks(geo, sign_words != 0));
 }
 
+int64_t nf_pass1_chunk_elems(int32_t W, int64_t n_total, int64_t bucket_n, int64_t* chunks_per_bucket) {
+  if (W < 1 || W > 255 || n_total <= 0 || bucket_n <= 0) return 0;
+  const nf::Geometry geo = nf::make_geometry(W, n_total, bucket_n);
+  if (chunks_per_bucket) *chunks_per_bucket = geo.chunks_full;
+  return (int64_t)geo.tile * geo.G;
+}
+
 const char* nf_last_error(void) { return g_err.c_str(); }
 
 nf_status nf_mask_from_segments(const int64_t* off_host, const int64_t* len_host,

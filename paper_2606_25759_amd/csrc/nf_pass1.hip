@@ -32,12 +32,18 @@ __device__ __forceinline__ XSum lane_sum(double s, double c, uint32_t nz) {
   return XSum{wave_sum(s), 0.0, 0.0};
 }
 
-// p += q for partial statistics; the |g| sums as XSums.
+// p += q for partial statistics; in exact mode the |g| sums as XSums, else
+// as plain FP64 sums (their error parts stay 0).
+template <bool EXACT>
 __device__ __forceinline__ void part_add(Partial& p, const Partial& q) {
-  const XSum x = xcombine(XSum{p.sabs, p.sabs_c, p.sabs_b}, XSum{q.sabs, q.sabs_c, q.sabs_b});
-  p.sabs = x.s;
-  p.sabs_c = x.c;
-  p.sabs_b = x.b;
+  if constexpr (EXACT) {
+    const XSum x = xcombine(XSum{p.sabs, p.sabs_c, p.sabs_b}, XSum{q.sabs, q.sabs_c, q.sabs_b});
+    p.sabs = x.s;
+    p.sabs_c = x.c;
+    p.sabs_b = x.b;
+  } else {
+    p.sabs += q.sabs;
+  }
   p.ssq += q.ssq;
   p.nonfinite += q.nonfinite;
 }
@@ -762,7 +768,7 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
   __syncthreads();
   for (int w = threadIdx.x; w < a.W; w += kThreads1) {
     Partial p = red[w];
-    for (int e = 1; e < a.eg; ++e) part_add(p, red[e * a.W + w]);
+    for (int e = 1; e < a.eg; ++e) part_add<EXACT>(p, red[e * a.W + w]);
     part[slot * a.W + w] = p;
   }
   if (threadIdx.x == 0) {
@@ -778,6 +784,7 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
 // t < parts * W takes worker t % W and every parts-th slot from t / W on;
 // the parts are then added in order, so the result does not depend on
 // timing.
+template <bool EXACT>
 __global__ __launch_bounds__(256) void k_slotsum(DecideArgs a) {
   __shared__ Partial red[256];
   const int b = (int)(blockIdx.x / (unsigned)a.groups);
@@ -796,13 +803,13 @@ __global__ __launch_bounds__(256) void k_slotsum(DecideArgs a) {
     r.sabs = r.sabs_c = r.sabs_b = r.ssq = 0.0;
     r.nonfinite = 0;
 #pragma unroll 8
-    for (int k = t / a.W; k < cnt; k += parts) part_add(r, P[(int64_t)k * a.W + w]);
+    for (int k = t / a.W; k < cnt; k += parts) part_add<EXACT>(r, P[(int64_t)k * a.W + w]);
     red[t] = r;
   }
   __syncthreads();
   if (t < a.W) {
     Partial r = red[t];
-    for (int p = 1; p < parts; ++p) part_add(r, red[p * a.W + t]);
+    for (int p = 1; p < parts; ++p) part_add<EXACT>(r, red[p * a.W + t]);
     a.part2[((int64_t)b * a.groups + grp) * a.W + t] = r;
   }
   if (t < 64) {
@@ -818,6 +825,7 @@ __global__ __launch_bounds__(256) void k_slotsum(DecideArgs a) {
 // four each), so that fewer slot sums wait on each other.
 constexpr int kDecideThreads = 1024;
 
+template <bool EXACT>
 __global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
   __shared__ nf_worker_stats st[256];
   __shared__ uint8_t redo[256];            // exact mode: re-sum this worker
@@ -842,8 +850,8 @@ __global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
     r.sabs = r.sabs_c = r.sabs_b = r.ssq = 0.0;
     r.nonfinite = 0;
 #pragma unroll 8
-    for (int k = lane; k < used; k += 64) part_add(r, P[(int64_t)k * a.W + w]);
-    const XSum x1 = wave_xsum(XSum{r.sabs, r.sabs_c, r.sabs_b});
+    for (int k = lane; k < used; k += 64) part_add<EXACT>(r, P[(int64_t)k * a.W + w]);
+    const XSum x1 = EXACT ? wave_xsum(XSum{r.sabs, r.sabs_c, r.sabs_b}) : XSum{wave_sum(r.sabs), 0.0, 0.0};
     const double s2 = wave_sum(r.ssq);
     const uint64_t nf = wave_sum_u64(r.nonfinite);
     if (lane == 0) {
@@ -852,7 +860,7 @@ __global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
       st[w].nonfinite = nf;
       st[w].sum_abs_elig = s1;
       st[w].sum_sq = s2;
-      redo[w] = a.exact && !certified;
+      redo[w] = EXACT && !certified;
     }
   }
   if (v == 0) {
@@ -867,7 +875,7 @@ __global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
   // summed again from its gradients, exactly (rare: it takes a total within
   // the bound of a rounding midpoint).
   uint32_t resummed = 0;
-  if (a.exact) {
+  if (EXACT) {
     for (int w = 0; w < a.W; ++w) {
       if (!redo[w]) continue;  // block-uniform
       const double e = exact_abs_sum(a.g + (int64_t)w * a.wstride, a.mask, (int64_t)b * a.bucket_n, nbe, hist);
@@ -955,11 +963,17 @@ hipError_t launch_pass1(const Geometry& geo, const Pass1Args& a, hipStream_t s) 
 
 hipError_t launch_decide(const Geometry& geo, const DecideArgs& a, hipStream_t s) {
   if (geo.gs > 0) {
-    hipLaunchKernelGGL(k_slotsum, dim3((unsigned)(geo.nb * geo.groups)), dim3(256), 0, s, a);
+    if (a.exact)
+      hipLaunchKernelGGL(k_slotsum<true>, dim3((unsigned)(geo.nb * geo.groups)), dim3(256), 0, s, a);
+    else
+      hipLaunchKernelGGL(k_slotsum<false>, dim3((unsigned)(geo.nb * geo.groups)), dim3(256), 0, s, a);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(k_decide, dim3((unsigned)geo.nb), dim3(kDecideThreads), 0, s, a);
+  if (a.exact)
+    hipLaunchKernelGGL(k_decide<true>, dim3((unsigned)geo.nb), dim3(kDecideThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL(k_decide<false>, dim3((unsigned)geo.nb), dim3(kDecideThreads), 0, s, a);
   return hipGetLastError();
 }
 

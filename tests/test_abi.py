@@ -249,6 +249,18 @@ def test_pass1_launch_counts():
     assert nf.nf_pass1_launches(256, 100, 100) == 0
 
 
+def test_pass1_chunk_geometry():
+    # W = 16: tiles of 512 elements, 32 per chunk; a 25 MiB bucket has 400 chunks
+    assert nf.nf_pass1_chunk_elems(16, 6_553_600 * 201, 6_553_600) == (16_384, 400)
+    # W = 64: four workers per wavefront, tiles of 256 elements, 16 per chunk
+    assert nf.nf_pass1_chunk_elems(64, 100_000_000, 100_000_000) == (4_096, 24_415)
+    # a small problem takes shorter chunks to fill the chip (at most 1,024 chunks)
+    e, c = nf.nf_pass1_chunk_elems(4, 1 << 20, 1 << 20)
+    assert c <= 1024 and e * c >= 1 << 20 and e % 64 == 0
+    assert nf.nf_pass1_chunk_elems(0, 100, 100) == (0, 0)
+    assert nf.nf_pass1_chunk_elems(16, 0, 100) == (0, 0)
+
+
 def test_workspace_sizes():
     assert nf.nf_workspace_bytes(0, 10) == 0
     # One bucket of 6,553,600 elements at W=16 is a small problem: 12,800 tiles

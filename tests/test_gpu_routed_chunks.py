@@ -18,24 +18,26 @@ from tests import nfgpu as H
 pytestmark = pytest.mark.gpu
 
 
-def _chunk(W):
-    """Elements per pass-1 chunk of the library's geometry for W > 16 (its
-    tiles, words per worker and LDS budget for sign words)."""
-    wpw = 1
-    while wpw < -(-W // 16):
-        wpw *= 2
-    nw = 8 if wpw == 1 else (4 if wpw == 2 else 16 // wpw)
-    return min(32, 4096 // (W * nw)) * 64 * nw
+def routed_chunks(m, n, chunk):
+    """Full chunks of `chunk` elements with no eligible element (one bucket)."""
+    elig = H.mask_bool(m, n)
+    full = n // chunk
+    return int((~elig[: full * chunk].reshape(full, chunk).any(axis=1)).sum())
 
 
 @pytest.mark.parametrize("W", [17, 32, 33, 64, 100, 129, 255])
 def test_routed_chunks_wide(W):
-    n = 1040 * _chunk(W) + 777
+    # the library's own chunk size for a problem this large (its geometry query)
+    chunk, _ = nf.nf_pass1_chunk_elems(W, 1 << 30, 1 << 30)
+    n = 1040 * chunk + 777
+    got, per_bucket = nf.nf_pass1_chunk_elems(W, n, n)
+    assert got == chunk and per_bucket == -(-n // chunk) > 1024, (got, per_bucket)
     lay = synth.small(W, n, 4000 + W, elig_frac=0.5, nruns=40)
     g = synth.generate_host(lay)
     m = nfo.mask_from_segments(*synth.mask_segments(lay), n)
     routed = np.flatnonzero(~H.mask_bool(m, n))
-    assert routed.size > 4 * _chunk(W)
+    # the element-major path runs: several whole chunks hold no eligible element
+    assert routed_chunks(m, n, chunk) >= 4, routed_chunks(m, n, chunk)
     rng = np.random.default_rng(W)
     bad = [0, W // 2, W - 1]
     vals = np.array([np.nan, np.inf, -np.inf], np.float32)
