@@ -42,7 +42,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=None,
-                    choices=["tiny", "resnet50", "vitb16", "gpt1p3b", "stress"],
+                    choices=["tiny", "resnet50", "vitb16", "gpt1p3b", "stress", "fanin255"],
                     help="measure this workload only (default: the GPT-1.3B-scale headline, then a few "
                          "steps of every other workload in the JSON line's `configs`)")
     ap.add_argument("--force-lowbit", action="store_true", help="guard disabled (forced low-bit)")
@@ -786,9 +786,9 @@ def committed_counters(workload, fmt):
 def sweep_configs(nf, torch, gpt, args):
     """Every workload of the sweep after the headline: G-Ternary on the same
     GPT-scale buffer, then ViT-B/16 scale, ResNet-50 scale, the tiny bucket
-    (warm and cold caches) and the stress bucket (route F, forced low-bit,
-    forced low-bit G-Ternary).  Each row is a few timed steps and a bounded
-    oracle sample."""
+    (warm and cold caches), the stress bucket (route F, forced low-bit,
+    forced low-bit G-Ternary) and the W = 255 fan-in bucket pair.  Each row
+    is a few timed steps and a bounded oracle sample."""
     rows = []
     tern = nf.policy(format=nf.NF_FORMAT_TERNARY, tau=args.tau)
     m = gpt.measure(tern, 10, 2)
@@ -799,7 +799,8 @@ def sweep_configs(nf, torch, gpt, args):
             ("resnet50", [(nf.policy(), False, 50)]),
             ("tiny", [(nf.policy(), False, 200), (nf.policy(), True, 50)]),
             ("stress", [(nf.policy(), False, 10), (nf.policy(force_lowbit=1), False, 10),
-                        (nf.policy(force_lowbit=1, format=nf.NF_FORMAT_TERNARY, tau=args.tau), False, 10)])]
+                        (nf.policy(force_lowbit=1, format=nf.NF_FORMAT_TERNARY, tau=args.tau), False, 10)]),
+            ("fanin255", [(nf.policy(), False, 10)])]
     for name, runs in plan:
         wl = Workload(nf, torch, name, planes=2 if any(p.format for p, _, _ in runs) else 1)
         for pol, cold, steps in runs:

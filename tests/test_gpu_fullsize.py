@@ -86,7 +86,7 @@ class Full:
             return list(ex.map(self.check_bucket, range(self.nb)))
 
 
-@pytest.mark.parametrize("name", ["tiny", "resnet50", "vitb16"])
+@pytest.mark.parametrize("name", ["tiny", "resnet50", "vitb16", "fanin255"])
 def test_fullsize_every_bucket(name):
     f = Full(name, nf.policy())
     try:
