@@ -305,7 +305,7 @@ nf_status nf_set_phase_events(void* before_pass1, void* after_pass1, void* after
 int64_t nf_pass1_launches(int32_t W, int64_t n_total, int64_t bucket_n, int32_t sign_words) {
   if (W < 1 || W > 255 || n_total <= 0 || bucket_n <= 0) return 0;
   const nf::Geometry geo = nf::make_geometry(W, n_total, bucket_n);
-  return nf::ceil_div(geo.total_chunks, nf::pass1_launch_chunks(geo, sign_words != 0));
+  return geo.ngroups * nf::ceil_div(geo.total_chunks, nf::pass1_launch_chunks(geo, sign_words != 0));
 }
 
 int64_t nf_pass1_chunk_elems(int32_t W, int64_t n_total, int64_t bucket_n, int64_t* chunks_per_bucket) {

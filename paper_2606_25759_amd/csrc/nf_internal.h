@@ -16,8 +16,16 @@ namespace nf {
 // Pass 1 is worker-major: a block is 16 wavefronts; wavefront v serves
 // worker group wg = v % WG and element group eg = v / WG.  With W <= 16 each
 // wavefront owns one worker (WG = W) and the spare wavefronts take further
-// element groups (EG = 16 / W); with W > 16 each wavefront owns
-// ceil(W / 16) workers.  A tile is EG * T consecutive elements of all W
+// element groups (EG = 16 / W); with 16 < W <= 64 each wavefront owns
+// ceil(W / 16) workers.  Above 64 workers the rows go in ceil(W / 64)
+// groups of near-equal size, one after another (a launch sequence per
+// group, all with the geometry of the largest): sixteen workers per
+// wavefront held 32 FP64 health sums per lane and spilled (W = 255: pass 1
+// at 2.9 TB/s).  Every group then has at least 32 rows, so each of the 16
+// wavefronts' first worker exists in every group.  The groups share the
+// chunk slots (each writes its own workers' partials) and carry the FP32
+// sums at routed positions from one to the next through the output, so the
+// workers are still added in order.  A tile is EG * T consecutive elements of all W
 // rows; staging one tile of all workers in LDS (to add the workers in order
 // at FP32-routed positions) takes at most 64 KiB.
 //
@@ -32,6 +40,7 @@ namespace nf {
 // One chunk per compute unit (256 on MI355X) per launch is the best epoch
 // measured (128: -30%, 192 and 384: -7%, 512: -4%, 1024: -7%).
 constexpr int kWaves = 16;
+constexpr int kRowGroup = 64;  // worker rows per pass-1 group at most
 constexpr int kThreads1 = kWaves * 64;
 constexpr int kStageFloats = 16384;      // 64 KiB of LDS
 #ifndef NF_BITS_WORDS
@@ -48,6 +57,9 @@ constexpr int kStageFloats = 16384;      // 64 KiB of LDS
 #endif
 constexpr int kBitsWords = NF_BITS_WORDS;      // LDS words for a chunk's sign words (32 KiB)
 constexpr int kMaxSlots = 512;                 // partials the decision reduces per bucket at most
+// ... above 64 workers (the decision then reads 64 * W partials per bucket:
+// with 400 of 255 workers each, a 25 MiB bucket's decision took 0.28 ms)
+constexpr int kMaxSlotsWide = 64;
 constexpr int kEpochBlocks = NF_EPOCH_BLOCKS;  // chunks per pass-1 launch
 // Without sign words (statistics and routed sums only) the writes are few and
 // bigger launches lose less to tails: G-Ternary's first pass at GPT scale,
@@ -84,6 +96,7 @@ constexpr NF_HD int routed_steps(int nw) { return (kMaxG * nw + kWaves - 1) / kW
 
 struct Geometry {
   int W, wg, eg, wpw, T, tile, G;
+  int rows, ngroups;     // worker rows of the largest pass-1 group (<= 64), and groups
   int64_t n_total, bucket_n, nb;
   int64_t chunks_full;   // chunks of a full bucket
   int64_t total_chunks;  // over all buckets
@@ -101,20 +114,31 @@ inline int64_t pass1_launch_chunks(const Geometry& g, bool sign_words) {
   return sign_words || g.total_chunks <= kOneLaunchChunks ? pass1_epoch(g) : kEpochNoPack;
 }
 
+// Row group i of a geometry: its first worker and its rows (the first
+// W % ngroups groups take one row more).
+inline void row_group(const Geometry& g, int i, int* wbase, int* rows) {
+  const int q = g.W / g.ngroups, r = g.W % g.ngroups;
+  *wbase = i * q + (i < r ? i : r);
+  *rows = q + (i < r ? 1 : 0);
+}
+
 inline Geometry make_geometry(int W, int64_t n_total, int64_t bucket_n) {
   Geometry g;
   g.W = W;
-  g.wg = W < kWaves ? W : kWaves;
+  g.ngroups = W > kRowGroup ? (W + kRowGroup - 1) / kRowGroup : 1;
+  g.rows = (W + g.ngroups - 1) / g.ngroups;
+  const int R = g.rows;  // the pass-1 kernel's workers
+  g.wg = R < kWaves ? R : kWaves;
   g.eg = kWaves / g.wg;
   // Workers per wavefront, rounded up to a power of two (a template
   // parameter of pass 1).
-  int need = (W + g.wg - 1) / g.wg;
+  int need = (R + g.wg - 1) / g.wg;
   g.wpw = 1;
   while (g.wpw < need) g.wpw *= 2;
-  g.T = 64 * pass1_words(g.wpw);  // W * EG * T <= kStageFloats for every W <= 255
+  g.T = 64 * pass1_words(g.wpw);  // R * EG * T <= kStageFloats for every R <= 64
   g.tile = g.eg * g.T;
-  // A chunk's sign words, W * G * EG * (T / 64), fit kBitsWords.
-  int per_tile = W * g.eg * (g.T / 64);
+  // A chunk's sign words, R * G * EG * (T / 64), fit kBitsWords.
+  int per_tile = R * g.eg * (g.T / 64);
   g.G = kBitsWords / per_tile;
   if (g.G > kMaxG) g.G = kMaxG;
   if (g.G < 1) g.G = 1;
@@ -139,10 +163,12 @@ inline Geometry make_geometry(int W, int64_t n_total, int64_t bucket_n) {
   g.chunks_full = ceil_div(tiles_full, g.G);
   g.total_chunks = total_for(g.G);
   // Every chunk owns a slot, so no two chunks ever touch the same partial.
-  // A bucket of more than kMaxSlots chunks is first summed in groups of gs
-  // consecutive slots (at most kMaxSlots groups), which the decision reads.
+  // A bucket of more than kMaxSlots chunks (kMaxSlotsWide above 64 workers)
+  // is first summed in groups of gs consecutive slots (at most that many
+  // groups), which the decision reads.
   g.slots = (int)(g.chunks_full > 1 ? g.chunks_full : 1);
-  g.gs = g.chunks_full > kMaxSlots ? (int)ceil_div(g.chunks_full, kMaxSlots) : 0;
+  const int cap = W > kRowGroup ? kMaxSlotsWide : kMaxSlots;
+  g.gs = g.chunks_full > cap ? (int)ceil_div(g.chunks_full, cap) : 0;
   g.groups = g.gs ? (int)ceil_div(g.chunks_full, g.gs) : 0;
   int64_t words = (full + 63) / 64;
   int64_t chunks2 = ceil_div(words, kWordsPerWave2 * 4);
@@ -189,16 +215,20 @@ inline WorkspaceLayout workspace_layout(const Geometry& g) {
 enum SumMode { kSumsNone = 0, kSumsRouted = 1, kSumsAll = 2 };
 
 struct Pass1Args {
-  const float* g;
+  const float* g;  // the row group's first row
   int64_t wstride;
   const uint64_t* mask;
-  uint64_t* bits;  // NULL: no sign payload
+  uint64_t* bits;  // NULL: no sign payload; else the row group's first row
   int64_t bstride;
   float* out;      // FP32 sums (sum mode != none)
   Partial* part;
   uint64_t* part_ne;
   int64_t n_total, bucket_n, chunks_full, total_chunks;
   int32_t nb, W, wg, eg, T, G, slots, sums, mean;
+  // Row groups: W is this group's rows; partials are [slot][wtot] with this
+  // group's workers from wbase; racc: the routed FP32 sums continue from
+  // out (not the first group); rfin: the last group (MEAN divides there).
+  int32_t wtot, wbase, racc, rfin;
 };
 
 struct DecideArgs {
@@ -242,9 +272,10 @@ struct TernArgs {
   float tau;
   int64_t n_total, bucket_n;
   int32_t W, decode_mode, bpb2;
-  // pack geometry (filled by the pack launcher from the Geometry)
+  // pack geometry (filled by the pack launcher from the Geometry): the
+  // launch's row group is workers wbase .. wbase + rows - 1
   int64_t chunks_full, total_chunks;
-  int32_t nb, wg, eg, T, G;
+  int32_t nb, wg, eg, T, G, rows, wbase;
 };
 
 struct Pass2Args {

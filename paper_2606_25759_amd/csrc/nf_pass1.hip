@@ -102,6 +102,10 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
       reinterpret_cast<uint64_t*>(smem + stage_off + (stage_on ? (size_t)a.W * tile * sizeof(float) : 0));
   __shared__ uint32_t tflags;  // mixed chunks: bit i = tile tb + i has a routed element
   if (threadIdx.x == 0) tflags = 0;
+  // FP32 sum at a position: an earlier row group's running sum comes first;
+  // the mean divides by all workers after the last group.
+  auto sum_first = [&](int64_t pos, float x0) { return a.racc ? out[pos] + x0 : x0; };
+  auto sum_last = [&](float s) { return a.mean && a.rfin ? s / (float)a.wtot : s; };
 
   // Per-worker health of this lane.  Exact mode (no sign words): sabs[j] +
   // sabc[j] is the lane's exact |g| sum (TwoSum per term).
@@ -222,6 +226,14 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
       float run[MS];
 #pragma unroll
       for (int i = 0; i < MS; ++i) run[i] = 0.0f;
+      if (a.racc) {
+#pragma unroll
+        for (int i = 0; i < MS; ++i) {
+          const int st = v + kWaves * i;
+          if (st >= nsteps) break;
+          run[i] = out[c0 + (int64_t)st * 64 + lane];
+        }
+      }
       for (int w0 = 0; w0 < a.W; w0 += GW) {
         double q2[GW];
         uint64_t nf2[GW];
@@ -239,7 +251,7 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
 #pragma unroll
           for (int w = 0; w < GW; ++w)
             x[w] = w0 + w < a.W ? __builtin_nontemporal_load(g + (int64_t)(w0 + w) * a.wstride + e) : 0.0f;
-          float sum = w0 == 0 ? x[0] : run[i] + x[0];
+          float sum = (w0 == 0 && !a.racc) ? x[0] : run[i] + x[0];
 #pragma unroll
           for (int w = 1; w < GW; ++w)
             if (w0 + w < a.W) sum = sum + x[w];
@@ -278,13 +290,13 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
           p.ssq += red[v2 * a.W + w].ssq;
           p.nonfinite += red[v2 * a.W + w].nonfinite;
         }
-        part[slot * a.W + w] = p;
+        part[slot * a.wtot + w] = p;
       }
 #pragma unroll
       for (int i = 0; i < MS; ++i) {
         const int st = v + kWaves * i;
         if (st >= nsteps) break;
-        out[c0 + (int64_t)st * 64 + lane] = a.mean ? run[i] / (float)a.W : run[i];
+        out[c0 + (int64_t)st * 64 + lane] = sum_last(run[i]);
       }
       if (PACK) {
         const int64_t gw0 = c0 / 64;
@@ -321,11 +333,11 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
       float x[WR];
 #pragma unroll
       for (int w = 0; w < WR; ++w) x[w] = w < a.W ? __builtin_nontemporal_load(g + (int64_t)w * a.wstride + e) : 0.0f;
-      float sum = x[0];
+      float sum = sum_first(e, x[0]);
 #pragma unroll
       for (int w = 1; w < WR; ++w)
         if (w < a.W) sum = sum + x[w];
-      out[e] = a.mean ? sum / (float)a.W : sum;
+      out[e] = sum_last(sum);
 #pragma unroll
       for (int w = 0; w < WR; ++w) {
         const double d = (double)x[w];
@@ -370,7 +382,7 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
         p.ssq += q3.ssq;
         p.nonfinite += q3.nonfinite;
       }
-      part[slot * a.W + w] = p;
+      part[slot * a.wtot + w] = p;
     }
     if (threadIdx.x == 0) part_ne[slot] = 0;
     return;
@@ -514,10 +526,9 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
           const uint64_t pick = a.sums == kSumsAll ? ~0ull : ~mwords[ti * nwt + kw];
           const int e = kw * 64 + lane;
           if ((pick >> lane) & 1ull) {
-            float s2 = stage[e];
+            float s2 = sum_first(base + t0 + e, stage[e]);
             for (int w = 1; w < a.W; ++w) s2 = s2 + stage[w * tile + e];
-            if (a.mean) s2 = s2 / (float)a.W;
-            out[base + t0 + e] = s2;
+            out[base + t0 + e] = sum_last(s2);
           }
         }
         __syncthreads();
@@ -683,10 +694,9 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
         const int e = kw * 64 + lane;
         const uint64_t pick = (a.sums == kSumsAll ? ~0ull : ~tmask[kw]) & low_bits(lim - kw * 64);
         if ((pick >> lane) & 1ull) {
-          float s = stage[e];
+          float s = sum_first(base + t0 + e, stage[e]);
           for (int w = 1; w < a.W; ++w) s = s + stage[w * tile + e];
-          if (a.mean) s = s / (float)a.W;
-          out[base + t0 + e] = s;
+          out[base + t0 + e] = sum_last(s);
         }
       }
       __syncthreads();
@@ -720,7 +730,7 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
         p.sabs_b = x1.b;
         p.ssq = s2;
         p.nonfinite = nonf[j];
-        part[slot * a.W + w] = p;
+        part[slot * a.wtot + w] = p;
       }
     }
     if (wg == 0 && lane == 0) part_ne[slot] = ne;
@@ -769,7 +779,7 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
   for (int w = threadIdx.x; w < a.W; w += kThreads1) {
     Partial p = red[w];
     for (int e = 1; e < a.eg; ++e) part_add<EXACT>(p, red[e * a.W + w]);
-    part[slot * a.W + w] = p;
+    part[slot * a.wtot + w] = p;
   }
   if (threadIdx.x == 0) {
     uint64_t s = 0;
@@ -821,8 +831,12 @@ __global__ __launch_bounds__(256) void k_slotsum(DecideArgs a) {
   }
 }
 
-// 1024 threads: sixteen wavefronts take the workers in turn (at W = 64,
-// four each), so that fewer slot sums wait on each other.
+// 1024 threads: up to 64 workers, sixteen wavefronts take the workers in
+// turn (at W = 64, four each), the lanes of one splitting its slots, so
+// that fewer slot sums wait on each other.  Above 64 workers (a wavefront
+// would take up to sixteen in turn: 0.28 ms at W = 255) thread t takes
+// worker t % W and every P-th slot from t / W, P the largest power of two
+// with P * W <= 1024; the P parts of a worker are then added in order.
 constexpr int kDecideThreads = 1024;
 
 template <bool EXACT>
@@ -833,6 +847,7 @@ __global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
   __shared__ uint64_t ne_s;
   __shared__ int kfin_s;
   __shared__ double med_s;
+  __shared__ Partial wide[kDecideThreads];  // W > 64: [part][W]
   const int b = blockIdx.x;
   const int v = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wavefront index, uniform
   const int lane = threadIdx.x & 63;
@@ -845,22 +860,48 @@ __global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
   const int used = (int)(two ? (chunks + a.gs - 1) / a.gs : chunks);
   // The slot loops are unrolled so that their loads are in flight together;
   // the adds keep their order.
-  for (int w = v; w < a.W; w += kDecideThreads / 64) {
-    Partial r;
-    r.sabs = r.sabs_c = r.sabs_b = r.ssq = 0.0;
-    r.nonfinite = 0;
+  if (a.W > kRowGroup) {
+    int parts = 1;
+    while (2 * parts * a.W <= kDecideThreads) parts *= 2;
+    const int t = threadIdx.x;
+    if (t < parts * a.W) {
+      const int w = t % a.W;
+      Partial r;
+      r.sabs = r.sabs_c = r.sabs_b = r.ssq = 0.0;
+      r.nonfinite = 0;
 #pragma unroll 8
-    for (int k = lane; k < used; k += 64) part_add<EXACT>(r, P[(int64_t)k * a.W + w]);
-    const XSum x1 = EXACT ? wave_xsum(XSum{r.sabs, r.sabs_c, r.sabs_b}) : XSum{wave_sum(r.sabs), 0.0, 0.0};
-    const double s2 = wave_sum(r.ssq);
-    const uint64_t nf = wave_sum_u64(r.nonfinite);
-    if (lane == 0) {
+      for (int k = t / a.W; k < used; k += parts) part_add<EXACT>(r, P[(int64_t)k * a.W + w]);
+      wide[t] = r;
+    }
+    __syncthreads();
+    if (t < a.W) {
+      Partial r = wide[t];
+      for (int p = 1; p < parts; ++p) part_add<EXACT>(r, wide[p * a.W + t]);
       double s1;
-      const bool certified = xround(x1, s1);
-      st[w].nonfinite = nf;
-      st[w].sum_abs_elig = s1;
-      st[w].sum_sq = s2;
-      redo[w] = EXACT && !certified;
+      const bool certified = xround(XSum{r.sabs, r.sabs_c, r.sabs_b}, s1);
+      st[t].nonfinite = r.nonfinite;
+      st[t].sum_abs_elig = s1;
+      st[t].sum_sq = r.ssq;
+      redo[t] = EXACT && !certified;
+    }
+  } else {
+    for (int w = v; w < a.W; w += kDecideThreads / 64) {
+      Partial r;
+      r.sabs = r.sabs_c = r.sabs_b = r.ssq = 0.0;
+      r.nonfinite = 0;
+#pragma unroll 8
+      for (int k = lane; k < used; k += 64) part_add<EXACT>(r, P[(int64_t)k * a.W + w]);
+      const XSum x1 = EXACT ? wave_xsum(XSum{r.sabs, r.sabs_c, r.sabs_b}) : XSum{wave_sum(r.sabs), 0.0, 0.0};
+      const double s2 = wave_sum(r.ssq);
+      const uint64_t nf = wave_sum_u64(r.nonfinite);
+      if (lane == 0) {
+        double s1;
+        const bool certified = xround(x1, s1);
+        st[w].nonfinite = nf;
+        st[w].sum_abs_elig = s1;
+        st[w].sum_sq = s2;
+        redo[w] = EXACT && !certified;
+      }
     }
   }
   if (v == 0) {
@@ -908,16 +949,17 @@ __global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
 // --------------------------------------------------------------- launchers
 
 template <bool PACK>
-static hipError_t pass1_dispatch(const Geometry& geo, const Pass1Args& a, hipStream_t s) {
+static hipError_t pass1_dispatch(const Geometry& geo, const Pass1Args& a0, hipStream_t s) {
   const dim3 block(kThreads1);
+  const int R = geo.rows;  // workers of the largest row group
   const int cw = geo.G * geo.eg * pass1_words(geo.wpw);
-  size_t smem = PACK ? (size_t)geo.W * cw * sizeof(uint64_t) : 0;
-  if (a.sums != kSumsNone) smem += (size_t)geo.W * geo.tile * sizeof(float);
+  size_t smem = PACK ? (size_t)R * cw * sizeof(uint64_t) : 0;
+  if (a0.sums != kSumsNone) smem += (size_t)R * geo.tile * sizeof(float);
   smem += (size_t)geo.G * geo.eg * pass1_words(geo.wpw) * sizeof(uint64_t);  // mask words of a mixed chunk
-  size_t red = (size_t)geo.eg * geo.W * sizeof(Partial) + (size_t)geo.eg * sizeof(uint64_t);
+  size_t red = (size_t)geo.eg * R * sizeof(Partial) + (size_t)geo.eg * sizeof(uint64_t);
   // routed chunks with several workers per wavefront: [kWaves][W] partials
-  if (geo.wpw > 1 && a.sums != kSumsNone && red < (size_t)kWaves * geo.W * sizeof(Partial))
-    red = (size_t)kWaves * geo.W * sizeof(Partial);
+  if (geo.wpw > 1 && a0.sums != kSumsNone && red < (size_t)kWaves * R * sizeof(Partial))
+    red = (size_t)kWaves * R * sizeof(Partial);
   if (smem < red) smem = red;
   if (smem > 65536) {
     // Above 64 KiB of dynamic LDS the kernel must opt in (gfx950 has 160 KiB per CU).
@@ -926,33 +968,46 @@ static hipError_t pass1_dispatch(const Geometry& geo, const Pass1Args& a, hipStr
       case 1: e = hipFuncSetAttribute((const void*)k_pass1<1, PACK>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem); break;
       case 2: e = hipFuncSetAttribute((const void*)k_pass1<2, PACK>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem); break;
       case 4: e = hipFuncSetAttribute((const void*)k_pass1<4, PACK>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem); break;
-      case 8: e = hipFuncSetAttribute((const void*)k_pass1<8, PACK>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem); break;
-      case 16: e = hipFuncSetAttribute((const void*)k_pass1<16, PACK>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem); break;
       default: return hipErrorInvalidValue;
     }
     if (e != hipSuccess) return e;
   }
-  // One launch per epoch of chunks (see the geometry notes).  The first
-  // launch is ordered after earlier work on the stream; later ones may
-  // start while the one before drains: every chunk writes only its own
-  // partial slot and sign words.  The next ordered launch (the decision)
-  // waits for all.
+  // One launch per epoch of chunks (see the geometry notes) and row group.
+  // The first launch is ordered after earlier work on the stream; later ones
+  // may start while the one before drains: every chunk writes only its own
+  // partial slots and sign words.  A later row group's first launch is
+  // ordered too when it continues the FP32 sums in the output.  The next
+  // ordered launch (the decision) waits for all.
   const uint32_t overlap = hipExtAnyOrderLaunch;
   const int64_t epoch = pass1_launch_chunks(geo, PACK);
-  for (int64_t q0 = 0; q0 < geo.total_chunks; q0 += epoch) {
-    const int64_t left = geo.total_chunks - q0;
-    const dim3 grid((unsigned)(left < epoch ? left : epoch));
-    const uint32_t fl = q0 > 0 ? overlap : 0u;
-    switch (geo.wpw) {
-      case 1: hipExtLaunchKernelGGL((k_pass1<1, PACK>), grid, block, smem, s, nullptr, nullptr, fl, a.g, a.mask, a.bits, a.out, a.part, a.part_ne, a, q0); break;
-      case 2: hipExtLaunchKernelGGL((k_pass1<2, PACK>), grid, block, smem, s, nullptr, nullptr, fl, a.g, a.mask, a.bits, a.out, a.part, a.part_ne, a, q0); break;
-      case 4: hipExtLaunchKernelGGL((k_pass1<4, PACK>), grid, block, smem, s, nullptr, nullptr, fl, a.g, a.mask, a.bits, a.out, a.part, a.part_ne, a, q0); break;
-      case 8: hipExtLaunchKernelGGL((k_pass1<8, PACK>), grid, block, smem, s, nullptr, nullptr, fl, a.g, a.mask, a.bits, a.out, a.part, a.part_ne, a, q0); break;
-      case 16: hipExtLaunchKernelGGL((k_pass1<16, PACK>), grid, block, smem, s, nullptr, nullptr, fl, a.g, a.mask, a.bits, a.out, a.part, a.part_ne, a, q0); break;
-      default: return hipErrorInvalidValue;
+  for (int grp = 0; grp < geo.ngroups; ++grp) {
+    Pass1Args a = a0;
+    int wb, rows;
+    row_group(geo, grp, &wb, &rows);
+    // every wavefront's first worker (wg < geo.wg) must be a row of the group
+    if (rows < geo.wg || rows > R) return hipErrorInvalidValue;
+    a.W = rows;
+    a.wtot = geo.W;
+    a.wbase = wb;
+    a.racc = grp > 0;
+    a.rfin = grp == geo.ngroups - 1;
+    a.g = a0.g + (int64_t)wb * a0.wstride;
+    if (a0.bits) a.bits = a0.bits + (int64_t)wb * a0.bstride;
+    a.part = a0.part + wb;
+    const bool chained = grp > 0 && a0.sums != kSumsNone;
+    for (int64_t q0 = 0; q0 < geo.total_chunks; q0 += epoch) {
+      const int64_t left = geo.total_chunks - q0;
+      const dim3 grid((unsigned)(left < epoch ? left : epoch));
+      const uint32_t fl = (q0 == 0 && (grp == 0 || chained)) ? 0u : overlap;
+      switch (geo.wpw) {
+        case 1: hipExtLaunchKernelGGL((k_pass1<1, PACK>), grid, block, smem, s, nullptr, nullptr, fl, a.g, a.mask, a.bits, a.out, a.part, a.part_ne, a, q0); break;
+        case 2: hipExtLaunchKernelGGL((k_pass1<2, PACK>), grid, block, smem, s, nullptr, nullptr, fl, a.g, a.mask, a.bits, a.out, a.part, a.part_ne, a, q0); break;
+        case 4: hipExtLaunchKernelGGL((k_pass1<4, PACK>), grid, block, smem, s, nullptr, nullptr, fl, a.g, a.mask, a.bits, a.out, a.part, a.part_ne, a, q0); break;
+        default: return hipErrorInvalidValue;
+      }
+      const hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
     }
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
   }
   return hipSuccess;
 }

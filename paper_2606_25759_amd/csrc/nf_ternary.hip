@@ -51,23 +51,30 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
   const int64_t te = (tb + a.G < ntiles) ? tb + a.G : ntiles;
   const int64_t te_full = (te * tile <= nbe) ? te : te - 1;  // tiles [tb, te_full) are full
   const int cw = a.G * a.eg * NW;                             // words per worker row and chunk
+  // This launch's rows: workers wbase .. wbase + R - 1; w below is a row of
+  // the group, and the planes of the group's rows start at pbits (positive)
+  // and nbits (negative).
+  const int R = a.rows;
+  const float* g = a.g + (int64_t)a.wbase * a.wstride;
+  uint64_t* pbits = a.bits + (int64_t)a.wbase * a.bstride;
+  uint64_t* nbits = a.bits + (int64_t)(a.W + a.wbase) * a.bstride;
   uint64_t* ppos = reinterpret_cast<uint64_t*>(smem);
-  uint64_t* pneg = ppos + (size_t)a.W * cw;
+  uint64_t* pneg = ppos + (size_t)R * cw;
 
   float th[WPW];
   const float* rp[WPW];
 #pragma unroll
   for (int j = 0; j < WPW; ++j) {
     const int w = wg + j * a.wg;
-    const int wl = w < a.W ? w : wg;
-    th[j] = a.dec ? ternary_threshold(a.stats[(int64_t)b * a.W + wl], a.dec[b].n_eligible, a.tau)
-                  : a.theta[wl];
-    rp[j] = a.g + (int64_t)wl * a.wstride + base + (int64_t)eg * T + lane;
+    const int wl = w < R ? w : wg;
+    th[j] = a.dec ? ternary_threshold(a.stats[(int64_t)b * a.W + a.wbase + wl], a.dec[b].n_eligible, a.tau)
+                  : a.theta[a.wbase + wl];
+    rp[j] = g + (int64_t)wl * a.wstride + base + (int64_t)eg * T + lane;
   }
   const uint64_t* mbase = a.mask + base / 64 + (int64_t)eg * (T / 64);
   // The first NW words of the bucket's first tile (full whenever any tile of
   // this chunk is): read by loads whose values are not needed.
-  const float* dp = a.g + (int64_t)wg * a.wstride + base + lane;
+  const float* dp = g + (int64_t)wg * a.wstride + base + lane;
   const uint64_t* dm = a.mask + base / 64;
 
   bool chunk_all = false, chunk_any = true;  // set below, after the first tile's loads are out
@@ -106,7 +113,7 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
 #pragma unroll
     for (int j = 0; j < WPW; ++j) {
       const int w = wg + j * a.wg;
-      if (j > 0 && w >= a.W) continue;
+      if (j > 0 && w >= R) continue;
       uint64_t pb[NW], nb[NW];
 #pragma unroll
       for (int k = 0; k < NW; ++k) {
@@ -155,11 +162,11 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
       const int64_t cn = ((te * tile < nbe) ? te * tile : nbe) - tb * tile;
       const int nwc = cn > 0 ? (int)((cn + 63) / 64) : 0;
       const int64_t gz = (base + tb * tile) / 64;
-      for (int i = threadIdx.x; i < a.W * nwc; i += kThreads1) {
+      for (int i = threadIdx.x; i < R * nwc; i += kThreads1) {
         const int w = i / nwc;
         const int o = i - w * nwc;
-        a.bits[(int64_t)w * a.bstride + gz + o] = 0ull;
-        a.bits[(int64_t)(a.W + w) * a.bstride + gz + o] = 0ull;
+        pbits[(int64_t)w * a.bstride + gz + o] = 0ull;
+        nbits[(int64_t)w * a.bstride + gz + o] = 0ull;
       }
       return;
     }
@@ -210,20 +217,20 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
 #pragma unroll
     for (int j = 0; j < WPW; ++j) {
       const int w = wg + j * a.wg;
-      if (w >= a.W) break;
+      if (w >= R) break;
       for (int o = lane; o < valid; o += 64) {
-        a.bits[(int64_t)w * a.bstride + gw0 + o] = ppos[w * cw + o];
-        a.bits[(int64_t)(a.W + w) * a.bstride + gw0 + o] = pneg[w * cw + o];
+        pbits[(int64_t)w * a.bstride + gw0 + o] = ppos[w * cw + o];
+        nbits[(int64_t)w * a.bstride + gw0 + o] = pneg[w * cw + o];
       }
     }
     return;
   }
   __syncthreads();
-  for (int i = threadIdx.x; i < a.W * valid; i += kThreads1) {
+  for (int i = threadIdx.x; i < R * valid; i += kThreads1) {
     const int w = i / valid;
     const int o = i - w * valid;
-    a.bits[(int64_t)w * a.bstride + gw0 + o] = ppos[w * cw + o];
-    a.bits[(int64_t)(a.W + w) * a.bstride + gw0 + o] = pneg[w * cw + o];
+    pbits[(int64_t)w * a.bstride + gw0 + o] = ppos[w * cw + o];
+    nbits[(int64_t)w * a.bstride + gw0 + o] = pneg[w * cw + o];
   }
 }
 
@@ -358,26 +365,29 @@ hipError_t launch_ternary_pack(const Geometry& geo, const TernArgs& a0, hipStrea
   a.eg = geo.eg;
   a.T = geo.T;
   a.G = geo.G;
-  // Both planes of a chunk: 2 * W * G * EG * (T / 64) words, at most 64 KiB.
-  const size_t smem = 2 * (size_t)geo.W * geo.G * geo.eg * pass1_words(geo.wpw) * sizeof(uint64_t);
+  // Both planes of a chunk: 2 * R * G * EG * (T / 64) words, at most 64 KiB.
+  const size_t smem = 2 * (size_t)geo.rows * geo.G * geo.eg * pass1_words(geo.wpw) * sizeof(uint64_t);
   if (smem > 65536) return hipErrorInvalidValue;
-  // No chunk shares state with another, so every launch after the first may
-  // start while the one before drains.
+  // No chunk or row group shares state with another, so every launch after
+  // the first may start while the one before drains.
   const int64_t epoch = one_launch_epoch(geo.total_chunks);  // chunks share no state here
-  for (int64_t q0 = 0; q0 < geo.total_chunks; q0 += epoch) {
-    const int64_t left = geo.total_chunks - q0;
-    const dim3 grid((unsigned)(left < epoch ? left : epoch));
-    const uint32_t fl = q0 > 0 ? hipExtAnyOrderLaunch : 0u;
-    switch (geo.wpw) {
-      case 1: hipExtLaunchKernelGGL((k_tpack<1>), grid, dim3(kThreads1), smem, s, nullptr, nullptr, fl, a, q0); break;
-      case 2: hipExtLaunchKernelGGL((k_tpack<2>), grid, dim3(kThreads1), smem, s, nullptr, nullptr, fl, a, q0); break;
-      case 4: hipExtLaunchKernelGGL((k_tpack<4>), grid, dim3(kThreads1), smem, s, nullptr, nullptr, fl, a, q0); break;
-      case 8: hipExtLaunchKernelGGL((k_tpack<8>), grid, dim3(kThreads1), smem, s, nullptr, nullptr, fl, a, q0); break;
-      case 16: hipExtLaunchKernelGGL((k_tpack<16>), grid, dim3(kThreads1), smem, s, nullptr, nullptr, fl, a, q0); break;
-      default: return hipErrorInvalidValue;
+  for (int grp = 0; grp < geo.ngroups; ++grp) {
+    row_group(geo, grp, &a.wbase, &a.rows);
+    // every wavefront's first worker (wg < geo.wg) must be a row of the group
+    if (a.rows < geo.wg || a.rows > geo.rows) return hipErrorInvalidValue;
+    for (int64_t q0 = 0; q0 < geo.total_chunks; q0 += epoch) {
+      const int64_t left = geo.total_chunks - q0;
+      const dim3 grid((unsigned)(left < epoch ? left : epoch));
+      const uint32_t fl = (q0 > 0 || grp > 0) ? hipExtAnyOrderLaunch : 0u;
+      switch (geo.wpw) {
+        case 1: hipExtLaunchKernelGGL((k_tpack<1>), grid, dim3(kThreads1), smem, s, nullptr, nullptr, fl, a, q0); break;
+        case 2: hipExtLaunchKernelGGL((k_tpack<2>), grid, dim3(kThreads1), smem, s, nullptr, nullptr, fl, a, q0); break;
+        case 4: hipExtLaunchKernelGGL((k_tpack<4>), grid, dim3(kThreads1), smem, s, nullptr, nullptr, fl, a, q0); break;
+        default: return hipErrorInvalidValue;
+      }
+      const hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
     }
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
   }
   return hipSuccess;
 }

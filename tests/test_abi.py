@@ -254,6 +254,13 @@ def test_pass1_chunk_geometry():
     assert nf.nf_pass1_chunk_elems(16, 6_553_600 * 201, 6_553_600) == (16_384, 400)
     # W = 64: four workers per wavefront, tiles of 256 elements, 16 per chunk
     assert nf.nf_pass1_chunk_elems(64, 100_000_000, 100_000_000) == (4_096, 24_415)
+    # W > 64: rows in ceil(W / 64) near-equal groups, with the geometry of the
+    # largest (255: four of 64 or 63 rows; 65: 33 and 32 rows, tiles of 256
+    # elements, 31 per chunk)
+    assert nf.nf_pass1_chunk_elems(255, 6_553_600 * 2, 6_553_600) == (4_096, 1_600)
+    assert nf.nf_pass1_chunk_elems(65, 6_553_600 * 2, 6_553_600) == (7_936, 826)
+    assert nf.nf_pass1_launches(255, 6_553_600 * 2, 6_553_600) == 4 * 13  # 3,200 chunks, 256 per launch
+    assert nf.nf_pass1_launches(65, 6_553_600 * 2, 6_553_600) == 2 * 7
     # a small problem takes shorter chunks to fill the chip (at most 1,024 chunks)
     e, c = nf.nf_pass1_chunk_elems(4, 1 << 20, 1 << 20)
     assert c <= 1024 and e * c >= 1 << 20 and e % 64 == 0
@@ -272,6 +279,11 @@ def test_workspace_sizes():
     b = nf.nf_workspace_bytes_buckets(16, 6_553_600 * 201, 6_553_600)
     assert b == 51_456_000 + 643_328
     assert nf.nf_workspace_bytes_buckets(16, 100, 0) == 0
+    # W = 255, two 25 MiB buckets: 1,600 chunk slots each, summed first in
+    # 64 groups of 25 (the decision reads at most 64 partials per worker above
+    # 64 workers).
+    c = nf.nf_workspace_bytes_buckets(255, 6_553_600 * 2, 6_553_600)
+    assert c == 2 * 1_600 * 255 * 40 + 25_600 + 2 * 64 * 255 * 40 + 1_024
 
 
 def declared_prototypes():

@@ -2,9 +2,9 @@
 `bench.py --format ternary`: one nf_route_buckets call over the whole
 stacked buffer, inputs generated on the device.
 
-Nothing is sampled.  GPT-1.3B scale: all 201 buckets checked in full against
-the oracle's ternary whole bucket (a pool of threads, one bucket copied to
-the host at a time).  Stress (W = 64, one 100M-element bucket, forced
+Nothing is sampled.  GPT-1.3B scale (and the W = 255 fan-in pair): every
+bucket checked in full against the oracle's ternary whole bucket (a pool of
+threads, one bucket copied to the host at a time).  Stress (W = 64, one 100M-element bucket, forced
 low-bit): statistics per worker row over every element, the thresholds from
 them, then the oracle's element-wise steps (planes, c+ and c-, FP32 path,
 output) over consecutive ranges covering the bucket, every word and value
@@ -76,6 +76,18 @@ def test_fullsize_ternary_gpt1p3b_every_bucket():
             routes = np.array(list(ex.map(f.check_bucket, range(f.nb))))
         assert (routes[:185] == nfo.ROUTE_L).all() and (routes[185:] == nfo.ROUTE_P).all(), routes
         print(f"[fullsize-ternary] gpt1p3b: {f.nb} buckets checked", flush=True)
+    finally:
+        f.release()
+
+
+def test_fullsize_ternary_fanin255_every_bucket():
+    """W = 255 (four groups of worker rows in the first pass and the plane
+    pack): both buckets in full."""
+    f = FullTernary("fanin255", nf.policy(format=nf.NF_FORMAT_TERNARY, tau=0.5))
+    try:
+        with ThreadPoolExecutor(POOL) as ex:
+            routes = list(ex.map(f.check_bucket, range(f.nb)))
+        assert all(r == nfo.ROUTE_L for r in routes), routes
     finally:
         f.release()
 

@@ -1,6 +1,6 @@
 """Pass-1 launch shapes against the oracle: a bucket small enough for one
-launch, buckets of more than 512 chunks (their per-chunk partials are summed
-in groups before the decision), in one launch and in several launches that
+launch, buckets of more than 512 chunks (64 above 64 workers: their
+per-chunk partials are summed in groups before the decision), in one launch and in several launches that
 may overlap, and a flat buffer of several buckets in one launch.  Every
 output of every bucket is checked (G-Binary and G-Ternary)."""
 import numpy as np
@@ -54,7 +54,8 @@ def run_binary(W, n, bucket_n, seed):
     (16, 20_000_000, 20_000_000, 5, 2),    # 1,221 chunks of 32 tiles: five launches, groups of 3
     (16, 20_000_000, 9_000_000, 5, 2),     # three buckets, the last of 123 chunks
     (64, 3_000_000, 3_000_000, 1, 1),      # 977 chunks, four workers per wavefront
-    (255, 600_000, 600_000, 1, 1),         # 938 chunks, one thread per worker in the groups
+    (255, 600_000, 600_000, 4, 4),         # 782 chunks, one launch per group of 64 worker rows;
+                                           # partials summed in groups of 13 (at most 64 per worker)
     (16, 1_000_000, 1_000_000, 1, 1),      # 977 chunks of 2 tiles
     (8, 6_000_000, 1_310_720, 1, 1),       # five buckets of at most 214 chunks: partials read directly
 ])

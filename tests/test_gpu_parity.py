@@ -179,6 +179,37 @@ def test_route_bucket_large(W):
     H.check_route(res, g, _clean_mask(m, n), n, pol, what=f"W={W} n={n}")
 
 
+@pytest.mark.parametrize("W", [65, 128, 129, 200])
+@pytest.mark.parametrize("kind", ["default", "veto_mean", "forced_mean"])
+def test_route_row_groups(W, kind):
+    """Above 64 workers pass 1 reads the worker rows in groups of 64, the
+    FP32 sums at routed positions carried from one group to the next in the
+    output.  Two buckets: the first clean, the second with a NaN and an
+    infinity at routed positions in different groups and a routed position
+    whose FP32 sum overflows only after the first group (every worker
+    3e38).  Policies: the fused route, a vetoed route (FP32 sums over every
+    element, no sign words, exact |g| sums) and forced low-bit, the last two
+    with the FP32 mean (divided once, after the last group)."""
+    n, bn = 300_007, 150_016
+    g = _grads(W, n, 800 + W)
+    el = np.random.default_rng(801 + W).random(n) < 0.8  # element-wise: routed positions in every chunk
+    m = np.packbits(np.concatenate([el, np.zeros((-n) % 64, bool)]), bitorder="little").view(np.uint64).copy()
+    routed = np.nonzero(~el)[0]
+    routed = routed[routed >= bn]
+    g[70 % W, routed[10]] = np.nan
+    g[W - 1, routed[20]] = np.inf
+    g[:, routed[30]] = np.float32(3e38)
+    pol = {"default": nf.policy(),
+           "veto_mean": nf.policy(veto=1, fp32_op=nf.NF_FP32_MEAN),
+           "forced_mean": nf.policy(force_lowbit=1, fp32_op=nf.NF_FP32_MEAN)}[kind]
+    run = H.Bucket(g, m, n, bucket_n=bn)
+    res = run.route(pol)
+    H.check_route(res, g, m, n, pol, bucket_n=bn, what=f"W={W} {kind}")
+    if kind == "default":
+        assert int(res["dec"][0]["route"]) == nfo.ROUTE_L
+    assert np.isinf(res["out"][routed[30]])
+
+
 @pytest.mark.parametrize("admitted,veto,guard_ok,force", [(a, v, gk, f) for a in (0, 1) for v in (0, 1)
                                                           for gk in (0, 1) for f in (0, 1)])
 @pytest.mark.parametrize("mode,op", [(nf.NF_DECODE_SOFT, nf.NF_FP32_SUM),

@@ -37,7 +37,7 @@ def unpack(words, n):
                          axis=-1)[..., :n]
 
 
-@pytest.mark.parametrize("W", [1, 2, 3, 8, 16, 64, 255])
+@pytest.mark.parametrize("W", [1, 2, 3, 8, 16, 64, 65, 255])
 @pytest.mark.parametrize("n", [1, 63, 64, 65, 4095, 65537])
 def test_pack_ternary_matches_oracle(W, n):
     g, mask = layout(W, n, 1000 * W + n, special=True)
@@ -55,7 +55,7 @@ def test_pack_ternary_matches_oracle(W, n):
     assert np.all(b[:, nw:] == np.uint64(0xFFFFFFFFFFFFFFFF)), "words past the end untouched"
 
 
-@pytest.mark.parametrize("W", [1, 3, 16, 64, 255])
+@pytest.mark.parametrize("W", [1, 3, 16, 64, 129, 255])
 @pytest.mark.parametrize("n", [1, 65, 4097, 100_003])
 @pytest.mark.parametrize("mode", [nfo.DECODE_SOFT, nfo.DECODE_MAJORITY])
 def test_ternary_reduce_matches_oracle(W, n, mode):
