@@ -323,22 +323,23 @@ NF_HD inline float bucket_scale(const nf_worker_stats* st, int W, int64_t ne) {
 
 NF_HD inline bool finite64(double x) { return x - x == 0.0; }
 
-NF_HD inline void decide_from(const nf_worker_stats* st, int W, int64_t n, int64_t ne,
-                              const nf_route_policy& p, int kfinite, double median,
-                              nf_route_decision* d) {
+// Norm-spike threshold: kappa^2 times the lower median of the finite sums
+// of squares; a worker spikes when its finite sum of squares exceeds it (with
+// at least two finite sums).
+NF_HD inline double spike_threshold(const nf_route_policy& p, double median) {
+  return (p.kappa * p.kappa) * median;
+}
+
+// Route, reasons, scale and modeled bytes of a bucket from its per-worker
+// findings: a non-finite value in some worker, a worker whose eligible |g|
+// sum is 0, a norm spike.
+NF_HD inline void decide_finish(int64_t n, int64_t ne, const nf_route_policy& p, bool nonf, bool zero,
+                                bool spike, float scale, nf_route_decision* d) {
   uint32_t r = 0;
   if (!p.admitted) r |= NF_REASON_NOT_ADMITTED;
   if (ne == 0) r |= NF_REASON_NO_ELIGIBLE;
   if (p.veto) r |= NF_REASON_VETO;
   if (!p.guard_ok) r |= NF_REASON_GUARD;
-  uint64_t nonf = 0;
-  bool zero = false, spike = false;
-  double thr = (p.kappa * p.kappa) * median;
-  for (int w = 0; w < W; ++w) {
-    nonf += st[w].nonfinite;
-    if (st[w].sum_abs_elig == 0.0) zero = true;
-    if (kfinite >= 2 && finite64(st[w].sum_sq) && st[w].sum_sq > thr) spike = true;
-  }
   if (nonf) r |= NF_REASON_NONFINITE;
   if (zero && ne > 0) r |= NF_REASON_ZERO_WORKER;
   if (spike) r |= NF_REASON_NORM_SPIKE;
@@ -356,7 +357,7 @@ NF_HD inline void decide_from(const nf_worker_stats* st, int W, int64_t n, int64
   }
   d->route = route;
   d->reasons = r;
-  d->scale = bucket_scale(st, W, ne);
+  d->scale = scale;
   d->resummed = 0;
   d->n_eligible = ne;
   d->bytes_fp32 = 4.0 * (double)n;
@@ -365,6 +366,22 @@ NF_HD inline void decide_from(const nf_worker_stats* st, int W, int64_t n, int64
                        ? (p.format == NF_FORMAT_TERNARY ? 2.0 : 1.0) * (double)ne / 8.0 + 4.0 +
                              4.0 * (double)(n - ne)
                        : 4.0 * (double)n;
+}
+
+// The same from the statistics, one worker after another (the host's
+// decision; the device kernel finds the per-worker facts in parallel).
+NF_HD inline void decide_from(const nf_worker_stats* st, int W, int64_t n, int64_t ne,
+                              const nf_route_policy& p, int kfinite, double median,
+                              nf_route_decision* d) {
+  uint64_t nonf = 0;
+  bool zero = false, spike = false;
+  const double thr = spike_threshold(p, median);
+  for (int w = 0; w < W; ++w) {
+    nonf += st[w].nonfinite;
+    if (st[w].sum_abs_elig == 0.0) zero = true;
+    if (kfinite >= 2 && finite64(st[w].sum_sq) && st[w].sum_sq > thr) spike = true;
+  }
+  decide_finish(n, ne, p, nonf != 0, zero, spike, bucket_scale(st, W, ne), d);
 }
 
 // G-Ternary write-side threshold: tau times the worker's mean |g| over
