@@ -17,6 +17,11 @@ fraction of the 8 TB/s HBM peak.  The JSON line also carries
   cpu_baseline  the oracle, single-threaded on one pinned host core, on a
                 bounded sample of the same workload
   achievable    a plain streaming read of the same input (reference rate)
+  configs       (default run) every other workload: G-Ternary at GPT scale,
+                ViT-B/16 and ResNet-50 scale, the tiny bucket, the stress
+                bucket, the W = 255 pair; each with its pass-1 roofline
+                (`traffic` from that workload's committed counters) and the
+                counter bytes per dispatch of every kernel of its step
 
   python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload gpt1p3b]
   python bench.py --calibrate-copy     (copy kernel of known size, for counters)
@@ -764,7 +769,11 @@ def config_record(wl, m, pol, cold, cpu, counters):
     row.update({k: m[k] for k in ("value", "pct_hbm_peak", "ms_per_step", "steps", "device_ms", "phases_ms",
                                   "routes", "mgtr")})
     row["unit"] = "GB/s"
-    row["roofline_pass1"] = m["pass1"]
+    roof = dict(m["pass1"])
+    roof["traffic"] = pass1_traffic(counters)
+    roof["traffic_gbs"] = (None if roof["traffic"] is None else
+                           round(roof["traffic"] / (roof["avg_launch_ms"] * 1e-3) / 1e9, 1))
+    row["roofline_pass1"] = roof
     row["cpu_baseline"] = cpu
     row["counter_bytes"] = counters
     return row
@@ -783,12 +792,24 @@ def committed_counters(workload, fmt):
     return rec.get("kernels")
 
 
+def pass1_traffic(counters):
+    """HBM bytes per pass-1 launch in a workload's committed counters (the
+    pass-1 instantiation the step ran), or None."""
+    if not counters:
+        return None
+    names = [k for k in counters if k.startswith("k_pass1<")]
+    if not names:
+        return None
+    return counters[max(names, key=lambda k: counters[k]["dispatches"])]["hbm_bytes_per_dispatch"]
+
+
 def sweep_configs(nf, torch, gpt, args):
     """Every workload of the sweep after the headline: G-Ternary on the same
     GPT-scale buffer, then ViT-B/16 scale, ResNet-50 scale, the tiny bucket
     (warm and cold caches), the stress bucket (route F, forced low-bit,
-    forced low-bit G-Ternary) and the W = 255 fan-in bucket pair.  Each row
-    is a few timed steps and a bounded oracle sample."""
+    forced low-bit G-Ternary) and the W = 255 fan-in bucket pair (G-Binary
+    and G-Ternary).  Each row is a few timed steps and a bounded oracle
+    sample."""
     rows = []
     tern = nf.policy(format=nf.NF_FORMAT_TERNARY, tau=args.tau)
     m = gpt.measure(tern, 10, 2)
@@ -800,7 +821,8 @@ def sweep_configs(nf, torch, gpt, args):
             ("tiny", [(nf.policy(), False, 200), (nf.policy(), True, 50)]),
             ("stress", [(nf.policy(), False, 10), (nf.policy(force_lowbit=1), False, 10),
                         (nf.policy(force_lowbit=1, format=nf.NF_FORMAT_TERNARY, tau=args.tau), False, 10)]),
-            ("fanin255", [(nf.policy(), False, 10)])]
+            ("fanin255", [(nf.policy(), False, 10),
+                          (nf.policy(format=nf.NF_FORMAT_TERNARY, tau=args.tau), False, 10)])]
     for name, runs in plan:
         wl = Workload(nf, torch, name, planes=2 if any(p.format for p, _, _ in runs) else 1)
         for pol, cold, steps in runs:
