@@ -18,7 +18,7 @@ fraction of the 8 TB/s HBM peak.  The JSON line also carries
                 bounded sample of the same workload
   achievable    a plain streaming read of the same input (reference rate)
   configs       (default run) every other workload: G-Ternary at GPT scale,
-                ViT-B/16 and ResNet-50 scale, the tiny bucket, the stress
+                GPT scale in DDP's buckets, ViT-B/16 and ResNet-50 scale, the tiny bucket, the stress
                 bucket, the W = 255 pair; each with its pass-1 roofline
                 (`traffic` from that workload's committed counters) and the
                 counter bytes per dispatch of every kernel of its step
@@ -51,6 +51,9 @@ def parse():
                     help="measure this workload only (default: the GPT-1.3B-scale headline, then a few "
                          "steps of every other workload in the JSON line's `configs`)")
     ap.add_argument("--force-lowbit", action="store_true", help="guard disabled (forced low-bit)")
+    ap.add_argument("--ddp-buckets", action="store_true",
+                    help="buckets cut as DDP cuts the model (25 MiB capacity, closed at tensor boundaries) "
+                         "through the bucket-table driver, instead of equal 25 MiB buckets")
     ap.add_argument("--no-counts", action="store_true", help="do not write the uint8 counts")
     ap.add_argument("--cold", action="store_true",
                     help="overwrite 1 GiB before every step so the caches hold none of the input; value "
@@ -421,19 +424,19 @@ def split_one_bucket(nf, torch, grads, mask, W, n, n_e, reps=10):
 
 class Workload:
     """One workload's device buffers, generated once, and measurements of
-    nf_route_buckets over all of its buckets under a given policy."""
+    one driver call over all of its buckets under a given policy: equal
+    buckets (nf_route_buckets) or, after set_buckets(offsets), the buckets of
+    a bucket table (nf_route_bucket_table)."""
 
-    def __init__(self, nf, torch, name, planes=1):
+    def __init__(self, nf, torch, name, planes=1, ddp=False):
         import numpy as np
         import synth
         self.nf, self.torch, self.np = nf, torch, np
         self.dev = torch.device("cuda:0")
         self.lay = lay = synth.CONFIGS[name]()
-        self.W, self.n, self.bn, self.nb = lay.W, lay.n_total, lay.bucket_n, lay.nb
-        W, n, nb = self.W, self.n, self.nb
+        self.W, self.n = lay.W, lay.n_total
+        W, n = self.W, self.n
         self.nw = (n + 63) // 64
-        print(f"[bench] {lay.name}: W={W} n={n:,} buckets={nb} bucket_n={self.bn:,} "
-              f"input={lay.input_bytes() / 1e9:.2f} GB", file=sys.stderr, flush=True)
         self.grads = torch.empty((W, lay.stride), dtype=torch.float32, device=self.dev)
         synth.generate_device(lay, self.grads)
         self.segs = synth.mask_segments(lay)
@@ -443,27 +446,63 @@ class Workload:
         self.bits = torch.empty((planes * W, self.nw), dtype=torch.int64, device=self.dev)
         self.counts = torch.empty(planes * n, dtype=torch.uint8, device=self.dev)
         self.out = torch.empty(n, dtype=torch.float32, device=self.dev)
-        self.stats = torch.empty(nb * W * nf.STATS_BYTES, dtype=torch.uint8, device=self.dev)
-        self.dec = torch.empty(nb * nf.DECISION_BYTES, dtype=torch.uint8, device=self.dev)
-        self.ws = nf.empty_workspace(nf.nf_workspace_bytes_buckets(W, n, self.bn), self.dev)
-        torch.cuda.synchronize()
+        self.set_buckets(synth.ddp_offsets(lay) if ddp else None)
         print("[bench] inputs resident", file=sys.stderr, flush=True)
 
+    def set_buckets(self, off=None):
+        """Equal buckets of the layout's bucket_n (off None), or the buckets
+        [off[b], off[b+1]) through a device bucket table."""
+        nf, torch, np = self.nf, self.torch, self.np
+        W, n, lay = self.W, self.n, self.lay
+        self.table = self.stats = self.dec = self.ws = None
+        if off is None:
+            self.bn = lay.bucket_n
+            self.off = np.array(list(range(0, n, self.bn)) + [n], np.int64)
+            ws = nf.nf_workspace_bytes_buckets(W, n, self.bn)
+        else:
+            self.bn = None
+            self.off = np.asarray(off, np.int64)
+            self.table = torch.empty(nf.nf_bucket_table_bytes(W, self.off), dtype=torch.uint8, device=self.dev)
+            nf.nf_bucket_table_init(W, self.off, self.table)
+            ws = nf.nf_workspace_bytes_table(W, self.off)
+        self.nb = nb = len(self.off) - 1
+        self.stats = torch.empty(nb * W * nf.STATS_BYTES, dtype=torch.uint8, device=self.dev)
+        self.dec = torch.empty(nb * nf.DECISION_BYTES, dtype=torch.uint8, device=self.dev)
+        self.ws = nf.empty_workspace(ws, self.dev)
+        torch.cuda.synchronize()
+        sizes = np.diff(self.off)
+        print(f"[bench] {lay.name}: W={W} n={n:,} buckets={nb} "
+              + (f"bucket_n={self.bn:,}" if self.bn else f"DDP cut, {sizes.min():,} to {sizes.max():,} elements")
+              + f" input={lay.input_bytes() / 1e9:.2f} GB", file=sys.stderr, flush=True)
+
+    def buckets_desc(self):
+        """The config's bucket fields: equal buckets or the DDP cut."""
+        if self.bn:
+            return {"buckets": self.nb, "bucket_n": self.bn}
+        sizes = self.np.diff(self.off)
+        return {"buckets": self.nb, "bucket_n": None,
+                "bucket_cut": f"DDP: 25 MiB capacity (first bucket 1 MiB), closed at tensor boundaries; "
+                              f"{int(sizes.min()):,} to {int(sizes.max()):,} elements"}
+
     def release(self):
-        del self.grads, self.mask, self.bits, self.counts, self.out, self.stats, self.dec, self.ws
+        del self.grads, self.mask, self.bits, self.counts, self.out, self.stats, self.dec, self.ws, self.table
         self.torch.cuda.synchronize()
         self.torch.cuda.empty_cache()
 
     def step(self, pol, counts=True):
         ternary = pol.format == self.nf.NF_FORMAT_TERNARY
         cnt = self.counts[: (2 if ternary else 1) * self.n] if counts else None
-        self.nf.nf_route_buckets(self.grads, self.n, self.bn, self.mask, pol, self.bits, cnt, self.out,
-                                 self.stats, self.dec, self.ws)
+        if self.table is not None:
+            self.nf.nf_route_bucket_table(self.grads, self.off, self.table, self.mask, pol, self.bits, cnt,
+                                          self.out, self.stats, self.dec, self.ws)
+        else:
+            self.nf.nf_route_buckets(self.grads, self.n, self.bn, self.mask, pol, self.bits, cnt, self.out,
+                                     self.stats, self.dec, self.ws)
 
     def measure(self, pol, steps, warmup, cold=False, counts=True):
         """Wall and device time of `steps` steps; algorithmic bytes and rates per phase."""
         nf, torch, np = self.nf, self.torch, self.np
-        W, n, bn, nb = self.W, self.n, self.bn, self.nb
+        W, n, nb = self.W, self.n, self.nb
         ternary = pol.format == nf.NF_FORMAT_TERNARY
         for _ in range(warmup):
             self.step(pol, counts)
@@ -493,7 +532,7 @@ class Workload:
         d = nf.decisions_host(self.dec, nb)
         routes = {"L": int((d["route"] == 0).sum()), "F": int((d["route"] == 1).sum()),
                   "P": int((d["route"] == 2).sum())}
-        nbs = np.array([min(bn, n - b * bn) for b in range(nb)], dtype=np.int64)
+        nbs = np.diff(self.off)
         ne = d["n_eligible"].astype(np.int64)
         nwb = (nbs + 63) // 64
         # pass 1: gradients once, mask once, sign words out (G-Binary only), FP32 sums at routed positions out
@@ -506,12 +545,14 @@ class Workload:
         else:
             l_bytes = 8 * W * nwb + 8 * nwb + cbytes + 4 * ne
         pass2_bytes = float((l_bytes * is_l).sum() + ((4 * W * ne + 8 * nwb + 4 * ne) * is_f).sum())
-        launches = nf.nf_pass1_launches(W, n, bn, sign_words=not ternary)
+        launches = (nf.nf_pass1_launches(W, n, self.bn, sign_words=not ternary) if self.bn else
+                    nf.nf_pass1_launches_table(W, self.off, sign_words=not ternary))
         # a cold run's wall clock includes the overwrites: its value comes from the device events
         value = self.lay.input_bytes() / ((device_ms if cold else ms_per_step) * 1e-3) / 1e9
         achieved = pass1_bytes / (pass1_ms * 1e-3) / 1e9
         print(f"[bench] {self.lay.name} {'ternary' if ternary else 'binary'}"
-              f"{' forced' if pol.force_lowbit else ''}{' cold' if cold else ''}: {steps} steps, "
+              f"{' forced' if pol.force_lowbit else ''}{' cold' if cold else ''}"
+              f"{'' if self.bn else ' DDP buckets'}: {steps} steps, "
               f"{ms_per_step:.4f} ms/step wall, device {device_ms:.4f} (pass1 {pass1_ms:.4f}, decide "
               f"{decide_ms:.4f}, pass2 {pass2_ms:.4f}), {value:.1f} GB/s", file=sys.stderr, flush=True)
         return {
@@ -537,7 +578,7 @@ class Workload:
         against the GPU's on the sample."""
         import oracle as nfo
         nf, np = self.nf, self.np
-        W, n, bn, nb = self.W, self.n, self.bn, self.nb
+        W, n, nb, off = self.W, self.n, self.nb, self.off
         ternary = pol.format == nf.NF_FORMAT_TERNARY
         opol = nfo.policy(admitted=pol.admitted, veto=pol.veto, guard_ok=pol.guard_ok,
                           force_lowbit=pol.force_lowbit, decode_mode=pol.decode_mode, fp32_op=pol.fp32_op,
@@ -551,8 +592,11 @@ class Workload:
             span = max(64, int(rate_guess * seconds / (4 * W)) // 64 * 64)
             ranges = [(0, min(span, n))]
         else:
-            k = max(1, min(nb, int(rate_guess * seconds / (4 * W * min(bn, n)))))
-            ranges = [(b * bn, min((b + 1) * bn, n)) for b in range(k)]
+            # leading buckets while they fit the budget (at least one)
+            k = 1
+            while k < nb and 4 * W * (off[k + 1] - off[0]) <= rate_guess * seconds:
+                k += 1
+            ranges = [(int(off[b]), int(off[b + 1])) for b in range(k)]
         model, ncpu = host_cpu()
         old_aff = os.sched_getaffinity(0)
         core = min(old_aff)
@@ -575,7 +619,7 @@ class Workload:
         finally:
             os.sched_setaffinity(0, old_aff)
         what = (f"elements 0..{ranges[0][1] - 1} of the one bucket, reduced as a bucket of their own"
-                if one_bucket else f"buckets 0..{len(ranges) - 1} ({len(ranges)} x {min(bn, n):,} elements)")
+                if one_bucket else f"buckets 0..{len(ranges) - 1} ({off[len(ranges)] - off[0]:,} elements)")
         if reps > 1:
             what += f", reduced {reps} times"
         rec = {"value": round(nbytes / t_cpu / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
@@ -692,12 +736,12 @@ def main():
     ternary = args.format == "ternary"
     pol = nf.policy(force_lowbit=int(args.force_lowbit), format=int(ternary), tau=args.tau)
     # the headline workload, with room for the G-Ternary planes when the sweep measures them too
-    wl = Workload(nf, torch, name, planes=2 if (ternary or sweep) else 1)
+    wl = Workload(nf, torch, name, planes=2 if (ternary or sweep) else 1, ddp=args.ddp_buckets)
     m = wl.measure(pol, args.steps, args.warmup, cold=args.cold, counts=not args.no_counts)
 
     split = None
     if not ternary and not args.no_split:
-        split = split_one_bucket(nf, torch, wl.grads, wl.mask, wl.W, min(wl.bn, wl.n),
+        split = split_one_bucket(nf, torch, wl.grads, wl.mask, wl.W, int(wl.off[1]),
                                  int(nf.decisions_host(wl.dec, wl.nb)["n_eligible"][0]))
         print(f"[bench] standalone, first bucket: " + ", ".join(f"{k} {v['ms']:.3f} ms" for k, v in split.items()
                                                             if isinstance(v, dict)), file=sys.stderr, flush=True)
@@ -735,7 +779,7 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "pct_hbm_peak": m["pct_hbm_peak"],
-        "config": {"workload": wl.lay.name, "W": wl.W, "n_total": wl.n, "buckets": wl.nb, "bucket_n": wl.bn,
+        "config": {"workload": wl.lay.name, "W": wl.W, "n_total": wl.n, **wl.buckets_desc(),
                    "eligible_frac": m["eligible_frac"],
                    "policy": "forced low-bit" if args.force_lowbit else "admitted, guard ok",
                    "format": args.format, "counts_written": not args.no_counts,
@@ -761,7 +805,7 @@ def config_record(wl, m, pol, cold, cpu, counters):
     """One row of the per-workload list: rate, share of peak, the pass-1
     roofline, the oracle's sample and the committed counter bytes."""
     ternary = pol.format == 1
-    row = {"workload": wl.lay.name, "W": wl.W, "n_total": wl.n, "buckets": wl.nb, "bucket_n": wl.bn,
+    row = {"workload": wl.lay.name, "W": wl.W, "n_total": wl.n, **wl.buckets_desc(),
            "format": "ternary" if ternary else "binary",
            "policy": "forced low-bit" if pol.force_lowbit else "admitted, guard ok",
            "caches": "cold (1 GiB overwritten before each step)" if cold else "warm",
@@ -805,7 +849,8 @@ def pass1_traffic(counters):
 
 def sweep_configs(nf, torch, gpt, args):
     """Every workload of the sweep after the headline: G-Ternary on the same
-    GPT-scale buffer, then ViT-B/16 scale, ResNet-50 scale, the tiny bucket
+    GPT-scale buffer, the same buffer cut into DDP's buckets (bucket table),
+    then ViT-B/16 scale, ResNet-50 scale, the tiny bucket
     (warm and cold caches), the stress bucket (route F, forced low-bit,
     forced low-bit G-Ternary) and the W = 255 fan-in bucket pair (G-Binary
     and G-Ternary).  Each row is a few timed steps and a bounded oracle
@@ -815,6 +860,13 @@ def sweep_configs(nf, torch, gpt, args):
     m = gpt.measure(tern, 10, 2)
     rows.append(config_record(gpt, m, tern, False, None if args.no_cpu_baseline else gpt.cpu_baseline(tern, 3.0),
                               committed_counters(gpt.lay.name, "ternary")))
+    # the same buffer cut as DDP cuts the model, through the bucket-table driver
+    import synth
+    gpt.set_buckets(synth.ddp_offsets(gpt.lay))
+    m = gpt.measure(nf.policy(), 10, 2)
+    rows.append(config_record(gpt, m, nf.policy(), False,
+                              None if args.no_cpu_baseline else gpt.cpu_baseline(nf.policy(), 3.0),
+                              committed_counters(gpt.lay.name, "ddp")))
     gpt.release()
     plan = [("vitb16", [(nf.policy(), False, 20)]),
             ("resnet50", [(nf.policy(), False, 50)]),

@@ -452,6 +452,47 @@ nf_status nf_route_buckets_noalloc(const float* grads, int64_t worker_stride, in
                                    nf_worker_stats* stats, nf_route_decision* decisions,
                                    void* stream);
 
+/*
+ * Buckets of different sizes in one flat buffer (§2.1, §2.3: DDP fills a
+ * bucket with whole parameters up to its capacity, so buckets end at
+ * parameter boundaries and differ in size).  Bucket b covers elements
+ * [bucket_offsets[b], bucket_offsets[b+1]) of every worker row, of the mask,
+ * of the bitmap rows (from word bucket_offsets[b] / 64), of counts and of out;
+ * n_total = bucket_offsets[nb].  bucket_offsets (host, nb + 1 values):
+ * offsets[0] = 0, strictly increasing (no empty bucket), every bucket start
+ * offsets[b] (b < nb) a multiple of 64.  stats is [nb][W], decisions [nb].
+ * Per bucket, the results equal those of nf_route_bucket on that bucket
+ * (with the ternary format, c- of bucket b starts at counts + n_total +
+ * offsets[b]).
+ *
+ * The kernels find a bucket through a device table built once per bucket
+ * layout and worker count (the layout is fixed for a training run):
+ *   nf_bucket_table_bytes   size of the table (0 for invalid offsets or W)
+ *   nf_bucket_table_init    builds it on the host and copies it into
+ *                           `table` (device, caller-owned, 256-byte aligned,
+ *                           at least nf_bucket_table_bytes), then
+ *                           synchronises `stream`: a set-up call, not for
+ *                           the step loop
+ *   nf_workspace_bytes_table  workspace of nf_route_bucket_table
+ * nf_route_bucket_table reads the table and needs the same W and offsets it
+ * was built with (not checked on the device: another table gives wrong
+ * results or invalid accesses).  Errors as nf_route_buckets, and
+ * NF_ERR_INVALID_ARG for invalid offsets, NF_ERR_WORKSPACE for a short table.
+ */
+size_t nf_bucket_table_bytes(int32_t W, const int64_t* bucket_offsets, int32_t nb);
+nf_status nf_bucket_table_init(int32_t W, const int64_t* bucket_offsets, int32_t nb, void* table,
+                               size_t table_bytes, void* stream);
+size_t nf_workspace_bytes_table(int32_t W, const int64_t* bucket_offsets, int32_t nb);
+/* Profiling query (no paper counterpart): nf_pass1_launches for a bucket
+ * table; 0 for invalid offsets or W.  Pure host function. */
+int64_t nf_pass1_launches_table(int32_t W, const int64_t* bucket_offsets, int32_t nb, int32_t sign_words);
+nf_status nf_route_bucket_table(const float* grads, int64_t worker_stride, int32_t W,
+                                const int64_t* bucket_offsets, int32_t nb, const void* table,
+                                const uint64_t* mask, const nf_route_policy* policy_host, uint64_t* bits,
+                                int64_t bits_stride_words, uint8_t* counts, float* out,
+                                nf_worker_stats* stats, nf_route_decision* decisions, void* ws,
+                                size_t ws_bytes, void* stream);
+
 /* ------------------------------------------------------------------------
  * Controller inputs on the host (§4.3 Supervisor recovery, §4.4 online
  * control, §6.4 endpoint-capacity guard).  These functions produce the

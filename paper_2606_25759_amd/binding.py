@@ -32,7 +32,8 @@ NF_FORMAT_BINARY, NF_FORMAT_TERNARY = 0, 1
 EXPORTS = ["nf_abi_version", "nf_last_error", "nf_mask_from_segments", "nf_workspace_bytes",
            "nf_bucket_health", "nf_pack_signs", "nf_fp32_reduce", "nf_signcount_reduce",
            "nf_route_decide", "nf_route_bucket", "nf_workspace_bytes_buckets", "nf_route_buckets",
-           "nf_route_buckets_noalloc",
+           "nf_route_buckets_noalloc", "nf_bucket_table_bytes", "nf_bucket_table_init",
+           "nf_workspace_bytes_table", "nf_pass1_launches_table", "nf_route_bucket_table",
            "nf_set_phase_events", "nf_pass1_launches", "nf_pass1_chunk_elems", "nf_slice_scales_from_pass1", "nf_ternary_threshold", "nf_pack_ternary",
            "nf_ternary_reduce", "nf_partial_counts", "nf_partial_count_reduce", "nf_stock_signcount",
            "nf_supervisor_init", "nf_supervisor_policy", "nf_supervisor_update", "nf_endpoint_guard",
@@ -134,6 +135,12 @@ def load(path=None):
                                             _P, _P, _P, _SZ, _P]),
         "nf_route_buckets_noalloc": (ctypes.c_int, [_P, _I64, _I32, _I64, _I64, _P, _P, _P, _I64, _P,
                                                     _P, _P, _P, _P]),
+        "nf_bucket_table_bytes": (_SZ, [_I32, _P, _I32]),
+        "nf_bucket_table_init": (ctypes.c_int, [_I32, _P, _I32, _P, _SZ, _P]),
+        "nf_workspace_bytes_table": (_SZ, [_I32, _P, _I32]),
+        "nf_pass1_launches_table": (_I64, [_I32, _P, _I32, _I32]),
+        "nf_route_bucket_table": (ctypes.c_int, [_P, _I64, _I32, _P, _I32, _P, _P, _P, _P, _I64, _P, _P,
+                                                 _P, _P, _P, _SZ, _P]),
         "nf_set_phase_events": (ctypes.c_int, [_P, _P, _P, _P]),
         "nf_slice_scales_from_pass1": (_I32, [_P, _I64, _I32, _I64, _P, _P, _I64, _P, _P, _P, _SZ, _P]),
         "nf_pass1_launches": (_I64, [_I32, _I64, _I64, _I32]),
@@ -499,6 +506,51 @@ def nf_route_buckets_noalloc(grads, n_total, bucket_n, mask, pol, bits, counts, 
                                            _dev_ptr(out, torch.float32, "out"),
                                            _dev_ptr(stats, torch.uint8, "stats"),
                                            _dev_ptr(decisions, torch.uint8, "decisions"), _stream(stream)))
+
+
+def _offsets(offsets):
+    """(int64 host array, its pointer, nb) of bucket offsets (nb + 1 values)."""
+    o = np.ascontiguousarray(offsets, dtype=np.int64)
+    if o.ndim != 1 or o.size < 1:
+        raise ValueError("bucket offsets: a 1-D sequence of nb + 1 values")
+    return o, o.ctypes.data_as(ctypes.c_void_p), int(o.size) - 1
+
+
+def nf_bucket_table_bytes(W, offsets):
+    o, p, nb = _offsets(offsets)
+    return int(load().nf_bucket_table_bytes(W, p, nb))
+
+
+def nf_bucket_table_init(W, offsets, table, stream=None):
+    """Builds the device bucket table of these offsets into `table` (a uint8
+    device tensor of at least nf_bucket_table_bytes); synchronises the stream."""
+    o, p, nb = _offsets(offsets)
+    _check(load().nf_bucket_table_init(W, p, nb, _dev_ptr(table, torch.uint8, "table"), table.numel(),
+                                       _stream(stream)))
+
+
+def nf_workspace_bytes_table(W, offsets):
+    o, p, nb = _offsets(offsets)
+    return int(load().nf_workspace_bytes_table(W, p, nb))
+
+
+def nf_pass1_launches_table(W, offsets, sign_words=True):
+    o, p, nb = _offsets(offsets)
+    return int(load().nf_pass1_launches_table(W, p, nb, int(bool(sign_words))))
+
+
+def nf_route_bucket_table(grads, offsets, table, mask, pol, bits, counts, out, stats, decisions, ws,
+                          stream=None):
+    g, stride, W = _rows(grads)
+    b, bstride = _bits_rows(bits)
+    o, p, nb = _offsets(offsets)
+    _check(load().nf_route_bucket_table(g, stride, W, p, nb, _dev_ptr(table, torch.uint8, "table"),
+                                        _words(mask), ctypes.byref(pol), b, bstride,
+                                        _dev_ptr(counts, torch.uint8, "counts"),
+                                        _dev_ptr(out, torch.float32, "out"),
+                                        _dev_ptr(stats, torch.uint8, "stats"),
+                                        _dev_ptr(decisions, torch.uint8, "decisions"),
+                                        _dev_ptr(ws, torch.uint8, "ws"), ws.numel(), _stream(stream)))
 
 
 def nf_set_phase_events(before_pass1=None, after_pass1=None, after_decide=None, after_pass2=None):

@@ -6,6 +6,7 @@
 
 #include <mutex>
 #include <string>
+#include <vector>
 
 #include "nf_internal.h"
 
@@ -134,6 +135,8 @@ void fill_pass1_geometry(const nf::Geometry& geo, nf::Pass1Args* a) {
   a->T = geo.T;
   a->G = geo.G;
   a->slots = geo.slots;
+  a->btab = nullptr;
+  a->cbucket = nullptr;
 }
 
 #define NF_TRY(x)                    \
@@ -148,7 +151,8 @@ nf_status run_pass1_decide(const nf::Geometry& geo, const float* g, int64_t stri
                            const uint64_t* mask, uint64_t* bits, int64_t bstride, float* out,
                            int sums, int mean, nf_worker_stats* stats, nf_route_decision* dec,
                            const nf_route_policy* pol, void* ws, hipStream_t s,
-                           bool phases = false) {
+                           bool phases = false, const nf::BucketRow* btab = nullptr,
+                           const int32_t* cbucket = nullptr) {
   const nf::WorkspaceLayout lay = nf::workspace_layout(geo);
   char* w = static_cast<char*>(ws);
   nf::Pass1Args a;
@@ -161,6 +165,8 @@ nf_status run_pass1_decide(const nf::Geometry& geo, const float* g, int64_t stri
   a.part = reinterpret_cast<nf::Partial*>(w + lay.partials);
   a.part_ne = reinterpret_cast<uint64_t*>(w + lay.ne);
   fill_pass1_geometry(geo, &a);
+  a.btab = btab;
+  a.cbucket = cbucket;
   a.sums = sums;
   a.mean = mean;
   if (phases) record_phase(0, s);
@@ -192,6 +198,7 @@ nf_status run_pass1_decide(const nf::Geometry& geo, const float* g, int64_t stri
   d.G = geo.G;
   d.gs = geo.gs;
   d.groups = geo.groups;
+  d.btab = btab;
   e = nf::launch_decide(geo, d, s);
   if (e != hipSuccess) return hip_fail(e, "decide launch");
   if (phases) record_phase(2, s);
@@ -209,10 +216,10 @@ nf::Pass2Args pass2_args(const nf::Geometry& geo) {
   return p;
 }
 
-nf_status route_flat(const float* g, int64_t stride, int32_t W, int64_t n_total, int64_t bucket_n,
-                     const uint64_t* mask, const nf_route_policy* pol, uint64_t* bits,
-                     int64_t bstride, uint8_t* counts, float* out, nf_worker_stats* stats,
-                     nf_route_decision* dec, void* ws, size_t ws_bytes, void* stream) {
+// Checks shared by the flat-buffer drivers (equal buckets or a table).
+nf_status check_route_args(const float* g, int64_t stride, int32_t W, int64_t n_total, const uint64_t* mask,
+                           const nf_route_policy* pol, float* out, nf_worker_stats* stats,
+                           nf_route_decision* dec) {
   NF_TRY(check_grads(g, stride, W, n_total));
   NF_TRY(check_mask(mask, n_total));
   NF_TRY(check_policy(pol));
@@ -220,7 +227,15 @@ nf_status route_flat(const float* g, int64_t stride, int32_t W, int64_t n_total,
   if (!aligned(out, 4)) return fail(NF_ERR_ALIGNMENT, "out not 4-byte aligned");
   if (!stats || !dec) return fail(NF_ERR_INVALID_ARG, "stats and decision are required");
   if (!aligned(stats, 8) || !aligned(dec, 8)) return fail(NF_ERR_ALIGNMENT, "stats/decision not 8-byte aligned");
-  const nf::Geometry geo = nf::make_geometry(W, n_total, bucket_n);
+  return NF_OK;
+}
+
+// The route over every bucket of a geometry (checked arguments).
+nf_status route_geo(const nf::Geometry& geo, const float* g, int64_t stride, int32_t W, const uint64_t* mask,
+                    const nf_route_policy* pol, uint64_t* bits, int64_t bstride, uint8_t* counts, float* out,
+                    nf_worker_stats* stats, nf_route_decision* dec, void* ws, size_t ws_bytes, void* stream,
+                    const nf::BucketRow* btab, const int32_t* cbucket) {
+  const int64_t n_total = geo.n_total;
   NF_TRY(check_ws(ws, ws_bytes, nf::workspace_layout(geo).total));
   // The policy alone fixes the route when low-bit is not admitted, vetoed
   // or guard-rejected (and not forced): then no sign payload is built and
@@ -233,7 +248,7 @@ nf_status route_flat(const float* g, int64_t stride, int32_t W, int64_t n_total,
   // bucket has been read: pass 1 then builds no sign payload.
   NF_TRY(run_pass1_decide(geo, g, stride, mask, (predecided || ternary) ? nullptr : bits, bstride, out,
                           predecided ? nf::kSumsAll : nf::kSumsRouted, pol->fp32_op == NF_FP32_MEAN,
-                          stats, dec, pol, ws, s, true));
+                          stats, dec, pol, ws, s, true, btab, cbucket));
   if (predecided || n_total == 0) {
     record_phase(3, s);
     return ok();
@@ -257,6 +272,8 @@ nf_status route_flat(const float* g, int64_t stride, int32_t W, int64_t n_total,
     t.W = W;
     t.decode_mode = pol->decode_mode;
     t.bpb2 = geo.bpb2;
+    t.btab = btab;
+    t.cbucket = cbucket;
     hipError_t e = nf::launch_ternary_pack(geo, t, s);
     if (e != hipSuccess) return hip_fail(e, "ternary pack launch");
     e = nf::launch_ternary_reduce(geo, t, s);
@@ -274,10 +291,37 @@ nf_status route_flat(const float* g, int64_t stride, int32_t W, int64_t n_total,
   p.op = ternary ? nf::kOpFallbackOnly : nf::kOpFromDecision;
   p.decode_mode = pol->decode_mode;
   p.mean = pol->fp32_op == NF_FP32_MEAN;
+  p.btab = btab;
   hipError_t e = nf::launch_pass2(geo, p, s);
   if (e != hipSuccess) return hip_fail(e, "pass-2 launch");
   record_phase(3, s);
   return ok();
+}
+
+nf_status route_flat(const float* g, int64_t stride, int32_t W, int64_t n_total, int64_t bucket_n,
+                     const uint64_t* mask, const nf_route_policy* pol, uint64_t* bits,
+                     int64_t bstride, uint8_t* counts, float* out, nf_worker_stats* stats,
+                     nf_route_decision* dec, void* ws, size_t ws_bytes, void* stream) {
+  NF_TRY(check_route_args(g, stride, W, n_total, mask, pol, out, stats, dec));
+  const nf::Geometry geo = nf::make_geometry(W, n_total, bucket_n);
+  return route_geo(geo, g, stride, W, mask, pol, bits, bstride, counts, out, stats, dec, ws, ws_bytes, stream,
+                   nullptr, nullptr);
+}
+
+// A bucket table's offsets: nb >= 1, off[0] = 0, strictly increasing, every
+// bucket start a multiple of 64 (its bitmap words start at off[b] / 64).
+nf_status check_table_offsets(const int64_t* off, int32_t nb) {
+  if (nb < 1) return fail(NF_ERR_INVALID_ARG, "nb=%d: a bucket table needs at least one bucket", nb);
+  if (!off) return fail(NF_ERR_INVALID_ARG, "bucket_offsets is NULL");
+  if (off[0] != 0) return fail(NF_ERR_INVALID_ARG, "bucket_offsets[0]=%lld, must be 0", (long long)off[0]);
+  for (int32_t b = 0; b < nb; ++b) {
+    if (off[b + 1] <= off[b])
+      return fail(NF_ERR_INVALID_ARG, "bucket %d is empty or negative: offsets %lld, %lld", b, (long long)off[b],
+                  (long long)off[b + 1]);
+    if (off[b] % 64) return fail(NF_ERR_INVALID_ARG, "bucket %d starts at %lld, not a multiple of 64", b,
+                                 (long long)off[b]);
+  }
+  return NF_OK;
 }
 
 }  // namespace
@@ -880,6 +924,71 @@ nf_status nf_route_buckets_noalloc(const float* grads, int64_t worker_stride, in
   NF_TRY(scratch_address(&ws));
   return route_flat(grads, worker_stride, W, n_total, bucket_n, mask, policy_host, bits,
                     bits_stride_words, counts, out, stats, decisions, ws, kStaticScratchBytes, stream);
+}
+
+size_t nf_bucket_table_bytes(int32_t W, const int64_t* bucket_offsets, int32_t nb) {
+  if (W < 1 || W > 255 || check_table_offsets(bucket_offsets, nb) != NF_OK) return 0;
+  return nf::table_bytes(nf::make_geometry_table(W, bucket_offsets, nb));
+}
+
+nf_status nf_bucket_table_init(int32_t W, const int64_t* bucket_offsets, int32_t nb, void* table,
+                               size_t table_bytes, void* stream) {
+  if (W < 1 || W > 255) return fail(NF_ERR_INVALID_ARG, "W=%d outside [1, 255]", W);
+  NF_TRY(check_table_offsets(bucket_offsets, nb));
+  const nf::Geometry geo = nf::make_geometry_table(W, bucket_offsets, nb);
+  const size_t need = nf::table_bytes(geo);
+  if (table_bytes < need) return fail(NF_ERR_WORKSPACE, "table of %zu bytes < %zu required", table_bytes, need);
+  if (!table) return fail(NF_ERR_INVALID_ARG, "table is NULL");
+  if (!aligned(table, 256)) return fail(NF_ERR_ALIGNMENT, "table not 256-byte aligned");
+  // Rows and the bucket of every chunk, built here and copied once.
+  std::vector<unsigned char> host(need, 0);
+  nf::BucketRow* rows = reinterpret_cast<nf::BucketRow*>(host.data());
+  int32_t* cb = reinterpret_cast<int32_t*>(host.data() + nf::table_rows_bytes(nb));
+  int64_t q = 0;
+  for (int32_t b = 0; b < nb; ++b) {
+    const int64_t len = bucket_offsets[b + 1] - bucket_offsets[b];
+    const int64_t chunks = nf::ceil_div(nf::ceil_div(len, geo.tile), geo.G);
+    rows[b].start = bucket_offsets[b];
+    rows[b].len = len;
+    rows[b].chunk0 = q;
+    rows[b].pad = 0;
+    for (int64_t c = 0; c < chunks; ++c) cb[q + c] = b;
+    q += chunks;
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = hipMemcpyAsync(table, host.data(), need, hipMemcpyHostToDevice, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e, "bucket table copy");
+  return ok();
+}
+
+int64_t nf_pass1_launches_table(int32_t W, const int64_t* bucket_offsets, int32_t nb, int32_t sign_words) {
+  if (W < 1 || W > 255 || check_table_offsets(bucket_offsets, nb) != NF_OK) return 0;
+  const nf::Geometry geo = nf::make_geometry_table(W, bucket_offsets, nb);
+  return geo.ngroups * nf::ceil_div(geo.total_chunks, nf::pass1_launch_chunks(geo, sign_words != 0));
+}
+
+size_t nf_workspace_bytes_table(int32_t W, const int64_t* bucket_offsets, int32_t nb) {
+  if (W < 1 || W > 255 || check_table_offsets(bucket_offsets, nb) != NF_OK) return 0;
+  return nf::workspace_layout(nf::make_geometry_table(W, bucket_offsets, nb)).total;
+}
+
+nf_status nf_route_bucket_table(const float* grads, int64_t worker_stride, int32_t W,
+                                const int64_t* bucket_offsets, int32_t nb, const void* table,
+                                const uint64_t* mask, const nf_route_policy* policy_host, uint64_t* bits,
+                                int64_t bits_stride_words, uint8_t* counts, float* out,
+                                nf_worker_stats* stats, nf_route_decision* decisions, void* ws,
+                                size_t ws_bytes, void* stream) {
+  NF_TRY(check_table_offsets(bucket_offsets, nb));
+  const int64_t n_total = bucket_offsets[nb];
+  NF_TRY(check_route_args(grads, worker_stride, W, n_total, mask, policy_host, out, stats, decisions));
+  if (!table) return fail(NF_ERR_INVALID_ARG, "table is NULL");
+  if (!aligned(table, 256)) return fail(NF_ERR_ALIGNMENT, "table not 256-byte aligned");
+  const nf::Geometry geo = nf::make_geometry_table(W, bucket_offsets, nb);
+  const unsigned char* t = static_cast<const unsigned char*>(table);
+  return route_geo(geo, grads, worker_stride, W, mask, policy_host, bits, bits_stride_words, counts, out, stats,
+                   decisions, ws, ws_bytes, stream, reinterpret_cast<const nf::BucketRow*>(t),
+                   reinterpret_cast<const int32_t*>(t + nf::table_rows_bytes(nb)));
 }
 
 }  // extern "C"

@@ -312,6 +312,37 @@ __device__ __forceinline__ int64_t bucket_len(int64_t n_total, int64_t bucket_n,
   return r < 0 ? 0 : (r < bucket_n ? r : bucket_n);
 }
 
+// The bucket b of pass-1 chunk q and the chunk's index c in it: equal
+// buckets of chunks_full chunks (btab NULL; the last may have fewer), or a
+// bucket table.
+__device__ __forceinline__ void chunk_home(int64_t q, const BucketRow* btab, const int32_t* cbucket, int nb,
+                                           int64_t chunks_full, int& b, int64_t& c) {
+  if (btab) {
+    b = cbucket[q];
+    c = q - btab[b].chunk0;
+  } else if (q < (int64_t)(nb - 1) * chunks_full) {
+    b = (int)(q / chunks_full);
+    c = q - (int64_t)b * chunks_full;
+  } else {
+    b = nb - 1;
+    c = q - (int64_t)b * chunks_full;
+  }
+}
+
+// First element, length and first chunk (partial slot) of bucket b.
+__device__ __forceinline__ void bucket_span(int b, const BucketRow* btab, int64_t n_total, int64_t bucket_n,
+                                            int64_t slots, int64_t& base, int64_t& len, int64_t& chunk0) {
+  if (btab) {
+    base = btab[b].start;
+    len = btab[b].len;
+    chunk0 = btab[b].chunk0;
+  } else {
+    base = (int64_t)b * bucket_n;
+    len = bucket_len(n_total, bucket_n, b);
+    chunk0 = (int64_t)b * slots;
+  }
+}
+
 // ------------------------------------------------------ bit-sliced counts
 
 struct FullAdd {

@@ -97,13 +97,25 @@ constexpr NF_HD int routed_steps(int nw) { return (kMaxG * nw + kWaves - 1) / kW
 struct Geometry {
   int W, wg, eg, wpw, T, tile, G;
   int rows, ngroups;     // worker rows of the largest pass-1 group (<= 64), and groups
-  int64_t n_total, bucket_n, nb;
-  int64_t chunks_full;   // chunks of a full bucket
+  int64_t n_total, bucket_n, nb;  // bucket_n: 0 for a bucket table
+  bool table;            // buckets from a bucket table (sizes vary)
+  int64_t chunks_full;   // chunks of a full bucket (of the largest, for a table)
   int64_t total_chunks;  // over all buckets
-  int slots;             // partial-statistics slots per bucket: one per chunk
+  int slots;             // partial-statistics slots per bucket (uniform): one per chunk
   int gs;                // slots per second-level group (0: no second level)
   int groups;            // second-level groups per full bucket (<= kMaxSlots)
   int bpb2;              // pass-2 blocks per bucket
+};
+
+// Bucket table: one row per bucket of a flat buffer whose buckets differ in
+// size (DDP closes a bucket at a parameter boundary, §2.1).  Chunk q of
+// pass 1 belongs to bucket cbucket[q] and owns partial slot q, so bucket b's
+// slots are chunk0 .. chunk0 + (its chunks) - 1.
+struct BucketRow {
+  int64_t start;   // first element (a multiple of 64)
+  int64_t len;     // elements (> 0)
+  int64_t chunk0;  // first pass-1 chunk
+  int64_t pad;
 };
 
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -122,7 +134,9 @@ inline void row_group(const Geometry& g, int i, int* wbase, int* rows) {
   *rows = q + (i < r ? 1 : 0);
 }
 
-inline Geometry make_geometry(int W, int64_t n_total, int64_t bucket_n) {
+// The worker-dependent part of the geometry (row groups, wavefront roles,
+// tile, chunk length before the fill rule).
+inline Geometry geometry_core(int W) {
   Geometry g;
   g.W = W;
   g.ngroups = W > kRowGroup ? (W + kRowGroup - 1) / kRowGroup : 1;
@@ -142,6 +156,43 @@ inline Geometry make_geometry(int W, int64_t n_total, int64_t bucket_n) {
   g.G = kBitsWords / per_tile;
   if (g.G > kMaxG) g.G = kMaxG;
   if (g.G < 1) g.G = 1;
+  g.table = false;
+  return g;
+}
+
+// A problem of fewer than kFillChunks chunks would leave compute units
+// idle: it takes the smallest G that keeps it within kFillChunks chunks (so
+// within one launch).  total_for(G): the problem's chunks at G tiles each.
+template <typename F>
+inline void fill_rule(Geometry& g, F total_for) {
+  if (total_for(g.G) < kFillChunks)
+    for (int G = 1; G < g.G; ++G)
+      if (total_for(G) <= kFillChunks) {
+        g.G = G;
+        break;
+      }
+}
+
+// Second-level groups and pass-2 blocks from the largest bucket's chunks
+// and words.
+inline void slot_groups(Geometry& g, int64_t max_len) {
+  // Every chunk owns a slot, so no two chunks ever touch the same partial.
+  // A bucket of more than kMaxSlots chunks (kMaxSlotsWide above 64 workers)
+  // is first summed in groups of gs consecutive slots (at most that many
+  // groups), which the decision reads.
+  g.slots = (int)(g.chunks_full > 1 ? g.chunks_full : 1);
+  const int cap = g.W > kRowGroup ? kMaxSlotsWide : kMaxSlots;
+  g.gs = g.chunks_full > cap ? (int)ceil_div(g.chunks_full, cap) : 0;
+  g.groups = g.gs ? (int)ceil_div(g.chunks_full, g.gs) : 0;
+  int64_t words = (max_len + 63) / 64;
+  int64_t chunks2 = ceil_div(words, kWordsPerWave2 * 4);
+  if (chunks2 < 1) chunks2 = 1;
+  g.bpb2 = (int)(chunks2 < kMaxBlocks2 ? chunks2 : kMaxBlocks2);
+}
+
+// Equal buckets of bucket_n elements (the last one shorter).
+inline Geometry make_geometry(int W, int64_t n_total, int64_t bucket_n) {
+  Geometry g = geometry_core(W);
   g.n_total = n_total;
   g.bucket_n = bucket_n;
   g.nb = n_total <= 0 ? 1 : ceil_div(n_total, bucket_n);
@@ -151,30 +202,41 @@ inline Geometry make_geometry(int W, int64_t n_total, int64_t bucket_n) {
   if (last < 0) last = 0;
   const int64_t tiles_full = ceil_div(full, g.tile), tiles_last = ceil_div(last, g.tile);
   auto total_for = [&](int G) { return (g.nb - 1) * ceil_div(tiles_full, G) + ceil_div(tiles_last, G); };
-  // A problem of fewer than kFillChunks chunks would leave compute units
-  // idle: it takes the smallest G that keeps it within kFillChunks chunks
-  // (so within one launch).
-  if (total_for(g.G) < kFillChunks)
-    for (int G = 1; G < g.G; ++G)
-      if (total_for(G) <= kFillChunks) {
-        g.G = G;
-        break;
-      }
+  fill_rule(g, total_for);
   g.chunks_full = ceil_div(tiles_full, g.G);
   g.total_chunks = total_for(g.G);
-  // Every chunk owns a slot, so no two chunks ever touch the same partial.
-  // A bucket of more than kMaxSlots chunks (kMaxSlotsWide above 64 workers)
-  // is first summed in groups of gs consecutive slots (at most that many
-  // groups), which the decision reads.
-  g.slots = (int)(g.chunks_full > 1 ? g.chunks_full : 1);
-  const int cap = W > kRowGroup ? kMaxSlotsWide : kMaxSlots;
-  g.gs = g.chunks_full > cap ? (int)ceil_div(g.chunks_full, cap) : 0;
-  g.groups = g.gs ? (int)ceil_div(g.chunks_full, g.gs) : 0;
-  int64_t words = (full + 63) / 64;
-  int64_t chunks2 = ceil_div(words, kWordsPerWave2 * 4);
-  if (chunks2 < 1) chunks2 = 1;
-  g.bpb2 = (int)(chunks2 < kMaxBlocks2 ? chunks2 : kMaxBlocks2);
+  slot_groups(g, full);
   return g;
+}
+
+// Buckets [off[b], off[b+1]) of a bucket table (nb >= 1, off[0] = 0,
+// off strictly increasing; validated by the caller).
+inline Geometry make_geometry_table(int W, const int64_t* off, int64_t nb) {
+  Geometry g = geometry_core(W);
+  g.table = true;
+  g.n_total = off[nb];
+  g.bucket_n = 0;
+  g.nb = nb;
+  auto total_for = [&](int G) {
+    int64_t t = 0;
+    for (int64_t b = 0; b < nb; ++b) t += ceil_div(ceil_div(off[b + 1] - off[b], g.tile), G);
+    return t;
+  };
+  fill_rule(g, total_for);
+  int64_t max_len = 0;
+  for (int64_t b = 0; b < nb; ++b)
+    if (off[b + 1] - off[b] > max_len) max_len = off[b + 1] - off[b];
+  g.chunks_full = ceil_div(ceil_div(max_len, g.tile), g.G);
+  g.total_chunks = total_for(g.G);
+  slot_groups(g, max_len);
+  return g;
+}
+
+// Device bucket table of a table geometry: the rows, then the bucket of
+// every chunk.
+inline size_t table_rows_bytes(int64_t nb) { return (size_t)((nb * (int64_t)sizeof(BucketRow) + 255) & ~(int64_t)255); }
+inline size_t table_bytes(const Geometry& g) {
+  return table_rows_bytes(g.nb) + (size_t)((g.total_chunks * 4 + 255) & ~(int64_t)255);
 }
 
 // Per (bucket, slot, worker) partial statistics written by pass 1.  The |g|
@@ -200,7 +262,8 @@ struct WorkspaceLayout {
 // second-level [bucket][group][W] and [bucket][group] sums.
 inline WorkspaceLayout workspace_layout(const Geometry& g) {
   WorkspaceLayout l;
-  const size_t slots = (size_t)g.nb * (size_t)g.slots;
+  // one slot per chunk: chunk q's partials at slot q
+  const size_t slots = g.table ? (size_t)(g.total_chunks > 0 ? g.total_chunks : 1) : (size_t)g.nb * (size_t)g.slots;
   const size_t groups = (size_t)g.nb * (size_t)g.groups;
   l.partials = 0;
   l.ne = align256(slots * (size_t)g.W * sizeof(Partial));
@@ -229,6 +292,8 @@ struct Pass1Args {
   // group's workers from wbase; racc: the routed FP32 sums continue from
   // out (not the first group); rfin: the last group (MEAN divides there).
   int32_t wtot, wbase, racc, rfin;
+  const BucketRow* btab;   // NULL: equal buckets of bucket_n
+  const int32_t* cbucket;  // bucket of every chunk (with btab)
 };
 
 struct DecideArgs {
@@ -248,6 +313,7 @@ struct DecideArgs {
   nf_route_policy pol;
   int64_t n_total, bucket_n;
   int32_t W, slots, tile, G, gs, groups;
+  const BucketRow* btab;  // NULL: equal buckets of bucket_n
 };
 
 // kOpFallbackOnly: route-driven, FP32 sums of the buckets routed F only.
@@ -276,6 +342,8 @@ struct TernArgs {
   // launch's row group is workers wbase .. wbase + rows - 1
   int64_t chunks_full, total_chunks;
   int32_t nb, wg, eg, T, G, rows, wbase;
+  const BucketRow* btab;   // NULL: equal buckets of bucket_n
+  const int32_t* cbucket;  // bucket of every chunk (with btab)
 };
 
 struct Pass2Args {
@@ -294,6 +362,7 @@ struct Pass2Args {
   // writes counts + z * z_counts, out + z * z_out
   int32_t nz, z_rows;
   int64_t z_counts, z_out;
+  const BucketRow* btab;  // NULL: equal buckets of bucket_n
 };
 
 // Partial-count reduction (inter-node sum of node-local counts + decode).

@@ -69,18 +69,11 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
   const int64_t q = q0 + blockIdx.x;  // this block's chunk
   if (q >= a.total_chunks) return;     // whole block
 
-  // chunk q -> bucket b, chunk c within it (all buckets but the last are full)
+  // chunk q -> bucket b, chunk c within it; the chunk's partials go to slot q
   int b;
-  int64_t c;
-  if (q < (int64_t)(a.nb - 1) * a.chunks_full) {
-    b = (int)(q / a.chunks_full);
-    c = q - (int64_t)b * a.chunks_full;
-  } else {
-    b = a.nb - 1;
-    c = q - (int64_t)b * a.chunks_full;
-  }
-  const int64_t base = (int64_t)b * a.bucket_n;
-  const int64_t nbe = bucket_len(a.n_total, a.bucket_n, b);
+  int64_t c, base, nbe, chunk0;
+  chunk_home(q, a.btab, a.cbucket, a.nb, a.chunks_full, b, c);
+  bucket_span(b, a.btab, a.n_total, a.bucket_n, a.slots, base, nbe, chunk0);
   const int v = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wavefront index, uniform
   const int lane = threadIdx.x & 63;
   const int wg = v % a.wg;
@@ -221,7 +214,7 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
       constexpr int MS = routed_steps(NW);   // steps per wavefront at most
       const int64_t c0 = base + tb * tile;
       const int nsteps = (int)((te - tb) * (tile / 64));
-      const int64_t slot = (int64_t)b * a.slots + c;
+      const int64_t slot = q;
       Partial* red = reinterpret_cast<Partial*>(smem);  // [kWaves][W]
       float run[MS];
 #pragma unroll
@@ -373,7 +366,7 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
       }
     }
     __syncthreads();
-    const int64_t slot = (int64_t)b * a.slots + c;
+    const int64_t slot = q;
     if ((int)threadIdx.x < a.W) {
       const int w = threadIdx.x;
       Partial p = red[w];
@@ -703,7 +696,7 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
     }
   }
 
-  const int64_t slot = (int64_t)b * a.slots + c;  // the chunk's own partial slot
+  const int64_t slot = q;  // the chunk's own partial slot
   if (a.eg == 1) {
     // One element group: each worker lives in exactly one wavefront, which
     // stores its own rows of sign words and its own partials, so the block
@@ -799,14 +792,15 @@ __global__ __launch_bounds__(256) void k_slotsum(DecideArgs a) {
   __shared__ Partial red[256];
   const int b = (int)(blockIdx.x / (unsigned)a.groups);
   const int grp = (int)(blockIdx.x - (unsigned)b * (unsigned)a.groups);
-  const int64_t nbe = bucket_len(a.n_total, a.bucket_n, b);
+  int64_t base, nbe, chunk0;
+  bucket_span(b, a.btab, a.n_total, a.bucket_n, a.slots, base, nbe, chunk0);
   const int64_t chunks = ((nbe + a.tile - 1) / a.tile + a.G - 1) / a.G;
   const int64_t s0 = (int64_t)grp * a.gs;
   if (s0 >= chunks) return;  // whole block: this bucket has fewer groups
   const int cnt = (int)(chunks - s0 < a.gs ? chunks - s0 : a.gs);
   const int parts = 256 / a.W;
   const int t = threadIdx.x;
-  const Partial* P = a.part + ((int64_t)b * a.slots + s0) * a.W;
+  const Partial* P = a.part + (chunk0 + s0) * a.W;
   if (t < parts * a.W) {
     const int w = t % a.W;
     Partial r;
@@ -823,7 +817,7 @@ __global__ __launch_bounds__(256) void k_slotsum(DecideArgs a) {
     a.part2[((int64_t)b * a.groups + grp) * a.W + t] = r;
   }
   if (t < 64) {
-    const uint64_t* N = a.part_ne + (int64_t)b * a.slots + s0;
+    const uint64_t* N = a.part_ne + chunk0 + s0;
     uint64_t ne = 0;
     for (int k = t; k < cnt; k += 64) ne += N[k];
     ne = wave_sum_u64(ne);
@@ -852,11 +846,12 @@ __global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
   const int v = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wavefront index, uniform
   const int lane = threadIdx.x & 63;
   // One slot per chunk of this bucket, or its second-level group sums.
-  const int64_t nbe = bucket_len(a.n_total, a.bucket_n, b);
+  int64_t base, nbe, chunk0;
+  bucket_span(b, a.btab, a.n_total, a.bucket_n, a.slots, base, nbe, chunk0);
   const int64_t chunks = ((nbe + a.tile - 1) / a.tile + a.G - 1) / a.G;
   const bool two = a.gs > 0;
-  const Partial* P = two ? a.part2 + (int64_t)b * a.groups * a.W : a.part + (int64_t)b * a.slots * a.W;
-  const uint64_t* PN = two ? a.part2_ne + (int64_t)b * a.groups : a.part_ne + (int64_t)b * a.slots;
+  const Partial* P = two ? a.part2 + (int64_t)b * a.groups * a.W : a.part + chunk0 * a.W;
+  const uint64_t* PN = two ? a.part2_ne + (int64_t)b * a.groups : a.part_ne + chunk0;
   const int used = (int)(two ? (chunks + a.gs - 1) / a.gs : chunks);
   // The slot loops are unrolled so that their loads are in flight together;
   // the adds keep their order.
@@ -919,7 +914,7 @@ __global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
   if (EXACT) {
     for (int w = 0; w < a.W; ++w) {
       if (!redo[w]) continue;  // block-uniform
-      const double e = exact_abs_sum(a.g + (int64_t)w * a.wstride, a.mask, (int64_t)b * a.bucket_n, nbe, hist);
+      const double e = exact_abs_sum(a.g + (int64_t)w * a.wstride, a.mask, base, nbe, hist);
       if (threadIdx.x == 0) st[w].sum_abs_elig = e;
       ++resummed;
     }

@@ -42,8 +42,8 @@ __global__ __launch_bounds__(kThreads2) void k_pass2(
   uint8_t* counts = counts0 ? counts0 + (int64_t)z * a.z_counts : nullptr;
   float* out = out0 ? out0 + (int64_t)z * a.z_out : nullptr;
   const int b = blockIdx.y;
-  const int64_t base = (int64_t)b * a.bucket_n;
-  const int64_t nbe = bucket_len(a.n_total, a.bucket_n, b);
+  int64_t base, nbe, chunk0;
+  bucket_span(b, a.btab, a.n_total, a.bucket_n, 0, base, nbe, chunk0);
   int op = a.op;
   int sel = a.select;
   float scale = 0.0f;

@@ -28,17 +28,10 @@ __global__ __launch_bounds__(kThreads1) __attribute__((amdgpu_waves_per_eu(WPW <
   const int64_t q = q0 + blockIdx.x;  // this block's chunk
   if (q >= a.total_chunks) return;     // whole block
   int b;
-  int64_t c;
-  if (q < (int64_t)(a.nb - 1) * a.chunks_full) {
-    b = (int)(q / a.chunks_full);
-    c = q - (int64_t)b * a.chunks_full;
-  } else {
-    b = a.nb - 1;
-    c = q - (int64_t)b * a.chunks_full;
-  }
+  int64_t c, base, nbe, chunk0;
+  chunk_home(q, a.btab, a.cbucket, a.nb, a.chunks_full, b, c);
   if (a.dec && a.dec[b].route != NF_ROUTE_LOWBIT) return;  // whole block: no planes
-  const int64_t base = (int64_t)b * a.bucket_n;
-  const int64_t nbe = bucket_len(a.n_total, a.bucket_n, b);
+  bucket_span(b, a.btab, a.n_total, a.bucket_n, 0, base, nbe, chunk0);
   const int v = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wavefront index, uniform
   const int lane = threadIdx.x & 63;
   const int wg = v % a.wg;
@@ -257,8 +250,8 @@ __global__ __launch_bounds__(kThreads2) void k_tpass2(TernArgs a) {
     for (int d = threadIdx.x; d <= 2 * a.W; d += kThreads2) tab[d] = scale * decode_qt(d - a.W, a.W, a.decode_mode);
     __syncthreads();
   }
-  const int64_t base = (int64_t)b * a.bucket_n;
-  const int64_t nbe = bucket_len(a.n_total, a.bucket_n, b);
+  int64_t base, nbe, chunk0;
+  bucket_span(b, a.btab, a.n_total, a.bucket_n, 0, base, nbe, chunk0);
   const int64_t nwords = (nbe + 63) / 64;
   const int64_t wbase = base / 64;
   const int v = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wavefront index, uniform

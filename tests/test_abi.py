@@ -229,6 +229,47 @@ def test_invalid_arguments_return_codes_without_launch():
     assert lib.nf_route_decide(st, 2, 10, 11, ctypes.byref(pol), ctypes.byref(d)) == nf.NF_ERR_INVALID_ARG
 
 
+def test_bucket_table_sizes_and_argument_errors():
+    lib = _lib()
+    P = ctypes.c_void_p
+    fake = P(0x1000)          # never dereferenced: validation fails first
+    ws = P(0x100000)
+    b = 6_553_600
+    # equal buckets through a table: the workspace of the equal-bucket driver
+    for W in (4, 16, 64, 255):
+        assert nf.nf_workspace_bytes_table(W, [0, b, 2 * b, 3 * b]) == nf.nf_workspace_bytes_buckets(W, 3 * b, b)
+    # a short last bucket holds fewer slots than a full one
+    assert 0 < nf.nf_workspace_bytes_table(16, [0, b, b + 64]) <= nf.nf_workspace_bytes_buckets(16, b + 64, b)
+    # the table: 32-byte rows, then an int32 per pass-1 chunk, each part 256-byte aligned
+    _, chunks = nf.nf_pass1_chunk_elems(16, 3 * b, b)
+    assert nf.nf_bucket_table_bytes(16, [0, b, 2 * b, 3 * b]) == 256 + -(-3 * chunks * 4 // 256) * 256
+    pol = nf.policy()
+    for bad in ([0], [1, 64], [0, 64, 64], [0, 100, 200], [0, 128, 64]):
+        assert nf.nf_bucket_table_bytes(16, bad) == 0 and nf.nf_workspace_bytes_table(16, bad) == 0, bad
+        o = np.array(bad, np.int64)
+        op = o.ctypes.data_as(P)
+        assert lib.nf_bucket_table_init(16, op, len(bad) - 1, fake, 1 << 20, None) == nf.NF_ERR_INVALID_ARG
+        assert lib.nf_route_bucket_table(fake, 1 << 10, 16, op, len(bad) - 1, fake, fake, ctypes.byref(pol),
+                                         fake, 16, None, fake, fake, fake, ws, 1 << 24, None) == \
+            nf.NF_ERR_INVALID_ARG, bad
+    assert "multiple of 64" in (lib.nf_bucket_table_init(16, np.array([0, 100, 200], np.int64).ctypes.data_as(P), 2,
+                                                         fake, 1 << 20, None) and nf.nf_last_error())
+    o = np.array([0, 640, 1000], np.int64)
+    op = o.ctypes.data_as(P)
+    need = nf.nf_bucket_table_bytes(16, o)
+    assert lib.nf_bucket_table_init(0, op, 2, fake, need, None) == nf.NF_ERR_INVALID_ARG
+    assert lib.nf_bucket_table_init(16, op, 2, fake, need - 1, None) == nf.NF_ERR_WORKSPACE
+    assert lib.nf_bucket_table_init(16, op, 2, None, need, None) == nf.NF_ERR_INVALID_ARG
+    assert lib.nf_bucket_table_init(16, op, 2, P(0x1008), need, None) == nf.NF_ERR_ALIGNMENT
+    assert lib.nf_route_bucket_table(fake, 1 << 10, 16, op, 2, None, fake, ctypes.byref(pol), fake, 16, None,
+                                     fake, fake, fake, ws, 1 << 24, None) == nf.NF_ERR_INVALID_ARG
+    assert lib.nf_route_bucket_table(fake, 1 << 10, 16, op, 2, P(0x1008), fake, ctypes.byref(pol), fake, 16, None,
+                                     fake, fake, fake, ws, 1 << 24, None) == nf.NF_ERR_ALIGNMENT
+    # a row stride shorter than n_total = offsets[nb]
+    assert lib.nf_route_bucket_table(fake, 996, 16, op, 2, fake, fake, ctypes.byref(pol), fake, 16, None,
+                                     fake, fake, fake, ws, 1 << 24, None) == nf.NF_ERR_INVALID_ARG
+
+
 def test_sliced_sizes():
     ne, seg = ctypes.c_int64(), ctypes.c_int64()
     ln = np.array([1, 65536, 65537, 200_000], dtype=np.int64)

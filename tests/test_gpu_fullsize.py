@@ -35,12 +35,18 @@ RANGE = 1 << 20  # elements per oracle range of the one-bucket stress workload (
 class Full:
     """A full-size workload on the device and one route call over it."""
 
-    def __init__(self, name, pol):
+    def __init__(self, name, pol, ddp=False):
+        """ddp: buckets cut at tensor boundaries (synth.ddp_offsets) and
+        routed through the bucket-table driver; else equal buckets."""
         self.lay = lay = synth.CONFIGS[name]()
         d = torch.device("cuda:0")
-        self.W, self.n, self.bn, self.nb = lay.W, lay.n_total, lay.bucket_n, lay.nb
+        self.W, self.n = lay.W, lay.n_total
+        self.off = synth.ddp_offsets(lay) if ddp else \
+            np.array(list(range(0, self.n, lay.bucket_n)) + [self.n], np.int64)
+        self.nb = len(self.off) - 1
         nw = (self.n + 63) // 64
-        print(f"[fullsize] {name}: W={self.W} n={self.n:,} buckets={self.nb}", flush=True)
+        print(f"[fullsize] {name}: W={self.W} n={self.n:,} buckets={self.nb} ({'DDP' if ddp else 'equal'})",
+              flush=True)
         self.g = torch.empty((self.W, lay.stride), dtype=torch.float32, device=d)
         synth.generate_device(lay, self.g)
         mask_dev, self.mask_o = oracle_masks(lay)
@@ -50,10 +56,17 @@ class Full:
         self.out = torch.full((self.n,), float("nan"), dtype=torch.float32, device=d)
         stats = torch.zeros(self.nb * self.W * nf.STATS_BYTES, dtype=torch.uint8, device=d)
         dec = torch.zeros(self.nb * nf.DECISION_BYTES, dtype=torch.uint8, device=d)
-        ws = nf.empty_workspace(nf.nf_workspace_bytes_buckets(self.W, self.n, self.bn), d)
         self.pol = pol
-        nf.nf_route_buckets(self.g, self.n, self.bn, mask, pol, self.bits, self.counts, self.out,
-                            stats, dec, ws)
+        if ddp:
+            table = torch.empty(nf.nf_bucket_table_bytes(self.W, self.off), dtype=torch.uint8, device=d)
+            nf.nf_bucket_table_init(self.W, self.off, table)
+            ws = nf.empty_workspace(nf.nf_workspace_bytes_table(self.W, self.off), d)
+            nf.nf_route_bucket_table(self.g, self.off, table, mask, pol, self.bits, self.counts, self.out,
+                                     stats, dec, ws)
+        else:
+            ws = nf.empty_workspace(nf.nf_workspace_bytes_buckets(self.W, self.n, lay.bucket_n), d)
+            nf.nf_route_buckets(self.g, self.n, lay.bucket_n, mask, pol, self.bits, self.counts, self.out,
+                                stats, dec, ws)
         torch.cuda.synchronize()
         self.stats = nf.stats_host(stats, self.W, self.nb)
         self.dec = nf.decisions_host(dec, self.nb)
@@ -67,7 +80,7 @@ class Full:
         """Every output of bucket b against the oracle on that bucket.  A
         route the policy fixes before reading writes no sign words, and its
         |g| sums and scale are the exact ones rounded once."""
-        a, e = b * self.bn, min((b + 1) * self.bn, self.n)
+        a, e = int(self.off[b]), int(self.off[b + 1])
         ka, ke = a // 64, (e + 63) // 64
         gh = self.g[:, a:e].cpu().numpy()
         mw = np.ascontiguousarray(self.mask_o[ka:ke])
@@ -108,6 +121,20 @@ def test_fullsize_fanin255_vetoed_mean():
     try:
         routes = f.check_every_bucket()
         assert all(r == nfo.ROUTE_F for r in routes), routes
+    finally:
+        f.release()
+
+
+@pytest.mark.parametrize("name", ["vitb16", "fanin255", "gpt1p3b"])
+def test_fullsize_ddp_buckets_every_bucket(name):
+    """Buckets as DDP cuts the model (25 MiB capacity, closed at tensor
+    boundaries, the first of 1 MiB; GPT scale: 73 buckets of 16.8M to 107M
+    elements) through the bucket-table driver, every bucket in full."""
+    f = Full(name, nf.policy(), ddp=True)
+    try:
+        routes = f.check_every_bucket()
+        assert set(routes) <= {nfo.ROUTE_L, nfo.ROUTE_P} and nfo.ROUTE_L in routes, routes
+        print(f"[fullsize] {name} DDP buckets: {f.nb} checked, routes {routes}", flush=True)
     finally:
         f.release()
 

@@ -30,10 +30,15 @@ RANGE = 1 << 20  # elements per oracle range of the one-bucket stress workload (
 
 
 class FullTernary:
-    def __init__(self, name, pol):
+    def __init__(self, name, pol, ddp=False):
+        """ddp: buckets cut at tensor boundaries through the bucket-table
+        driver; else equal buckets."""
         self.lay = lay = synth.CONFIGS[name]()
         d = torch.device("cuda:0")
-        self.W, self.n, self.bn, self.nb = lay.W, lay.n_total, lay.bucket_n, lay.nb
+        self.W, self.n = lay.W, lay.n_total
+        self.off = synth.ddp_offsets(lay) if ddp else \
+            np.array(list(range(0, self.n, lay.bucket_n)) + [self.n], np.int64)
+        self.nb = len(self.off) - 1
         nw = (self.n + 63) // 64
         print(f"[fullsize-ternary] {name}: W={self.W} n={self.n:,} buckets={self.nb}", flush=True)
         self.g = torch.empty((self.W, lay.stride), dtype=torch.float32, device=d)
@@ -45,9 +50,17 @@ class FullTernary:
         self.out = torch.full((self.n,), float("nan"), dtype=torch.float32, device=d)
         stats = torch.zeros(self.nb * self.W * nf.STATS_BYTES, dtype=torch.uint8, device=d)
         dec = torch.zeros(self.nb * nf.DECISION_BYTES, dtype=torch.uint8, device=d)
-        ws = nf.empty_workspace(nf.nf_workspace_bytes_buckets(self.W, self.n, self.bn), d)
         self.pol = pol
-        nf.nf_route_buckets(self.g, self.n, self.bn, mask, pol, self.bits, self.counts, self.out, stats, dec, ws)
+        if ddp:
+            table = torch.empty(nf.nf_bucket_table_bytes(self.W, self.off), dtype=torch.uint8, device=d)
+            nf.nf_bucket_table_init(self.W, self.off, table)
+            ws = nf.empty_workspace(nf.nf_workspace_bytes_table(self.W, self.off), d)
+            nf.nf_route_bucket_table(self.g, self.off, table, mask, pol, self.bits, self.counts, self.out, stats,
+                                     dec, ws)
+        else:
+            ws = nf.empty_workspace(nf.nf_workspace_bytes_buckets(self.W, self.n, lay.bucket_n), d)
+            nf.nf_route_buckets(self.g, self.n, lay.bucket_n, mask, pol, self.bits, self.counts, self.out, stats,
+                                dec, ws)
         torch.cuda.synchronize()
         self.stats = nf.stats_host(stats, self.W, self.nb)
         self.dec = nf.decisions_host(dec, self.nb)
@@ -58,7 +71,7 @@ class FullTernary:
         torch.cuda.empty_cache()
 
     def check_bucket(self, b):
-        a, e = b * self.bn, min((b + 1) * self.bn, self.n)
+        a, e = int(self.off[b]), int(self.off[b + 1])
         ka, ke = a // 64, (e + 63) // 64
         res = dict(bits=self.bits[:, ka:ke].cpu().numpy().view(np.uint64),
                    counts=np.concatenate([self.counts[a:e].cpu().numpy(),
@@ -88,6 +101,19 @@ def test_fullsize_ternary_fanin255_every_bucket():
         with ThreadPoolExecutor(POOL) as ex:
             routes = list(ex.map(f.check_bucket, range(f.nb)))
         assert all(r == nfo.ROUTE_L for r in routes), routes
+    finally:
+        f.release()
+
+
+@pytest.mark.parametrize("name", ["vitb16", "fanin255"])
+def test_fullsize_ternary_ddp_buckets_every_bucket(name):
+    """G-Ternary over buckets cut as DDP cuts the model, through the
+    bucket-table driver, every bucket in full."""
+    f = FullTernary(name, nf.policy(format=nf.NF_FORMAT_TERNARY, tau=0.5), ddp=True)
+    try:
+        with ThreadPoolExecutor(POOL) as ex:
+            routes = list(ex.map(f.check_bucket, range(f.nb)))
+        assert set(routes) <= {nfo.ROUTE_L, nfo.ROUTE_P} and nfo.ROUTE_L in routes, routes
     finally:
         f.release()
 
