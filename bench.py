@@ -760,7 +760,10 @@ def main():
     cpu = None if args.no_cpu_baseline else wl.cpu_baseline(pol, 10.0)
 
     # HBM bytes per pass-1 launch from the committed counters (null unless taken on this kernel source)
-    traffic = counter_traffic(name) if not ternary else None
+    if args.ddp_buckets:
+        traffic = None if ternary else pass1_traffic(committed_counters(name, "ddp"))
+    else:
+        traffic = counter_traffic(name) if not ternary else None
     roofline = dict(m["pass1"])
     roofline["traffic"] = traffic
     roofline["traffic_gbs"] = (None if traffic is None else
