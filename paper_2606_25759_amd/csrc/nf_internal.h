@@ -16,16 +16,20 @@ namespace nf {
 // Pass 1 is worker-major: a block is 16 wavefronts; wavefront v serves
 // worker group wg = v % WG and element group eg = v / WG.  With W <= 16 each
 // wavefront owns one worker (WG = W) and the spare wavefronts take further
-// element groups (EG = 16 / W); with 16 < W <= 64 each wavefront owns
-// ceil(W / 16) workers.  Above 64 workers the rows go in ceil(W / 64)
-// groups of near-equal size, one after another (a launch sequence per
-// group, all with the geometry of the largest): sixteen workers per
-// wavefront held 32 FP64 health sums per lane and spilled (W = 255: pass 1
-// at 2.9 TB/s).  Every group then has at least 32 rows, so each of the 16
-// wavefronts' first worker exists in every group.  The groups share the
-// chunk slots (each writes its own workers' partials) and carry the FP32
-// sums at routed positions from one to the next through the output, so the
-// workers are still added in order.  A tile is EG * T consecutive elements of all W
+// element groups (EG = 16 / W); with 16 < W <= 32 each wavefront owns
+// ceil(W / 16) workers.  Above 32 workers the rows go in groups of
+// near-equal size, one after another (a launch sequence per group, all
+// with the geometry of the largest): two groups up to 64 workers, then
+// ceil(W / 64).  Sixteen workers per wavefront held 32 FP64 health sums per
+// lane and spilled (W = 255: pass 1 at 2.9 TB/s); at W = 64, two groups of
+// 32 (two workers per wavefront, eight wavefronts per SIMD, two blocks per
+// compute unit) ran the stress bucket's G-Ternary step 4% faster than one
+// group of 64, while at W = 255 groups of 32 ran 26% slower than groups of
+// 64.  Every group has at least 16 rows, so each of the 16 wavefronts'
+// first worker exists in every group.  The groups share the chunk slots
+// (each writes its own workers' partials) and carry the FP32 sums at routed
+// positions from one to the next through the output, so the workers are
+// still added in order.  A tile is EG * T consecutive elements of all W
 // rows; staging one tile of all workers in LDS (to add the workers in order
 // at FP32-routed positions) takes at most 64 KiB.
 //
@@ -40,7 +44,8 @@ namespace nf {
 // One chunk per compute unit (256 on MI355X) per launch is the best epoch
 // measured (128: -30%, 192 and 384: -7%, 512: -4%, 1024: -7%).
 constexpr int kWaves = 16;
-constexpr int kRowGroup = 64;  // worker rows per pass-1 group at most
+constexpr int kRowGroup = 64;     // worker rows per pass-1 group at most
+constexpr int kWideWorkers = 32;  // above this: row groups, the decision's thread-per-worker reduction
 constexpr int kThreads1 = kWaves * 64;
 constexpr int kStageFloats = 16384;      // 64 KiB of LDS
 #ifndef NF_BITS_WORDS
@@ -57,8 +62,9 @@ constexpr int kStageFloats = 16384;      // 64 KiB of LDS
 #endif
 constexpr int kBitsWords = NF_BITS_WORDS;      // LDS words for a chunk's sign words (32 KiB)
 constexpr int kMaxSlots = 512;                 // partials the decision reduces per bucket at most
-// ... above 64 workers (the decision then reads 64 * W partials per bucket:
-// with 400 of 255 workers each, a 25 MiB bucket's decision took 0.28 ms)
+// ... above kWideWorkers workers (the decision then reads 64 * W partials
+// per bucket: with 400 of 255 workers each, a 25 MiB bucket's decision
+// took 0.28 ms)
 constexpr int kMaxSlotsWide = 64;
 constexpr int kEpochBlocks = NF_EPOCH_BLOCKS;  // chunks per pass-1 launch
 // Without sign words (statistics and routed sums only) the writes are few and
@@ -139,7 +145,7 @@ inline void row_group(const Geometry& g, int i, int* wbase, int* rows) {
 inline Geometry geometry_core(int W) {
   Geometry g;
   g.W = W;
-  g.ngroups = W > kRowGroup ? (W + kRowGroup - 1) / kRowGroup : 1;
+  g.ngroups = W > kRowGroup ? (W + kRowGroup - 1) / kRowGroup : (W > kWideWorkers ? 2 : 1);
   g.rows = (W + g.ngroups - 1) / g.ngroups;
   const int R = g.rows;  // the pass-1 kernel's workers
   g.wg = R < kWaves ? R : kWaves;
@@ -181,7 +187,7 @@ inline void slot_groups(Geometry& g, int64_t max_len) {
   // is first summed in groups of gs consecutive slots (at most that many
   // groups), which the decision reads.
   g.slots = (int)(g.chunks_full > 1 ? g.chunks_full : 1);
-  const int cap = g.W > kRowGroup ? kMaxSlotsWide : kMaxSlots;
+  const int cap = g.W > kWideWorkers ? kMaxSlotsWide : kMaxSlots;
   g.gs = g.chunks_full > cap ? (int)ceil_div(g.chunks_full, cap) : 0;
   g.groups = g.gs ? (int)ceil_div(g.chunks_full, g.gs) : 0;
   int64_t words = (max_len + 63) / 64;

@@ -825,10 +825,11 @@ __global__ __launch_bounds__(256) void k_slotsum(DecideArgs a) {
   }
 }
 
-// 1024 threads: up to 64 workers, sixteen wavefronts take the workers in
-// turn (at W = 64, four each), the lanes of one splitting its slots, so
-// that fewer slot sums wait on each other.  Above 64 workers (a wavefront
-// would take up to sixteen in turn: 0.28 ms at W = 255) thread t takes
+// 1024 threads: up to 32 workers, sixteen wavefronts take the workers in
+// turn (at W = 32, two each), the lanes of one splitting its slots, so
+// that fewer slot sums wait on each other.  Above 32 workers (a wavefront
+// would take up to sixteen in turn: 0.28 ms at W = 255; at W = 64 this
+// way halves the stress bucket's decision, 88 -> 38 us) thread t takes
 // worker t % W and every P-th slot from t / W, P the largest power of two
 // with P * W <= 1024; the P parts of a worker are then added in order.
 constexpr int kDecideThreads = 1024;
@@ -855,7 +856,7 @@ __global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
   const int used = (int)(two ? (chunks + a.gs - 1) / a.gs : chunks);
   // The slot loops are unrolled so that their loads are in flight together;
   // the adds keep their order.
-  if (a.W > kRowGroup) {
+  if (a.W > kWideWorkers) {
     int parts = 1;
     while (2 * parts * a.W <= kDecideThreads) parts *= 2;
     const int t = threadIdx.x;

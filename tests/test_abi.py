@@ -293,8 +293,9 @@ def test_pass1_launch_counts():
 def test_pass1_chunk_geometry():
     # W = 16: tiles of 512 elements, 32 per chunk; a 25 MiB bucket has 400 chunks
     assert nf.nf_pass1_chunk_elems(16, 6_553_600 * 201, 6_553_600) == (16_384, 400)
-    # W = 64: four workers per wavefront, tiles of 256 elements, 16 per chunk
-    assert nf.nf_pass1_chunk_elems(64, 100_000_000, 100_000_000) == (4_096, 24_415)
+    # W = 64: two row groups of 32, two workers per wavefront, tiles of 256 elements, 32 per chunk
+    assert nf.nf_pass1_chunk_elems(64, 100_000_000, 100_000_000) == (8_192, 12_208)
+    assert nf.nf_pass1_launches(64, 100_000_000, 100_000_000) == 2 * 48
     # W > 64: rows in ceil(W / 64) near-equal groups, with the geometry of the
     # largest (255: four of 64 or 63 rows; 65: 33 and 32 rows, tiles of 256
     # elements, 31 per chunk)

@@ -53,7 +53,7 @@ def run_binary(W, n, bucket_n, seed):
     (16, 9_000_000, 9_000_000, 1, 1),      # 977 chunks of 18 tiles
     (16, 20_000_000, 20_000_000, 5, 2),    # 1,221 chunks of 32 tiles: five launches, groups of 3
     (16, 20_000_000, 9_000_000, 5, 2),     # three buckets, the last of 123 chunks
-    (64, 3_000_000, 3_000_000, 1, 1),      # 977 chunks, four workers per wavefront
+    (64, 3_000_000, 3_000_000, 2, 2),      # 977 chunks, two row groups of 32 (a launch each)
     (255, 600_000, 600_000, 4, 4),         # 782 chunks, one launch per group of 64 worker rows;
                                            # partials summed in groups of 13 (at most 64 per worker)
     (16, 1_000_000, 1_000_000, 1, 1),      # 977 chunks of 2 tiles
