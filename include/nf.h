@@ -421,7 +421,10 @@ nf_status nf_route_bucket(const float* grads, int64_t worker_stride, int32_t W, 
  * unless bucket_n >= n_total.  stats is [nb][W], decisions is [nb] (device).
  * Per bucket, the results equal those of nf_route_bucket on that bucket (with
  * the ternary format, c- of bucket b starts at counts + n_total + b*bucket_n).
+ * At most NF_MAX_BUCKETS buckets per call (NF_ERR_INVALID_ARG beyond: the
+ * read side runs a launch-grid row per bucket).
  */
+#define NF_MAX_BUCKETS 65535
 size_t nf_workspace_bytes_buckets(int32_t W, int64_t n_total, int64_t bucket_n);
 nf_status nf_route_buckets(const float* grads, int64_t worker_stride, int32_t W,
                            int64_t n_total, int64_t bucket_n, const uint64_t* mask,
@@ -477,7 +480,8 @@ nf_status nf_route_buckets_noalloc(const float* grads, int64_t worker_stride, in
  * nf_route_bucket_table reads the table and needs the same W and offsets it
  * was built with (not checked on the device: another table gives wrong
  * results or invalid accesses).  Errors as nf_route_buckets, and
- * NF_ERR_INVALID_ARG for invalid offsets, NF_ERR_WORKSPACE for a short table.
+ * NF_ERR_INVALID_ARG for invalid offsets or nb above NF_MAX_BUCKETS,
+ * NF_ERR_WORKSPACE for a short table.
  */
 size_t nf_bucket_table_bytes(int32_t W, const int64_t* bucket_offsets, int32_t nb);
 nf_status nf_bucket_table_init(int32_t W, const int64_t* bucket_offsets, int32_t nb, void* table,

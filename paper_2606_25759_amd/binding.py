@@ -493,6 +493,7 @@ def nf_route_buckets(grads, n_total, bucket_n, mask, pol, bits, counts, out, sta
 
 
 NF_STATIC_SCRATCH_BYTES = 64 << 20
+NF_MAX_BUCKETS = 65535  # buckets per driver call at most
 
 
 def nf_route_buckets_noalloc(grads, n_total, bucket_n, mask, pol, bits, counts, out, stats, decisions,

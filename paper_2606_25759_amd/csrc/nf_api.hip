@@ -19,6 +19,7 @@ namespace {
 // each device's address comes from hipGetSymbolAddress, taken once per
 // device on the first call there, and only that address reaches a kernel.
 constexpr size_t kStaticScratchBytes = (size_t)NF_STATIC_SCRATCH_BYTES;
+constexpr int kMaxBuckets = NF_MAX_BUCKETS;
 __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
 constexpr int kMaxDevices = 64;
 std::mutex g_scratch_mu;
@@ -236,6 +237,9 @@ nf_status route_geo(const nf::Geometry& geo, const float* g, int64_t stride, int
                     nf_worker_stats* stats, nf_route_decision* dec, void* ws, size_t ws_bytes, void* stream,
                     const nf::BucketRow* btab, const int32_t* cbucket) {
   const int64_t n_total = geo.n_total;
+  // pass 2 and the G-Ternary count run a grid row per bucket
+  if (geo.nb > kMaxBuckets)
+    return fail(NF_ERR_INVALID_ARG, "%lld buckets, at most %d per call", (long long)geo.nb, kMaxBuckets);
   NF_TRY(check_ws(ws, ws_bytes, nf::workspace_layout(geo).total));
   // The policy alone fixes the route when low-bit is not admitted, vetoed
   // or guard-rejected (and not forced): then no sign payload is built and
@@ -312,6 +316,7 @@ nf_status route_flat(const float* g, int64_t stride, int32_t W, int64_t n_total,
 // bucket start a multiple of 64 (its bitmap words start at off[b] / 64).
 nf_status check_table_offsets(const int64_t* off, int32_t nb) {
   if (nb < 1) return fail(NF_ERR_INVALID_ARG, "nb=%d: a bucket table needs at least one bucket", nb);
+  if (nb > kMaxBuckets) return fail(NF_ERR_INVALID_ARG, "nb=%d buckets, at most %d", nb, kMaxBuckets);
   if (!off) return fail(NF_ERR_INVALID_ARG, "bucket_offsets is NULL");
   if (off[0] != 0) return fail(NF_ERR_INVALID_ARG, "bucket_offsets[0]=%lld, must be 0", (long long)off[0]);
   for (int32_t b = 0; b < nb; ++b) {

@@ -265,6 +265,15 @@ def test_bucket_table_sizes_and_argument_errors():
                                      fake, fake, fake, ws, 1 << 24, None) == nf.NF_ERR_INVALID_ARG
     assert lib.nf_route_bucket_table(fake, 1 << 10, 16, op, 2, P(0x1008), fake, ctypes.byref(pol), fake, 16, None,
                                      fake, fake, fake, ws, 1 << 24, None) == nf.NF_ERR_ALIGNMENT
+    # more buckets than a launch-grid row holds, in both drivers, before any launch
+    many = np.arange(0, 64 * 65_537, 64, dtype=np.int64)  # 65,536 buckets of 64
+    assert nf.nf_bucket_table_bytes(16, many) == 0
+    assert lib.nf_route_bucket_table(fake, 1 << 23, 16, many.ctypes.data_as(P), len(many) - 1, fake, fake,
+                                     ctypes.byref(pol), fake, 1 << 17, None, fake, fake, fake, ws, 1 << 30,
+                                     None) == nf.NF_ERR_INVALID_ARG
+    assert lib.nf_route_buckets(fake, 1 << 23, 16, 64 * 65_536, 64, fake, ctypes.byref(pol), fake, 1 << 17, None,
+                                fake, fake, fake, ws, 1 << 30, None) == nf.NF_ERR_INVALID_ARG
+    assert "at most 65535" in nf.nf_last_error()
     # a row stride shorter than n_total = offsets[nb]
     assert lib.nf_route_bucket_table(fake, 996, 16, op, 2, fake, fake, ctypes.byref(pol), fake, 16, None,
                                      fake, fake, fake, ws, 1 << 24, None) == nf.NF_ERR_INVALID_ARG
