@@ -386,6 +386,33 @@ def sliced_run(args, reps=5):
     return 0
 
 
+def pattern_probe(synth, torch, wl, reps=3):
+    """The first pass's read schedule without its arithmetic (16 rows in
+    chunks of 16 x 16,384 elements, launches of 256 chunks), alone and with
+    1/32 of the bytes read written back as 2 KiB rows at each chunk's end
+    (the sign words' share and layout): the rates the reducer's first pass
+    is bounded by on this machine."""
+    n = wl.n // 16384 * 16384
+    res = {"elements_per_row": n}
+    dst = torch.empty((16, n // 64), dtype=torch.int64, device=wl.dev)  # not the reducer's outputs
+    for store in (0, 1):
+        synth.pattern_probe(wl.grads, dst, n, store)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            launches = synth.pattern_probe(wl.grads, dst, n, store)
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3 / reps
+        nbytes = 4 * 16 * n + (2 * n if store else 0)
+        res["read_write" if store else "read_only"] = {"ms": round(ms, 3), "gbs": round(nbytes / ms / 1e6, 1),
+                                                        "bytes": nbytes, "launches": launches}
+    del dst
+    print(f"[bench] first-pass pattern probe: reads only {res['read_only']['ms']:.3f} ms "
+          f"({res['read_only']['gbs']} GB/s), with the 1/32 writes {res['read_write']['ms']:.3f} ms "
+          f"({res['read_write']['gbs']} GB/s)", file=sys.stderr, flush=True)
+    return res
+
+
 def split_one_bucket(nf, torch, grads, mask, W, n, n_e, reps=10):
     """Device time of each standalone entry point on one bucket of n elements
     (the first), with the algorithmic bytes each one moves."""
@@ -745,7 +772,7 @@ def main():
                                  int(nf.decisions_host(wl.dec, wl.nb)["n_eligible"][0]))
         print(f"[bench] standalone, first bucket: " + ", ".join(f"{k} {v['ms']:.3f} ms" for k, v in split.items()
                                                             if isinstance(v, dict)), file=sys.stderr, flush=True)
-    achievable = None
+    achievable = pattern = None
     if not args.no_probe:
         sink = torch.zeros(1024, dtype=torch.float32, device=wl.dev)
         synth.read_probe(wl.grads, sink)
@@ -757,6 +784,8 @@ def main():
         probe_ms = (time.perf_counter() - a0) * 1e3 / 3
         achievable = round(4 * wl.grads.numel() / (probe_ms * 1e-3) / 1e9, 1)
         print(f"[bench] streaming read of the input: {achievable} GB/s", file=sys.stderr, flush=True)
+        if wl.W == 16:
+            pattern = pattern_probe(synth, torch, wl)
     cpu = None if args.no_cpu_baseline else wl.cpu_baseline(pol, 10.0)
 
     # HBM bytes per pass-1 launch from the committed counters (null unless taken on this kernel source)
@@ -791,6 +820,7 @@ def main():
         "roofline": roofline,
         "phases_ms": m["phases_ms"],
         "achievable_read_gbs": achievable,
+        "pass1_pattern_probe": pattern,
         "split_one_bucket": split,
         "routes": m["routes"],
         "mgtr": m["mgtr"],

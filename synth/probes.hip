@@ -5,6 +5,15 @@
 //   nfs_copy        copies n floats with 128-bit loads and stores (a kernel
 //                   of known traffic, 4n bytes each way, used to scale the
 //                   hardware byte counters)
+//   nfs_pattern_probe  reads 16 rows in the reducer's first-pass schedule
+//                   (chunks of 16 x 16,384 elements, a row per wavefront,
+//                   512-element tiles with the next one in flight, launches
+//                   of 256 chunks that may overlap) and, if asked, writes 1/32
+//                   of the bytes read as 2 KiB rows at each chunk's end: the
+//                   read pattern alone and with the writes mixed in, without
+//                   the reducer's arithmetic (each word is a ballot of a data
+//                   bit)
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -27,6 +36,60 @@ __global__ __launch_bounds__(1024) void k_copy(const f4* __restrict__ src, f4* _
     dst[i] = __builtin_nontemporal_load(src + i);
 }
 
+constexpr int kPatRows = 16;       // rows: one per wavefront
+constexpr int kPatChunk = 16384;   // elements per row and chunk
+constexpr int kPatEpoch = 256;     // chunks per launch
+
+// Block = chunk c of every row; wavefront v = row v.  Lane l loads element
+// 64k + l of each 512-element tile's eight words; the word of 64 elements
+// is the ballot of their lowest mantissa bit.
+template <bool STORE>
+__global__ __launch_bounds__(1024) void k_pattern(const float* __restrict__ src, int64_t stride,
+                                                  uint64_t* __restrict__ dst, int64_t dstride, int64_t q0,
+                                                  int64_t nchunks) {
+  __shared__ uint64_t words[kPatRows * (kPatChunk / 64)];
+  const int64_t c = q0 + blockIdx.x;
+  if (c >= nchunks) return;
+  const int v = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const float* row = src + (int64_t)v * stride + c * kPatChunk + lane;
+  float xa[8], xb[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) xa[k] = __builtin_nontemporal_load(row + 64 * k);
+  for (int t = 0; t < kPatChunk / 512; t += 2) {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) xb[k] = __builtin_nontemporal_load(row + (t + 1) * 512 + 64 * k);
+    uint64_t my = 0;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const uint64_t b = __ballot((__float_as_uint(xa[k]) & 1u) != 0u);
+      if (lane == k) my = b;
+    }
+    if (lane < 8) words[v * (kPatChunk / 64) + t * 8 + lane] = my;
+    const int tn = t + 2 < kPatChunk / 512 ? t + 2 : 0;  // the last issue re-reads the chunk's first tile
+#pragma unroll
+    for (int k = 0; k < 8; ++k) xa[k] = __builtin_nontemporal_load(row + tn * 512 + 64 * k);
+    my = 0;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const uint64_t b = __ballot((__float_as_uint(xb[k]) & 1u) != 0u);
+      if (lane == k) my = b;
+    }
+    if (lane < 8) words[v * (kPatChunk / 64) + (t + 1) * 8 + lane] = my;
+  }
+  uint32_t keep = 0;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) keep ^= __float_as_uint(xa[k]);
+  __syncthreads();
+  if (STORE) {
+    for (int i = threadIdx.x; i < kPatRows * (kPatChunk / 64); i += 1024) {
+      const int r = i / (kPatChunk / 64), o = i - r * (kPatChunk / 64);
+      dst[(int64_t)r * dstride + c * (kPatChunk / 64) + o] = words[i];
+    }
+  } else if (keep == 0x9e3779b9u && lane == 0) {
+    dst[0] = words[threadIdx.x];  // keeps the words live; practically never taken
+  }
+}
+
 bool bad(const void* p, int64_t n) { return ((uintptr_t)p & 15) != 0 || n < 0 || (n & 3) != 0; }
 
 }  // namespace
@@ -38,6 +101,32 @@ extern "C" int nfs_read_probe(const float* src, int64_t n, float* sink, void* st
   hipLaunchKernelGGL(k_read, dim3(4096), dim3(1024), 0, (hipStream_t)stream, reinterpret_cast<const f4*>(src),
                      n / 4, sink);
   return hipGetLastError() == hipSuccess ? 0 : 2;
+}
+
+// 16 rows of n floats at src + r * stride (n a multiple of 16,384; stride a
+// multiple of 4 and >= n); dst: 16 rows of dstride >= n / 64 words.  With
+// store = 0 nothing is written (dst is touched only by a branch the data
+// practically never takes).  Returns the number of launches, or -1.
+extern "C" int nfs_pattern_probe(const float* src, int64_t stride, int64_t n, uint64_t* dst, int64_t dstride,
+                                 int store, void* stream) {
+  if (((uintptr_t)src & 15) || (stride & 3) || stride < n || n <= 0 || n % kPatChunk || dstride < n / 64 ||
+      ((uintptr_t)dst & 7))
+    return -1;
+  const int64_t nchunks = n / kPatChunk;
+  int launches = 0;
+  for (int64_t q0 = 0; q0 < nchunks; q0 += kPatEpoch, ++launches) {
+    const int64_t left = nchunks - q0;
+    const dim3 grid((unsigned)(left < kPatEpoch ? left : kPatEpoch));
+    const uint32_t fl = q0 > 0 ? hipExtAnyOrderLaunch : 0u;
+    if (store)
+      hipExtLaunchKernelGGL(k_pattern<true>, grid, dim3(1024), 0, (hipStream_t)stream, nullptr, nullptr, fl, src,
+                            stride, dst, dstride, q0, nchunks);
+    else
+      hipExtLaunchKernelGGL(k_pattern<false>, grid, dim3(1024), 0, (hipStream_t)stream, nullptr, nullptr, fl, src,
+                            stride, dst, dstride, q0, nchunks);
+    if (hipGetLastError() != hipSuccess) return -1;
+  }
+  return launches;
 }
 
 // n: floats, a multiple of 4; src and dst 16-byte aligned, not overlapping.
