@@ -390,12 +390,13 @@ def pattern_probe(synth, torch, wl, reps=3):
     """The first pass's read schedule without its arithmetic (16 rows in
     chunks of 16 x 16,384 elements, launches of 256 chunks), alone and with
     1/32 of the bytes read written back as 2 KiB rows at each chunk's end
-    (the sign words' share and layout): the rates the reducer's first pass
-    is bounded by on this machine."""
+    (the sign words' share and layout), or 2/32 (two planes, the G-Ternary
+    pack's share): the rates the reducer's first pass and the pack are
+    bounded by on this machine."""
     n = wl.n // 16384 * 16384
     res = {"elements_per_row": n}
-    dst = torch.empty((16, n // 64), dtype=torch.int64, device=wl.dev)  # not the reducer's outputs
-    for store in (0, 1):
+    dst = torch.empty((32, n // 64), dtype=torch.int64, device=wl.dev)  # not the reducer's outputs
+    for store in (0, 1, 2):
         synth.pattern_probe(wl.grads, dst, n, store)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
@@ -403,13 +404,14 @@ def pattern_probe(synth, torch, wl, reps=3):
             launches = synth.pattern_probe(wl.grads, dst, n, store)
         torch.cuda.synchronize()
         ms = (time.perf_counter() - t0) * 1e3 / reps
-        nbytes = 4 * 16 * n + (2 * n if store else 0)
-        res["read_write" if store else "read_only"] = {"ms": round(ms, 3), "gbs": round(nbytes / ms / 1e6, 1),
-                                                        "bytes": nbytes, "launches": launches}
+        nbytes = 4 * 16 * n + 2 * n * store
+        res[("read_only", "read_write", "read_write_two_planes")[store]] = {
+            "ms": round(ms, 3), "gbs": round(nbytes / ms / 1e6, 1), "bytes": nbytes, "launches": launches}
     del dst
     print(f"[bench] first-pass pattern probe: reads only {res['read_only']['ms']:.3f} ms "
           f"({res['read_only']['gbs']} GB/s), with the 1/32 writes {res['read_write']['ms']:.3f} ms "
-          f"({res['read_write']['gbs']} GB/s)", file=sys.stderr, flush=True)
+          f"({res['read_write']['gbs']} GB/s), with 2/32 {res['read_write_two_planes']['ms']:.3f} ms "
+          f"({res['read_write_two_planes']['gbs']} GB/s)", file=sys.stderr, flush=True)
     return res
 
 

@@ -9,6 +9,7 @@
 //                   (chunks of 16 x 16,384 elements, a row per wavefront,
 //                   512-element tiles with the next one in flight, launches
 //                   of 256 chunks that may overlap) and, if asked, writes 1/32
+//                   (or 2/32: two rows of words per row, as two bit planes)
 //                   of the bytes read as 2 KiB rows at each chunk's end: the
 //                   read pattern alone and with the writes mixed in, without
 //                   the reducer's arithmetic (each word is a ballot of a data
@@ -43,7 +44,7 @@ constexpr int kPatEpoch = 256;     // chunks per launch
 // Block = chunk c of every row; wavefront v = row v.  Lane l loads element
 // 64k + l of each 512-element tile's eight words; the word of 64 elements
 // is the ballot of their lowest mantissa bit.
-template <bool STORE>
+template <int NSTORE>
 __global__ __launch_bounds__(1024) void k_pattern(const float* __restrict__ src, int64_t stride,
                                                   uint64_t* __restrict__ dst, int64_t dstride, int64_t q0,
                                                   int64_t nchunks) {
@@ -80,10 +81,12 @@ __global__ __launch_bounds__(1024) void k_pattern(const float* __restrict__ src,
 #pragma unroll
   for (int k = 0; k < 8; ++k) keep ^= __float_as_uint(xa[k]);
   __syncthreads();
-  if (STORE) {
+  if (NSTORE > 0) {
+    // row r of words to dst row r (and to row 16 + r, inverted, for the second plane)
     for (int i = threadIdx.x; i < kPatRows * (kPatChunk / 64); i += 1024) {
       const int r = i / (kPatChunk / 64), o = i - r * (kPatChunk / 64);
       dst[(int64_t)r * dstride + c * (kPatChunk / 64) + o] = words[i];
+      if (NSTORE > 1) dst[(int64_t)(kPatRows + r) * dstride + c * (kPatChunk / 64) + o] = ~words[i];
     }
   } else if (keep == 0x9e3779b9u && lane == 0) {
     dst[0] = words[threadIdx.x];  // keeps the words live; practically never taken
@@ -104,13 +107,14 @@ extern "C" int nfs_read_probe(const float* src, int64_t n, float* sink, void* st
 }
 
 // 16 rows of n floats at src + r * stride (n a multiple of 16,384; stride a
-// multiple of 4 and >= n); dst: 16 rows of dstride >= n / 64 words.  With
-// store = 0 nothing is written (dst is touched only by a branch the data
+// multiple of 4 and >= n); dst: 16 * store rows (16 for store = 0) of
+// dstride >= n / 64 words.  store (0, 1 or 2): rows of words written per row
+// read; with 0 nothing is written (dst is touched only by a branch the data
 // practically never takes).  Returns the number of launches, or -1.
 extern "C" int nfs_pattern_probe(const float* src, int64_t stride, int64_t n, uint64_t* dst, int64_t dstride,
                                  int store, void* stream) {
   if (((uintptr_t)src & 15) || (stride & 3) || stride < n || n <= 0 || n % kPatChunk || dstride < n / 64 ||
-      ((uintptr_t)dst & 7))
+      ((uintptr_t)dst & 7) || store < 0 || store > 2)
     return -1;
   const int64_t nchunks = n / kPatChunk;
   int launches = 0;
@@ -118,11 +122,14 @@ extern "C" int nfs_pattern_probe(const float* src, int64_t stride, int64_t n, ui
     const int64_t left = nchunks - q0;
     const dim3 grid((unsigned)(left < kPatEpoch ? left : kPatEpoch));
     const uint32_t fl = q0 > 0 ? hipExtAnyOrderLaunch : 0u;
-    if (store)
-      hipExtLaunchKernelGGL(k_pattern<true>, grid, dim3(1024), 0, (hipStream_t)stream, nullptr, nullptr, fl, src,
+    if (store == 2)
+      hipExtLaunchKernelGGL(k_pattern<2>, grid, dim3(1024), 0, (hipStream_t)stream, nullptr, nullptr, fl, src,
+                            stride, dst, dstride, q0, nchunks);
+    else if (store == 1)
+      hipExtLaunchKernelGGL(k_pattern<1>, grid, dim3(1024), 0, (hipStream_t)stream, nullptr, nullptr, fl, src,
                             stride, dst, dstride, q0, nchunks);
     else
-      hipExtLaunchKernelGGL(k_pattern<false>, grid, dim3(1024), 0, (hipStream_t)stream, nullptr, nullptr, fl, src,
+      hipExtLaunchKernelGGL(k_pattern<0>, grid, dim3(1024), 0, (hipStream_t)stream, nullptr, nullptr, fl, src,
                             stride, dst, dstride, q0, nchunks);
     if (hipGetLastError() != hipSuccess) return -1;
   }
