@@ -125,7 +125,7 @@ def test_fullsize_fanin255_vetoed_mean():
         f.release()
 
 
-@pytest.mark.parametrize("name", ["vitb16", "fanin255", "gpt1p3b"])
+@pytest.mark.parametrize("name", ["vitb16", "gpt1p3b"])
 def test_fullsize_ddp_buckets_every_bucket(name):
     """Buckets as DDP cuts the model (25 MiB capacity, closed at tensor
     boundaries, the first of 1 MiB; GPT scale: 73 buckets of 16.8M to 107M

@@ -6,6 +6,8 @@ full number of tiles (up to 16 steps of 64 elements per wavefront).  Long
 FP32 runs hold whole routed chunks; non-finite values sit inside them, in
 workers of the first, a middle and the last group.  Every output is checked
 against the oracle: statistics, decision, sign words, counts and values."""
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 import pytest
 import torch
@@ -45,12 +47,18 @@ def test_routed_chunks_wide(W):
     for k, w in enumerate(bad):
         pos = rng.choice(routed, 5, replace=False)
         g_bad[w, pos] = vals[(np.arange(5) + k) % 3]
-    for gg, pol, what in ((g, nf.policy(), "clean"),
-                          (g, nf.policy(fp32_op=nf.NF_FP32_MEAN), "mean"),
-                          (g_bad, nf.policy(), "non-finite"),
-                          (g_bad, nf.policy(force_lowbit=1), "non-finite forced")):
+    cases = ((g, nf.policy(), "clean"),
+             (g, nf.policy(fp32_op=nf.NF_FP32_MEAN), "mean"),
+             (g_bad, nf.policy(), "non-finite"),
+             (g_bad, nf.policy(force_lowbit=1), "non-finite forced"))
+    # every route on the GPU first, then the oracle checks in a pool of host
+    # threads (its calls release the interpreter lock)
+    results = []
+    for gg, pol, what in cases:
         run = H.Bucket(gg, m, n)
-        res = run.route(pol)
-        H.check_route(res, gg, m, n, pol, what=f"W={W} {what}")
-        del run, res
+        results.append(run.route(pol))
+        del run
         torch.cuda.empty_cache()
+    with ThreadPoolExecutor(len(cases)) as ex:
+        list(ex.map(lambda k: H.check_route(results[k], cases[k][0], m, n, cases[k][1], what=f"W={W} {cases[k][2]}"),
+                    range(len(cases))))
