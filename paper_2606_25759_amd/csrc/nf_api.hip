@@ -945,8 +945,14 @@ nf_status nf_bucket_table_init(int32_t W, const int64_t* bucket_offsets, int32_t
   if (table_bytes < need) return fail(NF_ERR_WORKSPACE, "table of %zu bytes < %zu required", table_bytes, need);
   if (!table) return fail(NF_ERR_INVALID_ARG, "table is NULL");
   if (!aligned(table, 256)) return fail(NF_ERR_ALIGNMENT, "table not 256-byte aligned");
-  // Rows and the bucket of every chunk, built here and copied once.
-  std::vector<unsigned char> host(need, 0);
+  // Rows and the bucket of every chunk, built here and copied once (no
+  // exception crosses the C ABI: a failed host allocation is an error code).
+  std::vector<unsigned char> host;
+  try {
+    host.assign(need, 0);
+  } catch (...) {
+    return fail(NF_ERR_WORKSPACE, "no host memory for a %zu-byte table", need);
+  }
   nf::BucketRow* rows = reinterpret_cast<nf::BucketRow*>(host.data());
   int32_t* cb = reinterpret_cast<int32_t*>(host.data() + nf::table_rows_bytes(nb));
   int64_t q = 0;
