@@ -183,7 +183,7 @@ inline void fill_rule(Geometry& g, F total_for) {
 // and words.
 inline void slot_groups(Geometry& g, int64_t max_len) {
   // Every chunk owns a slot, so no two chunks ever touch the same partial.
-  // A bucket of more than kMaxSlots chunks (kMaxSlotsWide above 64 workers)
+  // A bucket of more than kMaxSlots chunks (kMaxSlotsWide above kWideWorkers)
   // is first summed in groups of gs consecutive slots (at most that many
   // groups), which the decision reads.
   g.slots = (int)(g.chunks_full > 1 ? g.chunks_full : 1);

@@ -842,7 +842,7 @@ __global__ __launch_bounds__(kDecideThreads) void k_decide(DecideArgs a) {
   __shared__ uint64_t ne_s;
   __shared__ double med_s;
   __shared__ double qterm[256];  // |g| sum / n_E per worker (the scale's terms)
-  __shared__ Partial wide[kDecideThreads];  // W > 64: [part][W]
+  __shared__ Partial wide[kDecideThreads];  // W > kWideWorkers: [part][W]
   const int b = blockIdx.x;
   const int v = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wavefront index, uniform
   const int lane = threadIdx.x & 63;

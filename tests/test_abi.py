@@ -332,7 +332,7 @@ def test_workspace_sizes():
     assert nf.nf_workspace_bytes_buckets(16, 100, 0) == 0
     # W = 255, two 25 MiB buckets: 1,600 chunk slots each, summed first in
     # 64 groups of 25 (the decision reads at most 64 partials per worker above
-    # 64 workers).
+    # 32 workers).
     c = nf.nf_workspace_bytes_buckets(255, 6_553_600 * 2, 6_553_600)
     assert c == 2 * 1_600 * 255 * 40 + 25_600 + 2 * 64 * 255 * 40 + 1_024
 

@@ -8,7 +8,7 @@ words require) every bucket equals the oracle on that bucket, in both
 formats and under the fused, forced low-bit and vetoed routes, with a
 non-finite value sending one bucket to the fallback; 1,500 small buckets
 (a chunk-to-bucket map of 1,500 entries); buckets of more than 512 chunks
-(more than 64 above 64 workers), whose partials are summed in groups first.
+(more than 64 above 32 workers), whose partials are summed in groups first.
 """
 import numpy as np
 import pytest
@@ -141,12 +141,12 @@ def test_table_many_small_buckets():
 
 @pytest.mark.parametrize("W,big", [(16, 25_000_000), (100, 3_000_000)])
 def test_table_buckets_above_the_slot_threshold(W, big):
-    """Buckets of more than 512 chunks (64 above 64 workers) next to small
+    """Buckets of more than 512 chunks (64 above 32 workers) next to small
     ones: the second-level group sums of each bucket cover its own slots."""
     sizes = [64 * 1000, big // 64 * 64, 4096, 777]
     off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
     _, chunks = nf.nf_pass1_chunk_elems(W, int(off[-1]), big)
-    assert chunks > (512 if W <= 64 else 64), chunks
+    assert chunks > (512 if W <= 32 else 64), chunks
     g, m = layout_for(W, int(off[-1]), 500 + W)
     for pol in (nf.policy(), nf.policy(format=nf.NF_FORMAT_TERNARY, tau=0.5)):
         res = table_route(g, m, off, pol)

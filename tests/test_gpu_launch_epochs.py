@@ -1,5 +1,5 @@
 """Pass-1 launch shapes against the oracle: a bucket small enough for one
-launch, buckets of more than 512 chunks (64 above 64 workers: their
+launch, buckets of more than 512 chunks (64 above 32 workers: their
 per-chunk partials are summed in groups before the decision), in one launch and in several launches that
 may overlap, and a flat buffer of several buckets in one launch.  Every
 output of every bucket is checked (G-Binary and G-Ternary)."""

@@ -182,7 +182,7 @@ def test_route_bucket_large(W):
 @pytest.mark.parametrize("W", [65, 128, 129, 200])
 @pytest.mark.parametrize("kind", ["default", "veto_mean", "forced_mean"])
 def test_route_row_groups(W, kind):
-    """Above 64 workers pass 1 reads the worker rows in groups of 64, the
+    """Above 64 workers pass 1 reads the worker rows in groups of up to 64, the
     FP32 sums at routed positions carried from one group to the next in the
     output.  Two buckets: the first clean, the second with a NaN and an
     infinity at routed positions in different groups and a routed position
