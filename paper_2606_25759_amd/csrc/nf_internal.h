@@ -82,6 +82,13 @@ constexpr int64_t kOneLaunchChunks = 4 * kEpochBlocks;
 // tiles) leaves most units idle in the second; 1,000 chunks of 25 tiles ran
 // pass 1 0.185 -> 0.163 ms.
 constexpr int64_t kFillChunks = 1024;
+// ... and of a problem of at most kFillChunks tiles: one chunk per compute
+// unit.  One block per unit with several tiles beat two or more blocks of
+// one tile each at every size tried: the tiny bucket's step 0.057 -> 0.049
+// ms, 2M elements at W = 4 0.074 -> 0.054 ms, 500K at W = 16 0.081 -> 0.055
+// ms, 200K at W = 255 0.394 -> 0.315 ms (fewer slots also spare the
+// decision its second level).
+constexpr int64_t kSmallFillChunks = 256;
 inline int64_t one_launch_epoch(int64_t total_chunks) {
   return total_chunks <= kOneLaunchChunks ? (total_chunks > 0 ? total_chunks : 1) : kEpochBlocks;
 }
@@ -168,12 +175,14 @@ inline Geometry geometry_core(int W) {
 
 // A problem of fewer than kFillChunks chunks would leave compute units
 // idle: it takes the smallest G that keeps it within kFillChunks chunks (so
-// within one launch).  total_for(G): the problem's chunks at G tiles each.
+// within one launch), or within kSmallFillChunks when it has at most
+// kFillChunks tiles.  total_for(G): the problem's chunks at G tiles each.
 template <typename F>
 inline void fill_rule(Geometry& g, F total_for) {
-  if (total_for(g.G) < kFillChunks)
+  const int64_t target = total_for(1) <= kFillChunks ? kSmallFillChunks : kFillChunks;
+  if (total_for(g.G) < target)
     for (int G = 1; G < g.G; ++G)
-      if (total_for(G) <= kFillChunks) {
+      if (total_for(G) <= target) {
         g.G = G;
         break;
       }

@@ -312,9 +312,13 @@ def test_pass1_chunk_geometry():
     assert nf.nf_pass1_chunk_elems(65, 6_553_600 * 2, 6_553_600) == (7_936, 826)
     assert nf.nf_pass1_launches(255, 6_553_600 * 2, 6_553_600) == 4 * 13  # 3,200 chunks, 256 per launch
     assert nf.nf_pass1_launches(65, 6_553_600 * 2, 6_553_600) == 2 * 7
-    # a small problem takes shorter chunks to fill the chip (at most 1,024 chunks)
-    e, c = nf.nf_pass1_chunk_elems(4, 1 << 20, 1 << 20)
-    assert c <= 1024 and e * c >= 1 << 20 and e % 64 == 0
+    # a problem of fewer than 1,024 chunks takes shorter ones to fill the chip
+    # (at most 1,024 chunks); one of at most 1,024 tiles takes one chunk per
+    # compute unit (at most 256, whole tiles)
+    for W, n, most in ((4, 1 << 20, 256), (16, 500_000, 256), (64, 200_000, 256), (255, 250_000, 256),
+                       (4, 4_000_000, 1024), (16, 8_000_000, 1024), (64, 1_000_000, 1024)):
+        e, c = nf.nf_pass1_chunk_elems(W, n, n)
+        assert most // 2 < c <= most and e * c >= n and e % 64 == 0, (W, n, e, c)
     assert nf.nf_pass1_chunk_elems(0, 100, 100) == (0, 0)
     assert nf.nf_pass1_chunk_elems(16, 0, 100) == (0, 0)
 
