@@ -8,7 +8,11 @@ fallback), for all W stacked workers.  Inputs are generated on the device
 before the timed region and stay resident in HBM.
 
 Metric: FP32-equivalent input GB/s = 4 * W * n_total / step time, and its
-fraction of the 8 TB/s HBM peak.  The JSON line also carries
+fraction of the 8 TB/s HBM peak, over the timed steps, which record four
+HIP events each for the phase split.  The JSON line also carries
+  without_phase_events  the same number of steps timed again without those
+                events (their records cost a few microseconds per step,
+                which shows only on the small workloads)
   roofline      the dominant kernel (pass 1): algorithmic bytes per launch
                 over its average launch time, from HIP events the library
                 records on its own launch stream; `traffic` is the counter-
@@ -551,6 +555,17 @@ class Workload:
         nf.nf_set_phase_events()
         del scrub
         ms_per_step = (t1 - t0) * 1e3 / steps
+        # The same steps again without the four phase events per step: each
+        # event record costs a few microseconds on the stream, which shows on
+        # the small workloads (about 13 us of the 1M-element bucket's step).
+        plain_ms = None
+        if not cold:
+            torch.cuda.synchronize()
+            p0 = time.perf_counter()
+            for k in range(steps):
+                self.step(pol, counts)
+            torch.cuda.synchronize()
+            plain_ms = (time.perf_counter() - p0) * 1e3 / steps
         ph = np.array([[hip.elapsed_ms(e[0], e[1]), hip.elapsed_ms(e[1], e[2]), hip.elapsed_ms(e[2], e[3]),
                         hip.elapsed_ms(e[0], e[3])] for e in evs])
         for e in evs:
@@ -578,15 +593,21 @@ class Workload:
                     nf.nf_pass1_launches_table(W, self.off, sign_words=not ternary))
         # a cold run's wall clock includes the overwrites: its value comes from the device events
         value = self.lay.input_bytes() / ((device_ms if cold else ms_per_step) * 1e-3) / 1e9
+        plain_value = None if plain_ms is None else self.lay.input_bytes() / (plain_ms * 1e-3) / 1e9
         achieved = pass1_bytes / (pass1_ms * 1e-3) / 1e9
         print(f"[bench] {self.lay.name} {'ternary' if ternary else 'binary'}"
               f"{' forced' if pol.force_lowbit else ''}{' cold' if cold else ''}"
               f"{'' if self.bn else ' DDP buckets'}: {steps} steps, "
               f"{ms_per_step:.4f} ms/step wall, device {device_ms:.4f} (pass1 {pass1_ms:.4f}, decide "
-              f"{decide_ms:.4f}, pass2 {pass2_ms:.4f}), {value:.1f} GB/s", file=sys.stderr, flush=True)
+              f"{decide_ms:.4f}, pass2 {pass2_ms:.4f}), {value:.1f} GB/s"
+              + ("" if plain_ms is None else f"; without phase events {plain_ms:.4f} ms/step, {plain_value:.1f} GB/s"),
+              file=sys.stderr, flush=True)
         return {
             "steps": steps, "warmup": warmup, "ms_per_step": round(ms_per_step, 4),
             "value": round(value, 2), "pct_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
+            "without_phase_events": None if plain_ms is None else {
+                "ms_per_step": round(plain_ms, 4), "value": round(plain_value, 2),
+                "pct_hbm_peak": round(100 * plain_value / HBM_PEAK_GBS, 2)},
             "device_ms": {"mean": round(device_ms, 4), "median": round(dev_med, 4), "min": round(dev_min, 4)},
             "phases_ms": {"pass1": round(pass1_ms, 4), "decide": round(decide_ms, 4),
                           "pass2": round(pass2_ms, 4), "device_total": round(device_ms, 4),
@@ -813,6 +834,7 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "pct_hbm_peak": m["pct_hbm_peak"],
+        "without_phase_events": m["without_phase_events"],
         "config": {"workload": wl.lay.name, "W": wl.W, "n_total": wl.n, **wl.buckets_desc(),
                    "eligible_frac": m["eligible_frac"],
                    "policy": "forced low-bit" if args.force_lowbit else "admitted, guard ok",
@@ -845,8 +867,8 @@ def config_record(wl, m, pol, cold, cpu, counters):
            "policy": "forced low-bit" if pol.force_lowbit else "admitted, guard ok",
            "caches": "cold (1 GiB overwritten before each step)" if cold else "warm",
            "input_gb": round(wl.lay.input_bytes() / 1e9, 4)}
-    row.update({k: m[k] for k in ("value", "pct_hbm_peak", "ms_per_step", "steps", "device_ms", "phases_ms",
-                                  "routes", "mgtr")})
+    row.update({k: m[k] for k in ("value", "pct_hbm_peak", "ms_per_step", "without_phase_events", "steps",
+                                  "device_ms", "phases_ms", "routes", "mgtr")})
     row["unit"] = "GB/s"
     roof = dict(m["pass1"])
     roof["traffic"] = pass1_traffic(counters)
