@@ -611,8 +611,9 @@ nf_status nf_set_phase_events(void* before_pass1, void* after_pass1, void* after
 /*
  * Profiling query (no paper counterpart): the number of pass-1 kernel
  * launches that one nf_route_buckets call with these sizes makes (pass 1
- * runs in launches of a fixed number of element chunks, and above 64
- * workers once per group of 64 worker rows).  sign_words = 1
+ * runs as one launch for a problem of at most 4,096 element chunks, else in
+ * launches of a fixed number of chunks, and above 32 workers once per row
+ * group).  sign_words = 1
  * for a pass 1 that packs sign words (G-Binary), 0 for one that does not
  * (G-Ternary's first pass, nf_bucket_health), which runs in bigger
  * launches.  0 for n_total = 0 or invalid sizes.  Pure host function.

@@ -73,10 +73,14 @@ constexpr int kEpochBlocks = NF_EPOCH_BLOCKS;  // chunks per pass-1 launch
 constexpr int64_t kEpochNoPack = NF_EPOCH_NOPACK;
 constexpr int kMaxG = NF_MAX_G;                // tiles per chunk at most
 static_assert(kMaxG <= 32, "pass 1 keeps a bit per tile of a chunk in 32 bits");
-// Small problems (at most 4 epochs of chunks) run as one launch: their few
-// stores cost less than the launch tails (measured on the 0.82 GB
-// ResNet-50-scale workload: pass 1 0.28 -> 0.19 ms).
-constexpr int64_t kOneLaunchChunks = 4 * kEpochBlocks;
+// Problems of at most 16 epochs of chunks (about 4 GiB of gradients) run as
+// one launch: their stores cost less than the launch tails.  Measured: the
+// 0.82 GB ResNet-50-scale workload's pass 1 0.28 -> 0.19 ms (up to 4
+// epochs); up to 16 epochs, 30M elements at W = 32 (3,663 chunks) 0.946 ->
+// 0.859 ms a step, 20M at W = 16 0.341 -> 0.317 ms, G-Ternary at W = 255
+// 5.43 -> 5.29 ms.  ViT-B/16 scale (5,284 chunks) ran 2% slower as one
+// launch, so larger problems keep launches of kEpochBlocks.
+constexpr int64_t kOneLaunchChunks = 16 * kEpochBlocks;
 // Chunks of a small problem: two rounds of two 16-wavefront blocks per
 // compute unit.  One round and a part (ResNet-50 scale: 782 chunks of 32
 // tiles) leaves most units idle in the second; 1,000 chunks of 25 tiles ran

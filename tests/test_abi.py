@@ -310,8 +310,12 @@ def test_pass1_chunk_geometry():
     # elements, 31 per chunk)
     assert nf.nf_pass1_chunk_elems(255, 6_553_600 * 2, 6_553_600) == (4_096, 1_600)
     assert nf.nf_pass1_chunk_elems(65, 6_553_600 * 2, 6_553_600) == (7_936, 826)
-    assert nf.nf_pass1_launches(255, 6_553_600 * 2, 6_553_600) == 4 * 13  # 3,200 chunks, 256 per launch
-    assert nf.nf_pass1_launches(65, 6_553_600 * 2, 6_553_600) == 2 * 7
+    assert nf.nf_pass1_launches(255, 6_553_600 * 2, 6_553_600) == 4  # 3,200 chunks: one launch per group
+    assert nf.nf_pass1_launches(65, 6_553_600 * 2, 6_553_600) == 2
+    # above 4,096 chunks, launches of 256 (1,024 without sign words)
+    assert nf.nf_pass1_launches(16, 70_000_000, 30_000_000) == 17  # 4,275 chunks
+    assert nf.nf_pass1_launches(16, 70_000_000, 30_000_000, sign_words=False) == 5
+    assert nf.nf_pass1_launches(16, 60_000_000, 30_000_000) == 1  # 3,664 chunks
     # a problem of fewer than 1,024 chunks takes shorter ones to fill the chip
     # (at most 1,024 chunks); one of at most 1,024 tiles takes one chunk per
     # compute unit (at most 256, whole tiles)

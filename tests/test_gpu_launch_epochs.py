@@ -1,8 +1,9 @@
-"""Pass-1 launch shapes against the oracle: a bucket small enough for one
-launch, buckets of more than 512 chunks (64 above 32 workers: their
-per-chunk partials are summed in groups before the decision), in one launch and in several launches that
-may overlap, and a flat buffer of several buckets in one launch.  Every
-output of every bucket is checked (G-Binary and G-Ternary)."""
+"""Pass-1 launch shapes against the oracle: problems of at most 4,096
+chunks in one launch, larger ones in launches of 256 chunks (1,024 without
+sign words) that may overlap, buckets of more than 512 chunks (64 above 32
+workers: their per-chunk partials are summed in groups before the
+decision), and flat buffers of several buckets.  Every output of every
+bucket is checked (G-Binary and G-Ternary)."""
 import numpy as np
 import pytest
 import torch
@@ -51,8 +52,10 @@ def run_binary(W, n, bucket_n, seed):
 @pytest.mark.parametrize("W,n,bucket_n,launches,launches_nosigns", [
     (16, 8_300_000, 8_300_000, 1, 1),      # a small problem: 1,014 chunks of 16 tiles, groups of 2 partials
     (16, 9_000_000, 9_000_000, 1, 1),      # 977 chunks of 18 tiles
-    (16, 20_000_000, 20_000_000, 5, 2),    # 1,221 chunks of 32 tiles: five launches, groups of 3
-    (16, 20_000_000, 9_000_000, 5, 2),     # three buckets, the last of 123 chunks
+    (16, 20_000_000, 20_000_000, 1, 1),    # 1,221 chunks of 32 tiles in one launch, groups of 3
+    (16, 20_000_000, 9_000_000, 1, 1),     # three buckets, the last of 123 chunks
+    (16, 70_000_000, 30_000_000, 17, 5),   # 4,275 chunks in three buckets: launches of 256 that may
+                                           # overlap (1,024 without sign words), groups of 4
     (64, 3_000_000, 3_000_000, 2, 2),      # 977 chunks, two row groups of 32 (a launch each)
     (255, 600_000, 600_000, 4, 4),         # 782 chunks, one launch per group of 64 worker rows;
                                            # partials summed in groups of 13 (at most 64 per worker)
@@ -77,13 +80,14 @@ def test_ternary_single_launch_flat():
 
 
 def test_ternary_multi_launch():
-    # 1,221 chunks: pass 1 without sign words in two launches (1,024 chunks
-    # each at most), the plane pack in five
-    W, n = 16, 20_000_000
-    assert nf.nf_pass1_launches(W, n, n, sign_words=False) == 2
+    # 4,273 chunks: pass 1 without sign words in five launches (1,024 chunks
+    # each at most), the plane pack in seventeen (256 at most)
+    W, n = 16, 70_000_000
+    assert nf.nf_pass1_launches(W, n, n, sign_words=False) == 5
+    assert nf.nf_pass1_launches(W, n, n) == 17
     lay = synth.small(W, n, 77, elig_frac=0.85, nruns=9)
     g = synth.generate_host(lay)
     mask = nfo.mask_from_segments(*synth.mask_segments(lay), n)
     pol = nf.policy(format=nf.NF_FORMAT_TERNARY, tau=0.5)
     res = ternary_route(g, mask, n, pol, bucket_n=n)
-    check_ternary_bucket(res, g, mask, n, pol, 0, n, "ternary 1,221 chunks")
+    check_ternary_bucket(res, g, mask, n, pol, 0, n, "ternary 4,273 chunks")
