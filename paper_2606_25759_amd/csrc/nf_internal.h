@@ -35,9 +35,10 @@ namespace nf {
 //
 // Work is cut into chunks of G consecutive tiles of one bucket; a block
 // takes one chunk and keeps the chunk's sign words in LDS until it ends.
-// Pass 1 runs as a sequence of launches of kEpochBlocks chunks each, so the
-// bitmap stores of a launch reach memory together at its end rather than
-// spread thinly through the gradient read stream.  Measured on MI355X:
+// Above kOneLaunchChunks chunks (below), pass 1 runs as a sequence of
+// launches of kEpochBlocks chunks each, so the bitmap stores of a launch
+// reach memory together at its end rather than spread thinly through the
+// gradient read stream.  Measured on MI355X:
 // writes mixed into a streaming read cost far more than their own bytes (a
 // 1/32 share of writes slows a plain 84 GB read by 35-45%); spread-out
 // stores cost about 40% of the scan's time, launch-end bursts about 15-20%.
