@@ -3,12 +3,16 @@
 compaction, per-slice scales from pass 1's chunk partials, and the count +
 decode from the compacted rows (every eligible tensor is one slice).
 
-Every slice's sums and scale are checked against the two-pass statistics on
-the GPU, and their total against pass 1's bucket sums.  Sampled slices (the
-first, two in the middle and the last) are checked in full against the
-oracle: sums and scale, the compacted words that lie inside them, their
-compacted-order counts and their decoded values.  Sampled positions outside
-every slice must be untouched."""
+Nothing is sampled.  Every slice's sums and scale are checked against the
+two-pass statistics on the GPU, and their total against pass 1's bucket
+sums.  Every slice is then checked against the oracle, in a pool of host
+threads (its calls release the interpreter lock): sums and scale, the
+compacted words that lie inside it, its compacted-order counts and its
+decoded values; every compacted word that straddles two slices is checked
+from both slices' signs; and every position outside the slices must be
+untouched."""
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 import pytest
 import torch
@@ -16,7 +20,7 @@ import torch
 import oracle as nfo
 import paper_2606_25759_amd as nf
 import synth
-from tests.nfgpu import same_f32
+from tests.nfgpu import POOL, same_f32
 
 pytestmark = pytest.mark.gpu
 
@@ -61,15 +65,16 @@ def test_fullsize_sliced_gpt1p3b():
     assert np.allclose(s1.sum(axis=0), st["sum_abs_elig"], rtol=1e-12, atol=0), "slices add up to the bucket"
 
     q = nfo.decode_table(W)
-    for s in sorted({0, sl.S // 3, 2 * sl.S // 3, sl.S - 1}):
+    ones = lambda k: np.full(k, np.uint64(0xFFFFFFFFFFFFFFFF))
+
+    def check_slice(s):
         o, L, r0 = int(soff[s]), int(sln[s]), int(sl.rstart[s])
         tag = f"slice {s} ({L:,} elements at {o:,})"
-        print(f"[fullsize sliced] {tag}", flush=True)
         gh = g[:, o:o + L].contiguous().cpu().numpy()
         ref_sums, ref_sc = nfo.slice_scales(gh, np.zeros(1, np.int64), np.array([L], np.int64))
         assert np.allclose(s1[s], ref_sums[0], rtol=1e-12, atol=0), f"{tag} sums"
         assert abs(sc[s] - ref_sc[0]) <= 1e-6 * abs(ref_sc[0]), f"{tag} scale"
-        full = np.full((L + 63) // 64, np.uint64(0xFFFFFFFFFFFFFFFF))
+        full = ones((L + 63) // 64)
         if L % 64:
             full[-1] = np.uint64((1 << (L % 64)) - 1)
         sbits = nfo.pack(gh, full)  # the slice's signs, in rank order
@@ -78,17 +83,43 @@ def test_fullsize_sliced_gpt1p3b():
         oa, ob = -(-r0 // 64), (r0 + L) // 64
         if ob > oa:
             sub = np.ascontiguousarray(gh[:, 64 * oa - r0:64 * ob - r0])
-            want_w = nfo.pack(sub, np.full(ob - oa, np.uint64(0xFFFFFFFFFFFFFFFF)))
+            want_w = nfo.pack(sub, ones(ob - oa))
             assert np.array_equal(cbits[:, oa:ob].cpu().numpy().view(np.uint64), want_w), f"{tag} compacted words"
         assert np.array_equal(counts_c[r0:r0 + L].cpu().numpy(), want_c), f"{tag} compacted-order counts"
         assert same_f32(out[o:o + L].cpu().numpy(), np.float32(sc[s]) * q[want_c]), f"{tag} decoded values"
-        del gh, sbits
+        return L
 
-    # positions outside every slice: untouched
-    rng = np.random.default_rng(5)
-    pos = rng.integers(0, n, 200_000)
-    words = sl.mask[pos // 64]
-    outside = pos[((words >> (pos % 64).astype(np.uint64)) & np.uint64(1)) == 0]
-    assert outside.size > 1000
-    idx = torch.from_numpy(outside).to(d)
-    assert torch.isnan(out[idx]).all().item(), "positions outside the slices written"
+    def check_straddle(s):
+        """The compacted word holding the last ranks of slice s: shared with the
+        first ranks of the next slice, or (after the last slice) the payload's
+        last, zero-padded word.  Every slice is far longer than 64 elements."""
+        r_end = int(sl.rstart[s]) + int(sln[s])
+        if r_end % 64 == 0:
+            return 0
+        w0 = r_end // 64
+        o, L = int(soff[s]), int(sln[s])
+        tail = g[:, o + L - (r_end - 64 * w0):o + L]
+        k = min(64 * w0 + 64, sl.n_eligible) - r_end
+        if k > 0:
+            o2 = int(soff[s + 1])
+            assert k <= int(sln[s + 1]), "a word spans three slices"
+            both = torch.cat([tail, g[:, o2:o2 + k]], dim=1).contiguous().cpu().numpy()
+        else:
+            both = tail.contiguous().cpu().numpy()
+        m = ones(1)
+        if both.shape[1] < 64:
+            m[0] = np.uint64((1 << both.shape[1]) - 1)
+        want = nfo.pack(both, m)
+        assert np.array_equal(cbits[:, w0:w0 + 1].cpu().numpy().view(np.uint64), want), f"word {w0} after slice {s}"
+        return 1
+
+    with ThreadPoolExecutor(POOL) as ex:
+        assert sum(ex.map(check_slice, range(sl.S))) == sl.n_eligible
+        straddles = sum(ex.map(check_straddle, range(sl.S)))
+    print(f"[fullsize sliced] {sl.S} slices and {straddles} straddling words checked", flush=True)
+
+    # every position outside the slices: untouched
+    elig = np.unpackbits(sl.mask.view(np.uint8), bitorder="little")[:n].astype(bool)
+    assert int(elig.sum()) == sl.n_eligible
+    oh = out.cpu().numpy()
+    assert np.isnan(oh[~elig]).all(), "positions outside the slices written"
