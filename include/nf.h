@@ -413,8 +413,10 @@ nf_status nf_route_bucket(const float* grads, int64_t worker_stride, int32_t W, 
                           void* ws, size_t ws_bytes, void* stream);
 
 /*
- * Many buckets of one flat gradient buffer in three launches (DDP cuts a
- * model's flat gradient into fixed-capacity buckets, §2.1).  Bucket b covers
+ * Many buckets of one flat gradient buffer in one call: pass 1 over all of
+ * them, every bucket's decision, then pass 2, each phase a few launches on
+ * `stream` (DDP cuts a model's flat gradient into fixed-capacity buckets,
+ * §2.1).  Bucket b covers
  * elements [b*bucket_n, min((b+1)*bucket_n, n_total)) of every worker row,
  * of the mask, of the bitmap rows (from word b*bucket_n/64), of counts and of
  * out; nb = ceil(n_total / bucket_n).  bucket_n must be a multiple of 64
